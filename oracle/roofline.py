@@ -1,0 +1,124 @@
+"""Attention-aware roofline latency model and the CU-split choice, in plain Python doubles.
+
+TEST INFRASTRUCTURE ONLY: the checker for the library's host-side predictor and optimiser.
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may use it.  It shares
+no code with the C++ implementation.
+
+Paper, Section 4.1 ("Sequence-Level Operators", "Overall Estimation"):
+  F_attn/req(q, c) = 4 h_q q (q + c) d_h + 2 h_q q (q + c)           FLOPs
+  B_attn/req(q, c) = 2 h_q q d_h b + 2 h_kv (q + c) d_h b               bytes
+  t_attn = sum over requests of max(F / Pi, B / B_HBM)
+  t_total = L * t_block, restricted here to the attention term of each of the L layers.
+Paper, Section 4.2 and Algorithm 1:
+  aggregated if t_mixed(S) <= tau; otherwise for each decode share S_d with t_d(S_d) <= tau,
+  S_p = S - S_d, k in (floor(t_p / t_d), floor(t_p / t_d) + 1) and
+  rho = (k T_decode + T_prefill) / max(k t_d, t_p); keep the first strictly larger rho.
+
+Readings where the paper is silent (each also listed in the design notes):
+  * CU shares are multiples of 8 (one CU per XCD), S_d runs 8, 16, ..., S - 8.
+  * k = 0 is dropped: decode must make progress.
+  * No feasible S_d: fall back to aggregated execution and flag SLO_INFEASIBLE.
+  * T_decode = number of decode requests; T_prefill = sum of the prefill requests' q.
+  * b = 2 bytes for bf16, 4 for fp32; times in seconds here, microseconds at the C boundary.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+TOTAL_CUS = 256
+CU_STEP = 8
+NOMINAL_BF16_FLOPS = 2.5e15      # dense bf16 MFMA peak, FLOP/s
+NOMINAL_HBM_BYTES = 8.0e12       # HBM3E bandwidth, B/s
+
+AGG, SPLIT = 0, 1
+SLO_INFEASIBLE = 1
+
+
+def attn_flops(q: int, c: int, h_q: int, d_h: int) -> float:
+    """F_attn/req: the QK^T and PV products over the q x (q + c) score block, plus softmax and scaling."""
+    return 4.0 * h_q * q * (q + c) * d_h + 2.0 * h_q * q * (q + c)
+
+
+def attn_bytes(q: int, c: int, h_q: int, h_kv: int, d_h: int, b: int) -> float:
+    """B_attn/req: query read and output write, plus the key and value reads of all q + c tokens."""
+    return 2.0 * h_q * q * d_h * b + 2.0 * h_kv * (q + c) * d_h * b
+
+
+@dataclass
+class Tables:
+    """Achievable compute (FLOP/s) and HBM bandwidth (B/s) as functions of the CU count."""
+    flops: dict
+    bw: dict
+
+    def pi(self, s: int) -> float:
+        return self.flops[s]
+
+    def b(self, s: int) -> float:
+        return self.bw[s]
+
+
+def nominal_tables() -> Tables:
+    cus = range(CU_STEP, TOTAL_CUS + 1, CU_STEP)
+    return Tables({s: NOMINAL_BF16_FLOPS * s / TOTAL_CUS for s in cus},
+                  {s: NOMINAL_HBM_BYTES * s / TOTAL_CUS for s in cus})
+
+
+def t_attn(reqs, s: int, tables: Tables, h_q: int, h_kv: int, d_h: int, b: int) -> float:
+    """Seconds for one layer's attention of the requests [(q, c), ...] on s CUs."""
+    pi, bw = tables.pi(s), tables.b(s)
+    return sum(max(attn_flops(q, c, h_q, d_h) / pi, attn_bytes(q, c, h_q, h_kv, d_h, b) / bw)
+               for q, c in reqs)
+
+
+def f_roofline(reqs, s, tables, *, h_q, h_kv, d_h, b, layers) -> float:
+    """Seconds for the attention of all `layers` layers (t_total = L t_block, attention only)."""
+    return layers * t_attn(reqs, s, tables, h_q, h_kv, d_h, b)
+
+
+def split_requests(batch):
+    """batch: [(kind, q, c), ...] with kind 0 = prefill, 1 = decode."""
+    pre = [(q, c) for k, q, c in batch if k == 0]
+    dec = [(q, c) for k, q, c in batch if k == 1]
+    return pre, dec
+
+
+def predict(batch, mode, s_p, s_d, k, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS) -> float:
+    """Predicted iteration latency in seconds: aggregated on all CUs, or max(k t_d(S_d), t_p(S_p))."""
+    kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
+    if mode == AGG:
+        return f_roofline([(q, c) for _, q, c in batch], total, tables, **kw)
+    pre, dec = split_requests(batch)
+    t_d = f_roofline(dec, s_d, tables, **kw) if dec else 0.0
+    t_p = f_roofline(pre, s_p, tables, **kw) if pre else 0.0
+    return max(k * t_d, t_p)
+
+
+def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP):
+    """Algorithm 1.  Returns dict(mode, s_p, s_d, k, rho, t, flags)."""
+    kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
+    mixed = [(q, c) for _, q, c in batch]
+    t_mixed = f_roofline(mixed, total, tables, **kw)
+    if t_mixed <= tau:
+        return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=0)
+    pre, dec = split_requests(batch)
+    t_decode_tokens = len(dec)
+    t_prefill_tokens = sum(q for q, _ in pre)
+    best_rho, best = 0.0, None
+    for s_d in range(step, total, step):
+        t_d = f_roofline(dec, s_d, tables, **kw)
+        if t_d > tau:
+            continue
+        s_p = total - s_d
+        t_p = f_roofline(pre, s_p, tables, **kw)
+        base = math.floor(t_p / t_d) if t_d > 0 else 1
+        for k in (base, base + 1):
+            if k < 1:
+                continue
+            t = max(k * t_d, t_p)
+            rho = (k * t_decode_tokens + t_prefill_tokens) / t
+            if rho > best_rho:
+                best_rho, best = rho, dict(mode=SPLIT, s_p=s_p, s_d=s_d, k=k, rho=rho, t=t, flags=0)
+    if best is None:
+        return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=SLO_INFEASIBLE)
+    return best
