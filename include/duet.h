@@ -1,0 +1,225 @@
+/*
+ * duet.h -- C ABI of the mixed-batch paged-attention library for MI355X (gfx950).
+ *
+ * One serving iteration's attention over a paged KV cache, split the way the paper
+ * splits a mixed prefill/decode iteration (Section 4 overview, Algorithm 1):
+ *   - prefill requests (chunked prefill, possibly with a cached prefix) run a causal,
+ *     compute-bound attention on MFMA;
+ *   - decode requests (one new token each) run a bandwidth-bound split-K paged attention
+ *     followed by a small reduce kernel;
+ *   - the two halves either share the whole GPU on one stream (temporal sharing), or run
+ *     concurrently on two streams bound to disjoint CU sets (spatial sharing, Section 4.3).
+ * A host-side roofline latency model (Section 4.1) and the split optimiser of Section 4.2 /
+ * Algorithm 1 choose between the two.
+ *
+ * Conventions
+ *   - Every function returns DUET_OK (0) or a negative DUET_E* code; the message of the last
+ *     failure on the calling thread is returned by duet_last_error().  Argument checks run
+ *     before any GPU work is enqueued: a call that fails launches nothing.
+ *   - No C++ exception crosses this boundary.
+ *   - Device pointers are plain HIP device addresses.  The caller owns every tensor (q, caches,
+ *     page table, workspace, out); the library never allocates or frees caller memory.  It owns
+ *     its streams, events, pinned staging buffers and latency-model tables.
+ *   - GPU work is asynchronous to the host: it starts after the work already queued on the
+ *     caller's `stream` and completes before work queued there later.
+ *
+ * Tensor layouts (one layer)
+ *   q, out    [T, h_q, d]                 tokens of all requests, packed in seq_meta order
+ *   k_cache   [P, h_kv, page_size, d]     token-major pages
+ *   v_cache   [P, h_kv, d, page_size]     dim-major pages (each dim's page_size tokens contiguous)
+ *   page_table[R, max_pages] int32        logical page j of request r is physical page
+ *                                         page_table[r * max_pages + j]; token t of request r is
+ *                                         slot t % page_size of logical page t / page_size.
+ *   Element type is bf16 or fp32 (shape.dtype) for q, caches and out.  Accumulation is fp32.
+ *
+ * Attention semantics (Section 2 and Section 4.1): request r with q_len scheduled tokens and
+ * cached_len cached tokens has kv_len = cached_len + q_len keys, the new tokens' keys and values
+ * already written to the cache.  Query i sits at absolute position cached_len + i and attends
+ * keys 0 .. cached_len + i with weights softmax(q.k / sqrt(d)).  Query head h reads kv head
+ * h / (h_q / h_kv).
+ */
+#ifndef DUET_H
+#define DUET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------------------------ */
+#define DUET_OK 0
+#define DUET_EINVAL (-1)       /* bad argument: null pointer, size out of range, bad split */
+#define DUET_EUNSUPPORTED (-2) /* valid but unsupported: head_dim, page size, dtype, group size */
+#define DUET_EWORKSPACE (-3)   /* workspace smaller than duet_workspace_bytes() */
+#define DUET_EHIP (-4)         /* a HIP runtime call failed */
+#define DUET_ENOMEM (-5)       /* host or pinned allocation failed */
+#define DUET_EPAGE (-6)        /* a kernel met a page id outside [0, num_phys_pages) */
+#define DUET_EIO (-7)          /* latency-model file could not be read or written */
+
+/* ---- enums --------------------------------------------------------------------------------- */
+#define DUET_BF16 0
+#define DUET_F32 1
+
+#define DUET_KIND_PREFILL 0
+#define DUET_KIND_DECODE 1
+
+#define DUET_AGG 0   /* temporal sharing: both halves on the caller's stream, all CUs */
+#define DUET_SPLIT 1 /* spatial sharing: decode on cus_decode CUs, prefill on cus_prefill CUs */
+
+/* status_flags of duet_choose_cu_split (bit set) */
+#define DUET_STATUS_SLO_INFEASIBLE 1 /* no decode share meets the TBT bound; aggregated returned */
+#define DUET_STATUS_UNCALIBRATED 2   /* the model still holds the nominal MI355X peaks */
+
+#define DUET_TOTAL_CUS 256
+#define DUET_CU_STEP 8 /* CU shares are multiples of 8: one CU per XCD */
+
+/* ---- plain structs (same bytes on host and device) ------------------------------------------ */
+typedef struct {
+  int32_t num_q_heads;  /* h_q */
+  int32_t num_kv_heads; /* h_kv, divides h_q */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t page_size;    /* 16 */
+  int32_t dtype;        /* DUET_BF16 or DUET_F32 */
+  int32_t num_layers;   /* L of the latency model: t_total = L * t_attn (attention kernels run one layer) */
+} duet_shape;
+
+typedef struct {
+  int32_t kind;       /* DUET_KIND_PREFILL or DUET_KIND_DECODE (decode requires q_len == 1) */
+  int32_t q_start;    /* first row of this request in q / out */
+  int32_t q_len;      /* scheduled (new) tokens, >= 1 */
+  int32_t cached_len; /* tokens already in the cache before this iteration, >= 0 */
+} duet_seq_meta;
+
+typedef struct {
+  const duet_seq_meta* reqs; /* host array, num_reqs entries; row r uses page_table row r */
+  int32_t num_reqs;
+} duet_batch;
+
+typedef struct {
+  int32_t mode;           /* DUET_AGG or DUET_SPLIT */
+  int32_t cus_prefill;    /* S_p, multiple of 8 (SPLIT) */
+  int32_t cus_decode;     /* S_d, multiple of 8 (SPLIT), S_p + S_d <= 256 */
+  int32_t k_decode_steps; /* k of Section 4.2: decode steps planned per prefill step (>= 1) */
+} duet_cu_split;
+
+typedef struct {
+  /* Filled by duet_last_kernel_times() when profiling is on: durations of the last
+   * duet_attn_mixed_batch call, measured with HIP events on each kernel's own stream. */
+  double decode_partial_us; /* split-K paged decode kernel */
+  double decode_reduce_us;  /* partial merge kernel */
+  double prefill_us;        /* prefill attention kernel */
+  double decode_total_us;   /* decode stream: partial start to reduce end */
+  double iteration_us;      /* fork to join on the caller's stream */
+} duet_kernel_times;
+
+typedef struct duet_ctx duet_ctx;
+typedef struct duet_model duet_model;
+
+/* ---- latency model (host only; Section 4.1, 4.2, Algorithm 1) ----------------------------- */
+
+/* New model holding nominal MI355X tables: Pi(S) = 2.5 PFLOP/s * S/256 (dense bf16 MFMA),
+ * B(S) = 8 TB/s * S/256, for S = 8, 16, ..., 256.  The caller frees it with duet_model_destroy. */
+int duet_model_create(duet_model** out);
+int duet_model_destroy(duet_model* m);
+
+/* Replace the achievable-throughput tables (Section 4.2: profiled once per partition size).
+ * cus[i] must be the 32 values 8, 16, ..., 256 in order; flops_per_s and bytes_per_s > 0.
+ * Marks the model calibrated. */
+int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
+                          const double* bytes_per_s);
+int duet_model_get_tables(const duet_model* m, int32_t n, int32_t* cus, double* flops_per_s,
+                          double* bytes_per_s);
+/* Kernel efficiencies in (0, 1]: Pi is multiplied by prefill_eff and B by decode_eff before use.
+ * Calibrate them so decode latency is never under-predicted (appendix: under-prediction is the
+ * harmful direction). */
+int duet_model_set_efficiency(duet_model* m, double prefill_eff, double decode_eff);
+int duet_model_save(const duet_model* m, const char* path); /* small JSON file */
+int duet_model_load(duet_model* m, const char* path);
+
+/* Predicted latency (microseconds) of one iteration of shape->num_layers layers.
+ * AGG: L * sum_r max(F_r / Pi(256), B_r / B(256)) over all requests.
+ * SPLIT: max(k * t_d(S_d), t_p(S_p)) with t_X(S) = L * sum_{r in X} max(F_r / Pi(S), B_r / B(S)).
+ * F_r = 4 h_q q (q + c) d + 2 h_q q (q + c); B_r = 2 h_q q d b + 2 h_kv (q + c) d b.
+ * m may be NULL (nominal tables). */
+int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                              duet_cu_split split, double* us);
+
+/* Algorithm 1: aggregated if the whole-GPU prediction meets tbt_slo_us, else the (S_p, S_d, k)
+ * maximising (k T_decode + T_prefill) / max(k t_d, t_p) subject to t_d <= tbt_slo_us, with S_d in
+ * 8, 16, ..., 248 and k in {floor(t_p/t_d), floor(t_p/t_d) + 1} minus 0.  Ties keep the first
+ * (smallest S_d, then smaller k).  max_decode_steps > 0 caps k at the number of decode steps the
+ * caller can launch ahead (Section 4.3, look-ahead decode); <= 0 leaves k uncapped.  predicted_us,
+ * rho and status_flags may be NULL; rho is 0 for aggregated.  m may be NULL (nominal tables). */
+int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                         double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,
+                         double* predicted_us, double* rho, int32_t* status_flags);
+
+/* ---- GPU context ----------------------------------------------------------------------------- */
+
+/* Context on HIP device `device`: checks for gfx950 and 256 CUs, creates the CU-masked stream
+ * pool lazily (one stream per distinct CU set, kept for the context's lifetime), events and
+ * pinned staging buffers, and a latency model with nominal tables. */
+int duet_init(int device, duet_ctx** out);
+int duet_destroy(duet_ctx* ctx);
+/* The context's own latency model (owned by the context; valid until duet_destroy). */
+duet_model* duet_ctx_model(duet_ctx* ctx);
+
+/* Bytes of device workspace duet_attn_mixed_batch needs for this shape and batch: metadata,
+ * work lists, split-K partials and an error word.  Host only. */
+int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
+
+/* One iteration's attention.  q, k_cache, v_cache, page_table, workspace and out are device
+ * pointers.  max_pages_per_req is the row stride of page_table.  Prefill requests go to the
+ * MFMA prefill kernel, decode requests to the split-K decode kernel and its reduce kernel.
+ * AGG runs decode then prefill on `stream` (all CUs).  SPLIT forks onto two CU-masked streams
+ * (decode on the first cus_decode CUs, prefill on the last cus_prefill CUs), dispatching decode
+ * first, and joins back onto `stream`.  The result is bit-identical for every split and every
+ * placement of the pages: all reduction orders depend on logical token positions only.
+ * Page ids read by a kernel outside [0, num_phys_pages) are not dereferenced; they set an error
+ * word that duet_check_device_error() reports.  k_decode_steps is not used here (one step). */
+int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
+                          const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                          int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split,
+                          void* workspace, size_t workspace_bytes, void* out, void* stream);
+
+/* Synchronises `stream`, reads the workspace's error word and clears it: DUET_OK or DUET_EPAGE. */
+int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream);
+
+/* Copy request `req`'s logical keys (which == 0, from a token-major cache) or values (which == 1,
+ * from a dim-major cache) into out_contig [kv_len, h_kv, d] -- the page gather the attention
+ * kernels perform, exported so it can be checked bit for bit. */
+int duet_gather_kv(duet_ctx* ctx, const duet_shape* shape, int32_t which, const void* cache,
+                   int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
+                   int32_t req, int32_t kv_len, void* out_contig, void* stream);
+
+/* Profiling: when on, every duet_attn_mixed_batch call records HIP events around each kernel on
+ * the stream it runs on; duet_last_kernel_times() waits for them and returns the durations. */
+int duet_set_profiling(duet_ctx* ctx, int32_t enable);
+int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out);
+
+/* ---- calibration probes (Section 3 "Opportunity", Section 4.2 profiling) -------------------- */
+
+/* Streaming HBM read over `bytes` of device memory at `buf` on a stream restricted to `cus` CUs
+ * (256 = the unrestricted stream); repeated `iters` times.  Returns achieved bytes/s. */
+int duet_probe_read_bw(duet_ctx* ctx, int32_t cus, const void* buf, size_t bytes, int32_t iters,
+                       double* bytes_per_s);
+/* Register-resident bf16 MFMA loop on `cus` CUs.  Returns achieved FLOP/s. */
+int duet_probe_mfma(duet_ctx* ctx, int32_t cus, int32_t iters, double* flops_per_s);
+/* Record the hardware placement of `blocks` workgroups launched on the stream restricted to
+ * `cus` CUs taken from the low end (high_end == 0, the decode side) or the high end (1, the
+ * prefill side) of the CU bit order.  hw_ids_dev receives 2 uint32 per workgroup:
+ * (XCC_ID register, HW_ID register).  Synchronous. */
+int duet_probe_placement(duet_ctx* ctx, int32_t cus, int32_t high_end, int32_t blocks, uint32_t* hw_ids_dev);
+/* Fill `m` with Pi(S) and B(S) measured by the two probes for S = 8, 16, ..., 256, using
+ * scratch device memory of `scratch_bytes` at `scratch` for the read probe. */
+int duet_calibrate(duet_ctx* ctx, duet_model* m, const void* scratch, size_t scratch_bytes);
+
+/* Thread-local message of the last failure ("" if none). */
+const char* duet_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DUET_H */

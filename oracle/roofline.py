@@ -16,7 +16,7 @@ Paper, Section 4.2 and Algorithm 1:
 
 Readings where the paper is silent (each also listed in the design notes):
   * CU shares are multiples of 8 (one CU per XCD), S_d runs 8, 16, ..., S - 8.
-  * k = 0 is dropped: decode must make progress.
+  * k = 0 is dropped: decode must make progress; k may be capped by the look-ahead depth.
   * No feasible S_d: fall back to aggregated execution and flag SLO_INFEASIBLE.
   * T_decode = number of decode requests; T_prefill = sum of the prefill requests' q.
   * b = 2 bytes for bf16, 4 for fp32; times in seconds here, microseconds at the C boundary.
@@ -94,8 +94,9 @@ def predict(batch, mode, s_p, s_d, k, tables, *, h_q, h_kv, d_h, b, layers, tota
     return max(k * t_d, t_p)
 
 
-def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP):
-    """Algorithm 1.  Returns dict(mode, s_p, s_d, k, rho, t, flags)."""
+def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP, kmax=None):
+    """Algorithm 1.  Returns dict(mode, s_p, s_d, k, rho, t, flags).  kmax caps k at the number of
+    decode steps the engine can launch ahead (Section 4.3); None leaves it uncapped."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
     mixed = [(q, c) for _, q, c in batch]
     t_mixed = f_roofline(mixed, total, tables, **kw)
@@ -113,7 +114,7 @@ def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, st
         t_p = f_roofline(pre, s_p, tables, **kw)
         base = math.floor(t_p / t_d) if t_d > 0 else 1
         for k in (base, base + 1):
-            if k < 1:
+            if k < 1 or (kmax is not None and k > kmax):
                 continue
             t = max(k * t_d, t_p)
             rho = (k * t_decode_tokens + t_prefill_tokens) / t

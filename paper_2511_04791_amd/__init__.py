@@ -1,0 +1,282 @@
+"""Mixed-batch paged attention for MI355X: the iteration hot path of adaptive prefill/decode
+multiplexing (DuetServe, arXiv 2511.04791), as a C-ABI HIP library with a thin Python binding.
+
+    attn_mixed_batch(q, k_cache, v_cache, page_table, seq_meta, cu_split) -> out
+    predict_iter_latency(batch, cu_split, shape) -> microseconds
+    choose_cu_split(batch, tbt_slo_us, shape) -> (CuSplit, predicted_us, rho, flags)
+
+Every step of the path runs in libduet.so; this module only marshals arguments.  PyTorch
+supplies device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import _native as N
+from ._native import (AGG, BF16, CU_STEP, F32, KIND_DECODE, KIND_PREFILL, SPLIT, STATUS_SLO_INFEASIBLE,
+                      STATUS_UNCALIBRATED, TOTAL_CUS, DuetError)
+from .workloads import AttnShape
+
+__all__ = ["AGG", "SPLIT", "CuSplit", "Context", "Model", "DuetError", "attn_mixed_batch", "predict_iter_latency",
+           "choose_cu_split", "default_context", "AttnShape", "STATUS_SLO_INFEASIBLE", "STATUS_UNCALIBRATED"]
+
+
+@dataclass(frozen=True)
+class CuSplit:
+    mode: int = AGG
+    cus_prefill: int = TOTAL_CUS
+    cus_decode: int = 0
+    k_decode_steps: int = 1
+
+    @staticmethod
+    def agg() -> "CuSplit":
+        return CuSplit(AGG, TOTAL_CUS, 0, 1)
+
+    @staticmethod
+    def split(cus_prefill: int, cus_decode: int, k: int = 1) -> "CuSplit":
+        return CuSplit(SPLIT, cus_prefill, cus_decode, k)
+
+    def to_c(self) -> N.CuSplit:
+        return N.CuSplit(self.mode, self.cus_prefill, self.cus_decode, self.k_decode_steps)
+
+    def __str__(self):
+        return "AGG" if self.mode == AGG else f"SPLIT(Sp={self.cus_prefill},Sd={self.cus_decode},k={self.k_decode_steps})"
+
+
+def _shape_c(shape: AttnShape) -> N.Shape:
+    return N.Shape(shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.page_size,
+                   BF16 if shape.dtype == "bf16" else F32, shape.num_layers)
+
+
+def _meta_rows(seq_meta):
+    """Accepts an int array [R, 4] of (kind, q_start, q_len, cached_len) or a list of
+    (kind, q_len, cached_len) triples (q_start is then filled in order)."""
+    arr = np.asarray(seq_meta, dtype=np.int64)
+    if arr.ndim != 2 or arr.shape[1] not in (3, 4):
+        raise ValueError("seq_meta must be [R, 4] (kind, q_start, q_len, cached_len) or [R, 3] (kind, q_len, cached)")
+    if arr.shape[1] == 3:
+        starts = np.concatenate([[0], np.cumsum(arr[:, 1])[:-1]]) if len(arr) else np.zeros(0, np.int64)
+        arr = np.stack([arr[:, 0], starts, arr[:, 1], arr[:, 2]], axis=1)
+    return np.ascontiguousarray(arr.astype(np.int32))
+
+
+class _BatchC:
+    """Keeps the ctypes array alive alongside the struct that points into it."""
+
+    def __init__(self, seq_meta):
+        rows = _meta_rows(seq_meta)
+        self.rows = rows
+        self.arr = (N.SeqMeta * max(1, len(rows)))()
+        if len(rows):
+            ctypes.memmove(self.arr, rows.ctypes.data, rows.nbytes)
+        self.c = N.Batch(self.arr, len(rows))
+
+
+class Model:
+    """The host-side roofline latency model (owns a duet_model unless borrowed from a Context)."""
+
+    def __init__(self, handle=None, owner=None):
+        if handle is None:
+            h = ctypes.c_void_p()
+            N.check(N.lib().duet_model_create(ctypes.byref(h)), "duet_model_create")
+            handle, self._owned = h, True
+        else:
+            handle, self._owned = ctypes.c_void_p(handle), False
+        self.handle = handle
+        self._owner = owner
+
+    def __del__(self):
+        if getattr(self, "_owned", False) and self.handle:
+            N.lib().duet_model_destroy(self.handle)
+            self.handle = None
+
+    def set_tables(self, flops_per_s, bytes_per_s):
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus = (ctypes.c_int32 * n)(*range(N.CU_STEP, N.TOTAL_CUS + 1, N.CU_STEP))
+        fl = (ctypes.c_double * n)(*[float(x) for x in flops_per_s])
+        by = (ctypes.c_double * n)(*[float(x) for x in bytes_per_s])
+        N.check(N.lib().duet_model_set_tables(self.handle, n, cus, fl, by), "duet_model_set_tables")
+
+    def tables(self):
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus, fl, by = (ctypes.c_int32 * n)(), (ctypes.c_double * n)(), (ctypes.c_double * n)()
+        N.check(N.lib().duet_model_get_tables(self.handle, n, cus, fl, by), "duet_model_get_tables")
+        return list(cus), list(fl), list(by)
+
+    def set_efficiency(self, prefill_eff: float, decode_eff: float):
+        N.check(N.lib().duet_model_set_efficiency(self.handle, prefill_eff, decode_eff), "duet_model_set_efficiency")
+
+    def save(self, path: str):
+        N.check(N.lib().duet_model_save(self.handle, path.encode()), "duet_model_save")
+
+    def load(self, path: str):
+        N.check(N.lib().duet_model_load(self.handle, path.encode()), "duet_model_load")
+
+
+def predict_iter_latency(batch, cu_split: CuSplit, shape: AttnShape, model: Model | None = None) -> float:
+    """Predicted latency (us) of one iteration of shape.num_layers layers."""
+    b = _BatchC(batch)
+    us = ctypes.c_double()
+    N.check(N.lib().duet_predict_iter_latency(model.handle if model else None, ctypes.byref(_shape_c(shape)),
+                                              ctypes.byref(b.c), cu_split.to_c(), ctypes.byref(us)),
+            "duet_predict_iter_latency")
+    return us.value
+
+
+def choose_cu_split(batch, tbt_slo_us: float, shape: AttnShape, model: Model | None = None,
+                    max_decode_steps: int = 0):
+    """Algorithm 1: returns (CuSplit, predicted_us, rho, status_flags).  max_decode_steps > 0
+    caps k, the decode steps run per prefill step."""
+    b = _BatchC(batch)
+    out, us, rho, flags = N.CuSplit(), ctypes.c_double(), ctypes.c_double(), ctypes.c_int32()
+    N.check(N.lib().duet_choose_cu_split(model.handle if model else None, ctypes.byref(_shape_c(shape)),
+                                         ctypes.byref(b.c), float(tbt_slo_us), int(max_decode_steps),
+                                         ctypes.byref(out), ctypes.byref(us),
+                                         ctypes.byref(rho), ctypes.byref(flags)), "duet_choose_cu_split")
+    return CuSplit(out.mode, out.cus_prefill, out.cus_decode, out.k_decode_steps), us.value, rho.value, flags.value
+
+
+def workspace_bytes(shape: AttnShape, seq_meta) -> int:
+    b = _BatchC(seq_meta)
+    n = ctypes.c_size_t()
+    N.check(N.lib().duet_workspace_bytes(ctypes.byref(_shape_c(shape)), ctypes.byref(b.c), ctypes.byref(n)),
+            "duet_workspace_bytes")
+    return n.value
+
+
+def shape_of(q, k_cache, num_layers: int = 1) -> AttnShape:
+    import torch
+    if q.dtype == torch.bfloat16:
+        dt = "bf16"
+    elif q.dtype == torch.float32:
+        dt = "f32"
+    else:
+        raise TypeError(f"q dtype {q.dtype}: bf16 or float32 expected")
+    return AttnShape(int(q.shape[1]), int(k_cache.shape[1]), int(q.shape[2]), dt, int(k_cache.shape[2]), num_layers)
+
+
+class Context:
+    """A duet_ctx on one GPU: CU-masked stream pool, kernels, probes and its latency model."""
+
+    def __init__(self, device: int = 0):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible: the HIP library needs an MI355X")
+        self.device = device
+        h = ctypes.c_void_p()
+        N.check(N.lib().duet_init(device, ctypes.byref(h)), "duet_init")
+        self.handle = h
+        self.model = Model(N.lib().duet_ctx_model(h), owner=self)
+        self._ws = None
+
+    def close(self):
+        if self.handle:
+            N.lib().duet_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace(self, nbytes: int):
+        import torch
+        if self._ws is None or self._ws.numel() < nbytes:
+            self._ws = torch.empty(max(nbytes, 1 << 20), dtype=torch.uint8, device=f"cuda:{self.device}")
+        return self._ws
+
+    def attn_mixed_batch(self, q, k_cache, v_cache, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
+                         out=None, workspace=None, stream=None, num_layers: int = 1, check_errors: bool = False):
+        import torch
+        shape = shape_of(q, k_cache, num_layers)
+        for t, name in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (page_table, "page_table")):
+            if not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous device tensor")
+        if page_table.dtype != torch.int32:
+            raise TypeError("page_table must be int32")
+        if v_cache.shape != (k_cache.shape[0], k_cache.shape[1], k_cache.shape[3], k_cache.shape[2]):
+            raise ValueError("v_cache must be [P, h_kv, d, page_size] for k_cache [P, h_kv, page_size, d]")
+        b = _BatchC(seq_meta)
+        n_tok = int(b.rows[:, 2].sum()) if len(b.rows) else 0
+        if q.shape[0] != n_tok:
+            raise ValueError(f"q has {q.shape[0]} rows, the batch schedules {n_tok} tokens")
+        if page_table.dim() != 2 or page_table.shape[0] < len(b.rows):
+            raise ValueError("page_table must be [R, max_pages] with a row per request")
+        need = workspace_bytes(shape, b.rows)
+        ws = self.workspace(need) if workspace is None else workspace
+        if out is None:
+            out = torch.empty_like(q)
+        st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_attn_mixed_batch(self.handle, ctypes.byref(_shape_c(shape)), q.data_ptr(),
+                                              k_cache.data_ptr(), v_cache.data_ptr(), int(k_cache.shape[0]),
+                                              page_table.data_ptr(), int(page_table.shape[1]), ctypes.byref(b.c),
+                                              cu_split.to_c(), ws.data_ptr(), ws.numel(), out.data_ptr(),
+                                              ctypes.c_void_p(st)), "duet_attn_mixed_batch")
+        if check_errors:
+            N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
+                    "duet_check_device_error")
+        return out
+
+    def gather_kv(self, cache, which: int, page_table, req: int, kv_len: int, shape: AttnShape):
+        import torch
+        if not 0 <= req < page_table.shape[0]:
+            raise ValueError(f"request {req} outside the page table's {page_table.shape[0]} rows")
+        out = torch.empty(kv_len, shape.num_kv_heads, shape.head_dim, dtype=cache.dtype, device=cache.device)
+        st = torch.cuda.current_stream(cache.device).cuda_stream
+        N.check(N.lib().duet_gather_kv(self.handle, ctypes.byref(_shape_c(shape)), which, cache.data_ptr(),
+                                       int(cache.shape[0]), page_table.data_ptr(), int(page_table.shape[1]), req,
+                                       kv_len, out.data_ptr(), ctypes.c_void_p(st)), "duet_gather_kv")
+        return out
+
+    def set_profiling(self, on: bool):
+        N.check(N.lib().duet_set_profiling(self.handle, 1 if on else 0), "duet_set_profiling")
+
+    def last_kernel_times(self) -> dict:
+        t = N.KernelTimes()
+        N.check(N.lib().duet_last_kernel_times(self.handle, ctypes.byref(t)), "duet_last_kernel_times")
+        return {f: getattr(t, f) for f, _ in N.KernelTimes._fields_}
+
+    def probe_read_bw(self, cus: int, buf, iters: int = 3) -> float:
+        v = ctypes.c_double()
+        N.check(N.lib().duet_probe_read_bw(self.handle, cus, buf.data_ptr(), buf.numel() * buf.element_size(), iters,
+                                           ctypes.byref(v)), "duet_probe_read_bw")
+        return v.value
+
+    def probe_mfma(self, cus: int, iters: int = 2048) -> float:
+        v = ctypes.c_double()
+        N.check(N.lib().duet_probe_mfma(self.handle, cus, iters, ctypes.byref(v)), "duet_probe_mfma")
+        return v.value
+
+    def probe_placement(self, cus: int, high_end: bool, blocks: int):
+        import torch
+        out = torch.zeros(2 * blocks, dtype=torch.int32, device=f"cuda:{self.device}")
+        N.check(N.lib().duet_probe_placement(self.handle, cus, 1 if high_end else 0, blocks, out.data_ptr()),
+                "duet_probe_placement")
+        return out.cpu().numpy().astype(np.uint32).reshape(blocks, 2)
+
+    def calibrate(self, scratch=None) -> Model:
+        import torch
+        if scratch is None:
+            scratch = torch.empty(1 << 30, dtype=torch.uint8, device=f"cuda:{self.device}")
+        N.check(N.lib().duet_calibrate(self.handle, self.model.handle, scratch.data_ptr(), scratch.numel()),
+                "duet_calibrate")
+        return self.model
+
+
+_default = None
+
+
+def default_context() -> Context:
+    global _default
+    if _default is None:
+        _default = Context(0)
+    return _default
+
+
+def attn_mixed_batch(q, k_cache, v_cache, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), **kw):
+    """One iteration's attention on the default context; see Context.attn_mixed_batch."""
+    return default_context().attn_mixed_batch(q, k_cache, v_cache, page_table, seq_meta, cu_split, **kw)

@@ -1,0 +1,50 @@
+// Launch interface between the runtime and the HIP kernels (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace duet {
+
+// Per-iteration tensors and shape, common to every attention kernel.
+struct AttnArgs {
+  const void* q;         // [T, h_q, d]
+  const void* k_cache;   // [P, h_kv, 16, d]
+  const void* v_cache;   // [P, h_kv, d, 16]
+  const int32_t* page_table;
+  void* out;             // [T, h_q, d]
+  long long num_phys_pages;
+  int32_t max_pages;     // row stride of page_table
+  int32_t h_q, h_kv, group, head_dim, dtype;
+  float scale_log2;      // log2(e) / sqrt(d): scores are kept in base-2 units
+};
+
+// Work lists and scratch that live in the caller's workspace.
+struct WorkArgs {
+  const int4* meta;     // [R]  (kind, q_start, q_len, cached_len)
+  const int4* pitems;   // [NP] prefill tiles (req, q_head, q_row0, 0), heaviest first
+  const int4* dreq;     // [RD] decode requests (req, item_base, n_split, n_pages)
+  float* pacc;          // [ND, group, d]  unnormalised split-K partial outputs
+  float* pml;           // [ND, group, 2]  (running max in base-2 units, softmax denominator)
+  int32_t* err;         // error word: bit 0 = page id out of range
+  int32_t n_pitems, n_dreq, max_split;
+  int32_t pages_per_split;
+};
+
+constexpr int kPrefillRows = 128;  // query rows per prefill tile (4 waves x 32)
+constexpr int kPrefillKeys = 64;   // keys per LDS stage (4 pages)
+
+hipError_t launch_decode_partial(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
+hipError_t launch_decode_reduce(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
+hipError_t launch_prefill(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
+
+hipError_t launch_gather(const void* cache, int which, int elem_bytes, int h_kv, int d, const int32_t* page_table,
+                         int max_pages, long long num_phys, int req, int kv_len, void* out, int32_t* err,
+                         hipStream_t s);
+
+hipError_t launch_read_probe(const void* buf, size_t bytes, int blocks, unsigned* sink, hipStream_t s);
+hipError_t launch_mfma_probe(int blocks, int iters, float* sink, hipStream_t s);
+hipError_t launch_placement_probe(int blocks, uint32_t* out, hipStream_t s);
+
+}  // namespace duet

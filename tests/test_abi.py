@@ -1,0 +1,79 @@
+"""The C-ABI library loads and exports every function include/duet.h declares; host-side
+argument checks return the documented codes without touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2511_04791_amd import _native as N
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "duet.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(duet_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(native):
+    names = declared_functions()
+    assert len(names) >= 20
+    for name in names:
+        assert hasattr(native, name), name
+        assert name in N._SIGS, f"{name} missing from the Python binding"
+
+
+def _shape(**kw):
+    base = dict(num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16, dtype=N.BF16, num_layers=1)
+    base.update(kw)
+    return N.Shape(**base)
+
+
+def _batch(rows):
+    arr = (N.SeqMeta * len(rows))(*[N.SeqMeta(*r) for r in rows])
+    return arr, N.Batch(arr, len(rows))
+
+
+@pytest.mark.parametrize("kw,code", [(dict(head_dim=96), -2), (dict(page_size=32), -2), (dict(num_kv_heads=5), -2),
+                                     (dict(dtype=7), -2), (dict(num_q_heads=0), -1), (dict(num_layers=0), -1)])
+def test_shape_validation(native, kw, code):
+    arr, b = _batch([(0, 0, 16, 0)])
+    n = ctypes.c_size_t()
+    assert native.duet_workspace_bytes(ctypes.byref(_shape(**kw)), ctypes.byref(b), ctypes.byref(n)) == code
+    assert native.duet_last_error()
+
+
+@pytest.mark.parametrize("row", [(1, 0, 2, 5), (0, 0, 0, 5), (0, 0, 4, -1), (3, 0, 1, 1)])
+def test_batch_validation(native, row):
+    arr, b = _batch([row])
+    n = ctypes.c_size_t()
+    assert native.duet_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(b), ctypes.byref(n)) == -1
+
+
+def test_split_validation(native):
+    arr, b = _batch([(0, 0, 128, 0), (1, 128, 1, 100)])
+    us = ctypes.c_double()
+    for sp in [N.CuSplit(1, 100, 100, 1), N.CuSplit(1, 248, 16, 1), N.CuSplit(1, 128, 128, 0), N.CuSplit(5, 0, 0, 1),
+               N.CuSplit(1, 0, 256, 1)]:
+        assert native.duet_predict_iter_latency(None, ctypes.byref(_shape()), ctypes.byref(b), sp, ctypes.byref(us)) == -1
+    assert native.duet_predict_iter_latency(None, ctypes.byref(_shape()), ctypes.byref(b), N.CuSplit(1, 128, 128, 1),
+                                            ctypes.byref(us)) == 0
+
+
+def test_attn_rejects_null_context(native):
+    arr, b = _batch([(1, 0, 1, 10)])
+    rc = native.duet_attn_mixed_batch(None, ctypes.byref(_shape()), 1, 1, 1, 10, 1, 4, ctypes.byref(b),
+                                      N.CuSplit(0, 256, 0, 1), 1, 1 << 20, 1, None)
+    assert rc == -1 and b"ctx" in native.duet_last_error()
+
+
+def test_workspace_grows_with_decode_splits(native):
+    small_arr, small = _batch([(1, 0, 1, 100)])
+    big_arr, big = _batch([(1, 0, 1, 30000)])
+    a, c = ctypes.c_size_t(), ctypes.c_size_t()
+    assert native.duet_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(small), ctypes.byref(a)) == 0
+    assert native.duet_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(big), ctypes.byref(c)) == 0
+    # 30001 keys = 1876 pages = 118 splits of 16 pages; each split stores 4 heads x (128 + 2) floats per kv head
+    assert c.value - a.value >= (118 - 1) * 8 * 4 * 130 * 4

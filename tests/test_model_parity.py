@@ -1,0 +1,128 @@
+"""The library's host-side latency model and Algorithm 1 against the oracle (no GPU needed)."""
+import os
+
+import numpy as np
+import pytest
+
+import paper_2511_04791_amd as duet
+from oracle import roofline as orf
+from paper_2511_04791_amd import workloads as wl
+
+CUS = list(range(8, 257, 8))
+
+
+def _tables(rng):
+    pis = np.cumsum(rng.uniform(0.5, 1.5, 32)) * 1e13
+    bws = np.cumsum(rng.uniform(0.0, 2.0, 32) * np.linspace(2, 0.2, 32)) * 1e11 + 1e11
+    return pis, bws
+
+
+def _batch(rng):
+    rows = [(1, 1, int(rng.integers(16, 20000))) for _ in range(int(rng.integers(0, 96)))]
+    for _ in range(int(rng.integers(0, 3))):
+        rows.append((0, int(rng.integers(1, 8192)), int(rng.integers(0, 30000))))
+    if not rows:
+        rows = [(1, 1, 5)]
+    rng.shuffle(rows)
+    return rows
+
+
+def _kw(shape):
+    return dict(h_q=shape.num_q_heads, h_kv=shape.num_kv_heads, d_h=shape.head_dim, b=shape.elem_bytes,
+                layers=shape.num_layers)
+
+
+@pytest.mark.parametrize("shape", [wl.AttnShape(32, 8, 128, "bf16", num_layers=32), wl.AttnShape(4, 2, 64, "f32"),
+                                   wl.AttnShape(64, 8, 128, "bf16", num_layers=1)])
+def test_predict_matches_oracle(shape):
+    rng = np.random.default_rng(30)
+    for _ in range(40):
+        pis, bws = _tables(rng)
+        model = duet.Model()
+        model.set_tables(pis, bws)
+        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)))
+        rows = _batch(rng)
+        want = orf.predict(rows, orf.AGG, 256, 0, 1, tab, **_kw(shape))
+        got = duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape, model)
+        assert got == pytest.approx(want * 1e6, rel=1e-12)
+        sd = int(rng.integers(1, 31)) * 8
+        k = int(rng.integers(1, 9))
+        want = orf.predict(rows, orf.SPLIT, 256 - sd, sd, k, tab, **_kw(shape))
+        got = duet.predict_iter_latency(rows, duet.CuSplit.split(256 - sd, sd, k), shape, model)
+        assert got == pytest.approx(want * 1e6, rel=1e-12)
+
+
+def test_choose_matches_oracle():
+    rng = np.random.default_rng(31)
+    shape = wl.AttnShape(32, 8, 128, "bf16", num_layers=32)
+    n_split = 0
+    for _ in range(80):
+        pis, bws = _tables(rng)
+        model = duet.Model()
+        model.set_tables(pis, bws)
+        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)))
+        rows = _batch(rng)
+        t_mixed = orf.predict(rows, orf.AGG, 256, 0, 1, tab, **_kw(shape))
+        tau = t_mixed * float(rng.uniform(0.05, 1.2))
+        want = orf.choose(rows, tau, tab, **_kw(shape))
+        sp, us, rho, flags = duet.choose_cu_split(rows, tau * 1e6, shape, model)
+        assert sp.mode == want["mode"]
+        assert flags == want["flags"]
+        assert us == pytest.approx(want["t"] * 1e6, rel=1e-12)
+        if sp.mode == duet.SPLIT:
+            n_split += 1
+            assert (sp.cus_prefill, sp.cus_decode, sp.k_decode_steps) == (want["s_p"], want["s_d"], want["k"])
+            assert rho == pytest.approx(want["rho"], rel=1e-12)
+    assert n_split >= 15
+
+
+def test_null_model_is_nominal_and_flagged():
+    shape = wl.LLAMA3_8B
+    rows = [(0, 2048, 0)] + [(1, 1, 3000)] * 64
+    tab = orf.nominal_tables()
+    want = orf.predict(rows, orf.AGG, 256, 0, 1, tab, **_kw(shape))
+    assert duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape) == pytest.approx(want * 1e6, rel=1e-12)
+    sp, us, rho, flags = duet.choose_cu_split(rows, 1e9, shape)
+    assert sp.mode == duet.AGG and flags & duet.STATUS_UNCALIBRATED
+
+
+def test_efficiency_scales_prediction():
+    shape = wl.LLAMA3_8B
+    rows = [(1, 1, 3000)] * 16
+    m = duet.Model()
+    base = duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape, m)
+    m.set_efficiency(1.0, 0.5)
+    assert duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape, m) == pytest.approx(2 * base, rel=1e-12)
+    with pytest.raises(duet.DuetError):
+        m.set_efficiency(0.0, 1.0)
+
+
+def test_save_load_roundtrip(tmp_path):
+    rng = np.random.default_rng(32)
+    pis, bws = _tables(rng)
+    m = duet.Model()
+    m.set_tables(pis, bws)
+    m.set_efficiency(0.8, 0.6)
+    path = os.path.join(tmp_path, "model.json")
+    m.save(path)
+    m2 = duet.Model()
+    m2.load(path)
+    cus, fl, by = m2.tables()
+    assert cus == CUS and np.array_equal(fl, pis) and np.array_equal(by, bws)
+    rows = [(0, 100, 50), (1, 1, 999)]
+    sp = duet.CuSplit.split(128, 128, 2)
+    assert duet.predict_iter_latency(rows, sp, wl.LLAMA3_8B, m) == duet.predict_iter_latency(rows, sp, wl.LLAMA3_8B, m2)
+    with pytest.raises(duet.DuetError):
+        m2.load(os.path.join(tmp_path, "missing.json"))
+
+
+def test_choose_is_fast():
+    """The paper keeps scheduling and partition solving under 1 ms per iteration."""
+    import time
+    shape = wl.AttnShape(32, 8, 128, "bf16", num_layers=32)
+    rows = [(1, 1, 4000)] * 256 + [(0, 4096, 8192)]
+    duet.choose_cu_split(rows, 1000.0, shape)
+    t0 = time.perf_counter()
+    for _ in range(50):
+        duet.choose_cu_split(rows, 1000.0, shape)
+    assert (time.perf_counter() - t0) / 50 < 1e-3
