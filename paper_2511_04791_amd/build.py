@@ -19,6 +19,8 @@ ARCH = "gfx950"
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall",
              # no packed-fp32 instructions anywhere in the device code
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             # MFMA accumulators in VGPRs: the online-softmax rescale works on them in place
+             "-mllvm", "-amdgpu-mfma-vgpr-form",
              "-I" + INCLUDE, "-I" + CSRC]
 CXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I" + INCLUDE, "-I" + CSRC,
              "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__"]

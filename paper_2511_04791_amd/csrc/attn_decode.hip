@@ -7,17 +7,19 @@
 // (pages_per_split).  One wave owns one item and reads each page of its kv head once for all
 // query heads of the GQA group, so the bytes moved are the algorithmic K/V bytes.
 //
-// bf16 path, per pair of pages (32 tokens), on the 16x16x32 bf16 MFMA (fp32 accumulate):
-//   S^T [16 tokens x 16 heads] = K_page [16 x d] . Q^T [d x 16]     (one MFMA per 32 dims)
-//   O^T [16 dims x 16 heads]  += V^T   [16 x 32] . P^T [32 x 16]    (one MFMA per 16 dims)
+// bf16 path, per page (16 tokens), on MFMA with fp32 accumulate:
+//   S^T [16 tokens x 16 heads] = K_page [16 x d] . Q^T [d x 16]   (16x16x32, one per 32 dims)
+//   O^T [16 dims x 16 heads]  += V^T   [16 x 16] . P^T [16 x 16]  (16x16x16, one per 16 dims)
 // Heads beyond the group size are zero columns.  K is read token-major (16 B per lane, the
 // MFMA A layout); V pages are stored dim-major, so a lane's 4 consecutive tokens of one dim
-// are 8 contiguous bytes and P^T never leaves registers.  Online softmax keeps a running max
-// and denominator per head; partials (unnormalised output, max, denominator) go to the
-// workspace and the reduce kernel merges the splits.  All arithmetic order depends on logical
-// token positions only.
+// are 8 contiguous bytes and P^T never leaves registers.  Pages cycle through three register
+// buffers (the loop is unrolled by three), so two pages are in flight while one is computed.
+// Online softmax keeps a running max and denominator per head.  Partials (unnormalised
+// output, running max, denominator) go to the workspace and the reduce kernel merges the splits.
+// All arithmetic order depends on logical token positions only.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "kernels.h"
@@ -26,66 +28,61 @@ namespace duet {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// K/V pages are read exactly once per iteration.
+#ifdef DUET_DECODE_NT_LOADS
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ __forceinline__ T stream_load(const char* p) {
+  if constexpr (sizeof(T) == 16)
+    return __builtin_bit_cast(T, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+  else
+    return __builtin_bit_cast(T, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p)));
+}
+#else
+template <typename T>
+__device__ __forceinline__ T stream_load(const char* p) {
+  return *reinterpret_cast<const T*>(p);
+}
+#endif
 
 __device__ __forceinline__ uint64_t low_elems_mask(int n) {  // keep the first n of 4 bf16
   return n >= 4 ? ~0ull : (n <= 0 ? 0ull : ((1ull << (16 * n)) - 1ull));
 }
 
 template <int D>
-struct PagePair {
-  uint4 k0[D / 32], k1[D / 32];  // K rows (token = lane % 16), 8 dims per lane per 32-dim step
-  uint2 v0[D / 16], v1[D / 16];  // V^T rows (dim = 16 n + lane % 16), tokens 4 (lane / 16) .. +4
+struct Page {
+  uint4 k[D / 32];  // K rows (token = lane % 16), 8 dims per lane per 32-dim step
+  uint2 v[D / 16];  // V^T rows (dim = 16 n + lane % 16), tokens 4 (lane / 16) .. +4
 };
 
 template <int D>
-__device__ __forceinline__ void load_pair(PagePair<D>& pp, const char* kbase, const char* vbase, int id0, int id1,
-                                          bool ok0, bool ok1, int lane) {
+__device__ __forceinline__ void load_page(Page<D>& pg, const char* kbase, const char* vbase, size_t slab, int lane) {
   const int row = lane & 15, quad = lane >> 4;
   constexpr size_t kPageBytes = 16 * D * 2;  // one (page, kv head) slab
-  if (ok0) {
-    const char* kp = kbase + (size_t)id0 * kPageBytes + row * D * 2 + quad * 16;
-    const char* vp = vbase + (size_t)id0 * kPageBytes + row * 32 + quad * 8;
+  const char* kp = kbase + slab * kPageBytes + row * D * 2 + quad * 16;
+  const char* vp = vbase + slab * kPageBytes + row * 32 + quad * 8;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) pp.k0[ks] = *reinterpret_cast<const uint4*>(kp + ks * 64);
+  for (int ks = 0; ks < D / 32; ++ks) pg.k[ks] = stream_load<uint4>(kp + ks * 64);
 #pragma unroll
-    for (int n = 0; n < D / 16; ++n) pp.v0[n] = *reinterpret_cast<const uint2*>(vp + n * 16 * 32);
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) pp.k0[ks] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) pp.v0[n] = make_uint2(0, 0);
-  }
-  if (ok1) {
-    const char* kp = kbase + (size_t)id1 * kPageBytes + row * D * 2 + quad * 16;
-    const char* vp = vbase + (size_t)id1 * kPageBytes + row * 32 + quad * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) pp.k1[ks] = *reinterpret_cast<const uint4*>(kp + ks * 64);
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) pp.v1[n] = *reinterpret_cast<const uint2*>(vp + n * 16 * 32);
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) pp.k1[ks] = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) pp.v1[n] = make_uint2(0, 0);
-  }
+  for (int n = 0; n < D / 16; ++n) pg.v[n] = stream_load<uint2>(vp + n * 16 * 32);
 }
 
 __device__ __forceinline__ bool page_ok(int id, long long num_phys) { return id >= 0 && (long long)id < num_phys; }
 
-template <int D>
-__global__ __launch_bounds__(256) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
-  const int wave = uniform(threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  const int4 dr = w.dreq[blockIdx.y];  // (req, item_base, n_split, n_pages)
-  const int witem = blockIdx.x * 4 + wave;
-  const int j = witem / dr.z;
-  const int s = witem - j * dr.z;
-  if (j >= a.h_kv) return;  // no barriers in this kernel: idle waves leave early
+// One work item: decode request i (an index into dreq), kv head j, split s.
+template <int D, int PPS>
+__device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w, int i, int j, int s, int lane) {
+  const int4 dr = w.dreq[i];    // (req, item_base, n_split, n_pages)
   const int4 m = w.meta[dr.x];  // (kind, q_start, q_len, cached_len)
   const int L = m.w + m.z;
   const int g = a.group;
@@ -113,84 +110,82 @@ __global__ __launch_bounds__(256) void decode_partial_bf16(AttnArgs a, WorkArgs 
   f32x4 acc[D / 16];
 #pragma unroll
   for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  float l_run = 0.f;
   int bad = 0;
 
-  auto page_ids = [&](int p, int& id0, int& id1, bool& ok0, bool& ok1) {
-    id0 = uniform(prow[p]);
-    ok0 = page_ok(id0, a.num_phys_pages);
-    const bool has1 = p + 1 < pe;
-    id1 = has1 ? uniform(prow[p + 1]) : 0;
-    ok1 = has1 && page_ok(id1, a.num_phys_pages);
-    bad |= (!ok0) | (has1 && !ok1);
+  // The split's page ids (at most 64) are fetched once, one per lane, and broadcast per page.
+  // An out-of-range id is replaced by page 0 for the load and its tokens are masked.  Loads of
+  // page slots past the split re-read its last page (an L2 hit), so every load is unconditional
+  // and the compiler never has to merge a loaded buffer with a stale one.
+  const int my_id = lane < pe - pb ? prow[pb + lane] : 0;
+  struct Ids {
+    size_t slab;
+    bool ok;
+  };
+  auto page_id = [&](int p) {
+    Ids r;
+    const int id = __builtin_amdgcn_readlane(my_id, min(p, pe - 1) - pb);
+    r.ok = page_ok(id, a.num_phys_pages);
+    bad |= !r.ok;
+    r.slab = (size_t)(r.ok ? id : 0) * slab_stride_pages;
+    return r;
   };
 
-  PagePair<D> cur, nxt;
-  int id0, id1;
-  bool ok0, ok1;
-  page_ids(pb, id0, id1, ok0, ok1);
-  load_pair<D>(cur, kbase, vbase, (int)(id0 * slab_stride_pages), (int)(id1 * slab_stride_pages), ok0, ok1, lane);
-
-  for (int p = pb; p < pe; p += 2) {
-    const bool c_ok0 = ok0, c_ok1 = ok1;
-    if (p + 2 < pe) {
-      page_ids(p + 2, id0, id1, ok0, ok1);
-      load_pair<D>(nxt, kbase, vbase, (int)(id0 * slab_stride_pages), (int)(id1 * slab_stride_pages), ok0, ok1,
-                   lane);
-    }
-    // Scores S^T: lane holds head `col`, tokens 4 quad + i of each page.
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  auto compute = [&](const Page<D>& pg, int p, const Ids& ids) {
+    // Scores S^T: lane holds head `col`, tokens 4 quad + i of the page.
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur.k0[ks]), qf[ks], s0, 0, 0, 0);
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur.k1[ks]), qf[ks], s1, 0, 0, 0);
-
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pg.k[ks]), qf[ks], sc, 0, 0, 0);
     const int t0 = 16 * p + 4 * quad;
-    float x[8];
+    float x[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[i] = (c_ok0 && t0 + i < L) ? s0[i] * a.scale_log2 : -INFINITY;
-      x[4 + i] = (c_ok1 && t0 + 16 + i < L) ? s1[i] * a.scale_log2 : -INFINITY;
-    }
-    float mx = x[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, x[i]);
+    for (int i = 0; i < 4; ++i) x[i] = (ids.ok && t0 + i < L) ? sc[i] * a.scale_log2 : -INFINITY;
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
     m_run = m_new;
-    float pr[8], psum = 0.f;
+    bf16x4 pb4;
+    float psum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pr[i] = fast_exp2(x[i] - m_new);
-      psum += pr[i];
+    for (int i = 0; i < 4; ++i) {
+      const float pr = fast_exp2(x[i] - m_new);
+      psum += pr;
+      pb4[i] = static_cast<__bf16>(pr);
     }
     l_run = l_run * alpha + psum;
-    bf16x8 pb8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) pb8[i] = static_cast<__bf16>(pr[i]);
-
-    // Values of tokens past the end (NaN-poisoned slots) must not reach the MFMA.
-    if (16 * (p + 2) > L) {
-      const uint64_t mk0 = low_elems_mask(L - t0), mk1 = low_elems_mask(L - t0 - 16);
-#pragma unroll
-      for (int n = 0; n < D / 16; ++n) {
-        uint64_t v0 = ((uint64_t)cur.v0[n].y << 32 | cur.v0[n].x) & mk0;
-        uint64_t v1 = ((uint64_t)cur.v1[n].y << 32 | cur.v1[n].x) & mk1;
-        cur.v0[n] = make_uint2((uint32_t)v0, (uint32_t)(v0 >> 32));
-        cur.v1[n] = make_uint2((uint32_t)v1, (uint32_t)(v1 >> 32));
-      }
-    }
+    // Values of tokens past the end (NaN-poisoned slots) or of a bad page must not reach the MFMA.
+    const bool tail = 16 * (p + 1) > L || !ids.ok;
+    const uint64_t mk = !ids.ok ? 0ull : (tail ? low_elems_mask(L - t0) : ~0ull);
+    const s16x4 pbs = __builtin_bit_cast(s16x4, pb4);
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) {
+      const uint64_t v = ((uint64_t)pg.v[n].y << 32 | pg.v[n].x) & mk;
       acc[n] *= alpha;
-      const uint4 vv = make_uint4(cur.v0[n].x, cur.v0[n].y, cur.v1[n].x, cur.v1[n].y);
-      acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv), pb8, acc[n], 0, 0, 0);
+      acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, v), pbs, acc[n], 0, 0, 0);
     }
-    if (p + 2 < pe) cur = nxt;
+  };
+
+  // Three page buffers used in turn: the next two pages are in flight while one page is
+  // computed.  The split has at most PPS pages and the loop is fully unrolled, so no buffer is
+  // ever copied and every wait counts exactly the loads still needed.
+  Page<D> buf[3];
+  Ids ids[3];
+  ids[0] = page_id(pb);
+  load_page<D>(buf[0], kbase, vbase, ids[0].slab, lane);
+  ids[1] = page_id(pb + 1);
+  load_page<D>(buf[1], kbase, vbase, ids[1].slab, lane);
+#pragma unroll
+  for (int k = 0; k < PPS; ++k) {
+    if (k + 2 < PPS) {
+      ids[(k + 2) % 3] = page_id(pb + k + 2);
+      load_page<D>(buf[(k + 2) % 3], kbase, vbase, ids[(k + 2) % 3].slab, lane);
+    }
+    compute(buf[k % 3], pb + k, ids[k % 3]);
+    if (pb + k + 1 >= pe) break;
   }
 
   float l_tot = l_run + __shfl_xor(l_run, 16);
@@ -205,6 +200,22 @@ __global__ __launch_bounds__(256) void decode_partial_bf16(AttnArgs a, WorkArgs 
       w.pml[((size_t)item * g + col) * 2 + 0] = m_run;
       w.pml[((size_t)item * g + col) * 2 + 1] = l_tot;
     }
+  }
+}
+
+// Persistent: the grid holds as many waves as fit on the CUs the stream may use, and each wave
+// takes the next item from a counter until the list is exhausted (every wave reaches the exit).
+// Items are listed longest first.  Which wave computes an item never changes its arithmetic.
+template <int D, int PPS>
+__global__ __launch_bounds__(256) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
+  const int lane = threadIdx.x & 63;
+  for (;;) {
+    int next = 0;
+    if (lane == 0) next = atomicAdd(w.work_counter, 1);
+    const int item = __builtin_amdgcn_readfirstlane(next);
+    if (item >= w.n_ditems) break;
+    const int code = w.ditems[item];
+    decode_item<D, PPS>(a, w, code & 0xffff, (code >> 16) & 63, (code >> 22) & 1023, lane);
   }
 }
 
@@ -272,7 +283,8 @@ __global__ __launch_bounds__(256) void decode_partial_f32(AttnArgs a, WorkArgs w
   if (bad && lane == 0) atomicOr(w.err, 1);
 }
 
-// Merge the splits of one (decode request, query head): one wave, lane = dim.
+// Merge the splits of one (decode request, query head): one wave.  Lanes first take one split
+// each to find the common max and the denominator, then take one dim each to sum the outputs.
 template <int D, typename OutT>
 __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
   constexpr int E = D / 64;
@@ -285,19 +297,30 @@ __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
   const int4 m = w.meta[dr.x];
   const int g = a.group;
   const int j = h / g, col = h - j * g;
-  const int base = dr.y + j * dr.z;
+  const size_t base = (size_t)(dr.y + j * dr.z) * g + col;  // partial row of split 0
+  const int n = dr.z;
   float M = -INFINITY;
-  for (int s = 0; s < dr.z; ++s) M = fmaxf(M, w.pml[((size_t)(base + s) * g + col) * 2]);
+  for (int s = lane; s < n; s += 64) M = fmaxf(M, w.pml[(base + (size_t)s * g) * 2]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
   float den = 0.f, num[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) num[e] = 0.f;
-  for (int s = 0; s < dr.z; ++s) {
-    const size_t it = (size_t)(base + s) * g + col;
-    const float wgt = fast_exp2(w.pml[it * 2] - M);
-    den += wgt * w.pml[it * 2 + 1];
+  for (int s0 = 0; s0 < n; s0 += 64) {
+    const int s = s0 + lane;
+    const size_t row = base + (size_t)s * g;
+    const float wgt = s < n ? fast_exp2(w.pml[row * 2] - M) : 0.f;
+    den += s < n ? wgt * w.pml[row * 2 + 1] : 0.f;
+    const int cnt = min(64, n - s0);
+    for (int t = 0; t < cnt; ++t) {
+      const float wt = __shfl(wgt, t);
+      const float* pa = w.pacc + (base + (size_t)(s0 + t) * g) * D + lane;
 #pragma unroll
-    for (int e = 0; e < E; ++e) num[e] += wgt * w.pacc[it * D + lane + 64 * e];
+      for (int e = 0; e < E; ++e) num[e] += wt * pa[64 * e];
+    }
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) den += __shfl_xor(den, off);
   const float inv = 1.0f / den;
   OutT* o = reinterpret_cast<OutT*>(a.out) + ((size_t)m.y * a.h_q + h) * D;
 #pragma unroll
@@ -306,12 +329,26 @@ __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
 
 }  // namespace
 
+template <int D>
+hipError_t launch_persistent(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
+  static int per_cu = 0;  // resident 256-thread blocks per CU, from the occupancy calculator
+  if (per_cu == 0) {
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, reinterpret_cast<const void*>(&decode_partial_bf16<D, kDecodePagesPerSplit>), 256, 0);
+    if (e != hipSuccess) return e;
+    if (per_cu < 1) per_cu = 1;
+  }
+  const int blocks = std::max(1, std::min((w.n_ditems + 3) / 4, w.decode_cus * per_cu));
+  hipLaunchKernelGGL((decode_partial_bf16<D, kDecodePagesPerSplit>), dim3(blocks), dim3(256), 0, s, a, w);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_partial(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   if (w.n_dreq == 0) return hipSuccess;
   const dim3 grid((a.h_kv * w.max_split + 3) / 4, w.n_dreq);
   if (a.dtype == 0) {
-    if (a.head_dim == 128) hipLaunchKernelGGL(decode_partial_bf16<128>, grid, dim3(256), 0, s, a, w);
-    else hipLaunchKernelGGL(decode_partial_bf16<64>, grid, dim3(256), 0, s, a, w);
+    if (w.pages_per_split != kDecodePagesPerSplit) return hipErrorInvalidValue;
+    return a.head_dim == 128 ? launch_persistent<128>(a, w, s) : launch_persistent<64>(a, w, s);
   } else {
     if (a.head_dim == 128) hipLaunchKernelGGL(decode_partial_f32<128>, grid, dim3(256), 0, s, a, w);
     else hipLaunchKernelGGL(decode_partial_f32<64>, grid, dim3(256), 0, s, a, w);

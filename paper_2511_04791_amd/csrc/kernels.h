@@ -27,13 +27,31 @@ struct WorkArgs {
   const int4* dreq;     // [RD] decode requests (req, item_base, n_split, n_pages)
   float* pacc;          // [ND, group, d]  unnormalised split-K partial outputs
   float* pml;           // [ND, group, 2]  (running max in base-2 units, softmax denominator)
+  const int32_t* ditems;  // [ND] bf16 decode items in execution order: i | j << 16 | s << 22
   int32_t* err;         // error word: bit 0 = page id out of range
-  int32_t n_pitems, n_dreq, max_split;
+  int32_t* work_counter;  // next decode item to take (zeroed by the per-call upload)
+  int32_t n_pitems, n_dreq, max_split, n_ditems;
   int32_t pages_per_split;
+  int32_t decode_cus;   // CUs the decode stream may use (sizes the persistent grid)
 };
 
-constexpr int kPrefillRows = 128;  // query rows per prefill tile (4 waves x 32)
+#ifndef DUET_DECODE_PAGES_PER_SPLIT
+#define DUET_DECODE_PAGES_PER_SPLIT 16
+#endif
+// Decode split length in pages (bf16); fixed, so results do not depend on the CU split.
+constexpr int kDecodePagesPerSplit = DUET_DECODE_PAGES_PER_SPLIT;
+constexpr int kDecodePagesPerSplitF32 = 2;
+
+// Keys a prefill request may attend (its page ids are staged in LDS: 8192 ids, 32 KB).
+constexpr int kMaxPrefillKeys = 131072;
+
+constexpr int kPrefillRows = 128;  // query rows per fp32 prefill item (4 waves x 32)
 constexpr int kPrefillKeys = 64;   // keys per LDS stage (4 pages)
+
+// bf16 prefill work unit: prefill_heads_per_unit(group) query heads of one GQA group times
+// prefill_rows_per_unit(group, dtype) queries.  fp32 items are one head times kPrefillRows.
+int prefill_heads_per_unit(int group);
+int prefill_rows_per_unit(int group, int dtype);
 
 hipError_t launch_decode_partial(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
 hipError_t launch_decode_reduce(const AttnArgs& a, const WorkArgs& w, hipStream_t s);

@@ -31,7 +31,7 @@ namespace {
 using namespace duet;
 
 constexpr int kStagingSlots = 4;
-constexpr size_t kMaxMaskedStreams = 24;  // each CU-masked stream owns a hardware queue
+constexpr size_t kMaxMaskedStreams = 6;  // each CU-masked stream owns a hardware queue
 constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
@@ -52,11 +52,16 @@ struct StagingSlot {
 // Work lists of one iteration and where they live in the caller's workspace.
 struct Plan {
   std::vector<int4> meta, pitems, dreq;
+  std::vector<int32_t> ditems;
   int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0;
-  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_pacc = 0, off_pml = 0, upload_bytes = 0, total = 0;
+  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, off_pacc = 0, off_pml = 0, upload_bytes = 0,
+         total = 0;
 };
 
-int pages_per_split_for(const duet_shape* s) { return s->dtype == DUET_F32 ? 2 : 16; }
+// Fixed per dtype, never per split or placement, so results are identical for every CU split.
+int pages_per_split_for(const duet_shape* s) {
+  return s->dtype == DUET_F32 ? kDecodePagesPerSplitF32 : kDecodePagesPerSplit;
+}
 
 void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
   const int g = s->num_q_heads / s->num_kv_heads;
@@ -66,6 +71,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
   p->meta.clear();
   p->pitems.clear();
   p->dreq.clear();
+  p->ditems.clear();
   int64_t n_pitems = 0, n_dreq = 0, n_items = 0;
   int max_split = 0;
   struct Tile {
@@ -78,16 +84,22 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
     if (fill) p->meta.push_back(make_int4(q.kind, q.q_start, q.q_len, q.cached_len));
     const int64_t L = (int64_t)q.cached_len + q.q_len;
     if (q.kind == DUET_KIND_PREFILL) {
-      const int n_tiles = (q.q_len + kPrefillRows - 1) / kPrefillRows;
-      n_pitems += (int64_t)n_tiles * s->num_q_heads;
+      // bf16: a unit is nh heads of one group x rows queries; fp32: one head x rows queries.
+      const int nh = s->dtype == DUET_BF16 ? prefill_heads_per_unit(g) : 1;
+      const int rows = prefill_rows_per_unit(g, s->dtype == DUET_BF16 ? 0 : 1);
+      const int n_tiles = (q.q_len + rows - 1) / rows;
+      const int units = s->num_q_heads / nh;
+      n_pitems += (int64_t)n_tiles * units;
       if (fill) {
         for (int t = 0; t < n_tiles; ++t) {
-          const int64_t keys = q.cached_len + std::min(q.q_len, (t + 1) * kPrefillRows);
-          // Heads ordered so that workgroup index mod 8 equals the kv head mod 8: the query
-          // heads sharing one kv head land on one XCD and share its L2.
-          for (int pidx = 0; pidx < s->num_q_heads; ++pidx) {
-            const int h = (pidx % s->num_kv_heads) * g + pidx / s->num_kv_heads;
-            tiles.push_back({keys, make_int4(r, h, t * kPrefillRows, 0)});
+          const int64_t keys = q.cached_len + std::min(q.q_len, (t + 1) * rows);
+          // Units ordered so that workgroup index mod 8 follows the kv head: the units sharing
+          // one kv head land on one XCD and share its L2.
+          for (int u = 0; u < units; ++u) {
+            int h;
+            if (nh == 1) h = (u % s->num_kv_heads) * g + u / s->num_kv_heads;
+            else h = u * nh;
+            tiles.push_back({keys, make_int4(r, h, t * rows, 0)});
           }
         }
       }
@@ -104,6 +116,21 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
     std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& x, const Tile& y) { return x.keys > y.keys; });
     p->pitems.reserve(tiles.size());
     for (const Tile& t : tiles) p->pitems.push_back(t.item);
+    // bf16 decode items in execution order: every full split first, then the shorter last
+    // splits (longest first), packed as i | j << 16 | s << 22.
+    if (s->dtype == DUET_BF16) {
+      p->ditems.reserve(n_items);
+      for (int pass = 0; pass < 2; ++pass)
+        for (size_t i = 0; i < p->dreq.size(); ++i) {
+          const int4 d = p->dreq[i];
+          const bool full_last = d.w % pps == 0;
+          for (int j = 0; j < s->num_kv_heads; ++j)
+            for (int sp = 0; sp < d.z; ++sp) {
+              const bool is_full = sp + 1 < d.z || full_last;
+              if (is_full == (pass == 0)) p->ditems.push_back((int32_t)i | (j << 16) | (sp << 22));
+            }
+        }
+    }
   }
   p->n_items_decode = (int)n_items;
   p->max_split = max_split;
@@ -114,6 +141,8 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
   off = align_up(off + (size_t)n_pitems * sizeof(int4));
   p->off_dreq = off;
   off = align_up(off + (size_t)n_dreq * sizeof(int4));
+  p->off_ditems = off;
+  off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)n_items * sizeof(int32_t) : 0));
   p->upload_bytes = off;
   p->off_pacc = off;
   off = align_up(off + (size_t)n_items * g * s->head_dim * sizeof(float));
@@ -200,10 +229,11 @@ int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
     slot.cap = cap;
   }
   char* h = static_cast<char*>(slot.host);
-  std::memset(h, 0, kAlign);  // clears the error word
+  std::memset(h, 0, kAlign);  // clears the error word and the decode work counter
   std::memcpy(h + p.off_meta, p.meta.data(), p.meta.size() * sizeof(int4));
   std::memcpy(h + p.off_pitems, p.pitems.data(), p.pitems.size() * sizeof(int4));
   std::memcpy(h + p.off_dreq, p.dreq.data(), p.dreq.size() * sizeof(int4));
+  std::memcpy(h + p.off_ditems, p.ditems.data(), p.ditems.size() * sizeof(int32_t));
   HIP_TRY(hipMemcpyAsync(ws, h, p.upload_bytes, hipMemcpyHostToDevice, st));
   HIP_TRY(hipEventRecord(slot.done, st));
   slot.pending = true;
@@ -319,6 +349,21 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
       return fail(DUET_EINVAL, "request %d needs %lld pages, page_table rows hold %d", r, (long long)((L + 15) / 16),
                   max_pages_per_req);
   }
+  {
+    int n_dec = 0;
+    for (int r = 0; r < batch->num_reqs; ++r) {
+      const duet_seq_meta& q = batch->reqs[r];
+      const int64_t L = (int64_t)q.cached_len + q.q_len;
+      if (q.kind == DUET_KIND_DECODE) ++n_dec;
+      if (q.kind == DUET_KIND_PREFILL && L > kMaxPrefillKeys)
+        return fail(DUET_EUNSUPPORTED, "request %d: prefill attends %lld keys, at most %d supported", r,
+                    (long long)L, kMaxPrefillKeys);
+      if (q.kind == DUET_KIND_DECODE && (L + 15) / 16 > 1023LL * kDecodePagesPerSplit)
+        return fail(DUET_EUNSUPPORTED, "request %d: decode context %lld too long", r, (long long)L);
+    }
+    if (n_dec > 65535) return fail(DUET_EUNSUPPORTED, "more than 65535 decode requests");
+    if (shape->num_kv_heads > 63) return fail(DUET_EUNSUPPORTED, "more than 63 kv heads");
+  }
   if (split.mode == DUET_SPLIT) {
     if (split.cus_prefill < DUET_CU_STEP || split.cus_decode < DUET_CU_STEP || split.cus_prefill % DUET_CU_STEP ||
         split.cus_decode % DUET_CU_STEP || split.cus_prefill + split.cus_decode > ctx->num_cus)
@@ -363,7 +408,11 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
   w.dreq = reinterpret_cast<const int4*>(ws + p.off_dreq);
   w.pacc = reinterpret_cast<float*>(ws + p.off_pacc);
   w.pml = reinterpret_cast<float*>(ws + p.off_pml);
+  w.ditems = reinterpret_cast<const int32_t*>(ws + p.off_ditems);
   w.err = reinterpret_cast<int32_t*>(ws);
+  w.work_counter = reinterpret_cast<int32_t*>(ws) + 16;
+  w.n_ditems = (int)p.ditems.size();
+  w.decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
   w.n_pitems = (int)p.pitems.size();
   w.n_dreq = (int)p.dreq.size();
   w.max_split = p.max_split;
