@@ -14,8 +14,9 @@
 // MFMA A layout); V pages are stored dim-major, so a lane's 4 consecutive tokens of one dim
 // are 8 contiguous bytes and P^T never leaves registers.  Pages cycle through three register
 // buffers (the loop is unrolled by three), so two pages are in flight while one is computed.
-// Online softmax keeps a running max and denominator per head.  Partials (unnormalised
-// output, running max, denominator) go to the workspace and the reduce kernel merges the splits.
+// Online softmax keeps a reference max per head that only moves when a score exceeds it by
+// more than 2^8 (base-2 units), so the output rescale is rare.  Partials (unnormalised output,
+// reference max, denominator) go to the workspace and the reduce kernel merges the splits.
 // All arithmetic order depends on logical token positions only.
 #include <hip/hip_runtime.h>
 
@@ -29,7 +30,10 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
@@ -131,7 +135,7 @@ __device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w
     return r;
   };
 
-  float m_run = -INFINITY;
+  float m_ref = -INFINITY;  // reference max (base-2 units) the probabilities are taken against
   auto compute = [&](const Page<D>& pg, int p, const Ids& ids) {
     // Scores S^T: lane holds head `col`, tokens 4 quad + i of the page.
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
@@ -139,32 +143,45 @@ __device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w
     for (int ks = 0; ks < D / 32; ++ks)
       sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pg.k[ks]), qf[ks], sc, 0, 0, 0);
     const int t0 = 16 * p + 4 * quad;
-    float x[4];
+    // Tokens past the end (NaN-poisoned slots) and tokens of a bad page are masked; only the
+    // last page of a request or a bad page needs it.
+    const bool tail = 16 * (p + 1) > L || !ids.ok;
+    if (tail) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = (ids.ok && t0 + i < L) ? sc[i] * a.scale_log2 : -INFINITY;
-    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      for (int i = 0; i < 4; ++i)
+        if (!ids.ok || t0 + i >= L) sc[i] = -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    bf16x4 pb4;
-    float psum = 0.f;
+    mx *= a.scale_log2;  // the scale is positive: max of scaled = scaled max
+    // The reference max moves only when a score exceeds it by more than the slack, so the
+    // output rescale is rare; numerator and denominator share the reference.
+#ifndef DUET_DECODE_EAGER_RESCALE
+    if (__any(mx > m_ref + kRescaleSlack)) {
+#endif
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = fast_exp2(m_ref - m_new);
+      m_ref = m_new;
+      l_run *= alpha;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float pr = fast_exp2(x[i] - m_new);
-      psum += pr;
-      pb4[i] = static_cast<__bf16>(pr);
+      for (int n = 0; n < D / 16; ++n) acc[n] *= alpha;
+#ifndef DUET_DECODE_EAGER_RESCALE
     }
-    l_run = l_run * alpha + psum;
-    // Values of tokens past the end (NaN-poisoned slots) or of a bad page must not reach the MFMA.
-    const bool tail = 16 * (p + 1) > L || !ids.ok;
-    const uint64_t mk = !ids.ok ? 0ull : (tail ? low_elems_mask(L - t0) : ~0ull);
+#endif
+    bf16x4 pb4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pb4[i] = static_cast<__bf16>(fast_exp2(__builtin_fmaf(sc[i], a.scale_log2, -m_ref)));
+    // The denominator sums the bf16 probabilities the PV product consumes.
+    const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+    l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[0], pb4[1]}, ones, l_run, false);
+    l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[2], pb4[3]}, ones, l_run, false);
     const s16x4 pbs = __builtin_bit_cast(s16x4, pb4);
+    // Their values must not reach the MFMA either (0 x NaN is NaN).
+    const uint64_t mk = !ids.ok ? 0ull : (tail ? low_elems_mask(L - t0) : ~0ull);
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) {
       const uint64_t v = ((uint64_t)pg.v[n].y << 32 | pg.v[n].x) & mk;
-      acc[n] *= alpha;
       acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, v), pbs, acc[n], 0, 0, 0);
     }
   };
@@ -197,7 +214,7 @@ __device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) *reinterpret_cast<f32x4*>(pa + 16 * n) = acc[n];
     if (quad == 0) {
-      w.pml[((size_t)item * g + col) * 2 + 0] = m_run;
+      w.pml[((size_t)item * g + col) * 2 + 0] = m_ref;
       w.pml[((size_t)item * g + col) * 2 + 1] = l_tot;
     }
   }
@@ -206,8 +223,11 @@ __device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w
 // Persistent: the grid holds as many waves as fit on the CUs the stream may use, and each wave
 // takes the next item from a counter until the list is exhausted (every wave reaches the exit).
 // Items are listed longest first.  Which wave computes an item never changes its arithmetic.
+#ifndef DUET_DECODE_MIN_BLOCKS_PER_CU
+#define DUET_DECODE_MIN_BLOCKS_PER_CU 1
+#endif
 template <int D, int PPS>
-__global__ __launch_bounds__(256) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
+__global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
   const int lane = threadIdx.x & 63;
   for (;;) {
     int next = 0;
@@ -312,11 +332,22 @@ __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
     const float wgt = s < n ? fast_exp2(w.pml[row * 2] - M) : 0.f;
     den += s < n ? wgt * w.pml[row * 2 + 1] : 0.f;
     const int cnt = min(64, n - s0);
-    for (int t = 0; t < cnt; ++t) {
-      const float wt = __shfl(wgt, t);
-      const float* pa = w.pacc + (base + (size_t)(s0 + t) * g) * D + lane;
+    // Eight partial rows are loaded before any is accumulated, so their loads overlap.
+    for (int t0 = 0; t0 < cnt; t0 += 8) {
+      float part[8][E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) num[e] += wt * pa[64 * e];
+      for (int u = 0; u < 8; ++u) {
+        const int t = min(t0 + u, cnt - 1);
+        const float* pa = w.pacc + (base + (size_t)(s0 + t) * g) * D + lane;
+#pragma unroll
+        for (int e = 0; e < E; ++e) part[u][e] = pa[64 * e];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float wt = t0 + u < cnt ? __shfl(wgt, t0 + u) : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) num[e] += wt * part[u][e];
+      }
     }
   }
 #pragma unroll
@@ -329,6 +360,17 @@ __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
 
 }  // namespace
 
+#ifndef DUET_DECODE_MIN_ROUNDS
+#define DUET_DECODE_MIN_ROUNDS 4
+#endif
+#ifndef DUET_DECODE_MIN_WAVES_PER_CU
+#define DUET_DECODE_MIN_WAVES_PER_CU 4
+#endif
+
+// Persistent grid size.  The memory system needs far fewer waves in flight than fit, so the grid
+// is sized for at least DUET_DECODE_MIN_ROUNDS items per wave (a short tail when the last items
+// finish), but never below DUET_DECODE_MIN_WAVES_PER_CU waves per CU (bandwidth on small CU
+// shares) nor above what is resident at once.
 template <int D>
 hipError_t launch_persistent(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   static int per_cu = 0;  // resident 256-thread blocks per CU, from the occupancy calculator
@@ -338,8 +380,11 @@ hipError_t launch_persistent(const AttnArgs& a, const WorkArgs& w, hipStream_t s
     if (e != hipSuccess) return e;
     if (per_cu < 1) per_cu = 1;
   }
-  const int blocks = std::max(1, std::min((w.n_ditems + 3) / 4, w.decode_cus * per_cu));
-  hipLaunchKernelGGL((decode_partial_bf16<D, kDecodePagesPerSplit>), dim3(blocks), dim3(256), 0, s, a, w);
+  const int capacity = w.decode_cus * per_cu * 4;
+  const int floor_waves = w.decode_cus * DUET_DECODE_MIN_WAVES_PER_CU;
+  const int want = (w.n_ditems + DUET_DECODE_MIN_ROUNDS - 1) / DUET_DECODE_MIN_ROUNDS;
+  const int waves = std::max(1, std::min(capacity, std::max(want, floor_waves)));
+  hipLaunchKernelGGL((decode_partial_bf16<D, kDecodePagesPerSplit>), dim3((waves + 3) / 4), dim3(256), 0, s, a, w);
   return hipGetLastError();
 }
 

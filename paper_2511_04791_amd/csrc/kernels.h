@@ -36,7 +36,7 @@ struct WorkArgs {
 };
 
 #ifndef DUET_DECODE_PAGES_PER_SPLIT
-#define DUET_DECODE_PAGES_PER_SPLIT 16
+#define DUET_DECODE_PAGES_PER_SPLIT 32
 #endif
 // Decode split length in pages (bf16); fixed, so results do not depend on the CU split.
 constexpr int kDecodePagesPerSplit = DUET_DECODE_PAGES_PER_SPLIT;
