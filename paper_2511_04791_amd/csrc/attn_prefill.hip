@@ -192,17 +192,48 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     if (kt < w_tiles) {
       const __bf16* ks = lds + (kt % kStages) * PrefillSmem<D>::kStageElems;
       const __bf16* vs = ks + BN * D;
-      f32x16 sacc[2];
+      // All K fragments of the step are read before the first MFMA, so LDS latency is paid once.
+      bf16x8 kf[2][NK];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[nb][v] = 0.f;
         const int row = 32 * nb + swap_bits23(lane & 31);
 #pragma unroll
         for (int kk = 0; kk < NK; ++kk) {
           const int ch = (2 * kk + hh) ^ (kswz(row) & (KCH - 1));
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + row * D + ch * 8);
-          sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[nb], 0, 0, 0);
+          kf[nb][kk] = *reinterpret_cast<const bf16x8*>(ks + row * D + ch * 8);
+        }
+      }
+      f32x16 sacc[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc[nb][v] = 0.f;
+#ifdef DUET_PREFILL_SETPRIO
+      __builtin_amdgcn_s_setprio(1);
+#endif
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+          sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[nb][kk], qf[kk], sacc[nb], 0, 0, 0);
+#ifdef DUET_PREFILL_SETPRIO
+      __builtin_amdgcn_s_setprio(0);
+#endif
+      // V fragments are read now; their LDS latency hides behind the softmax below.  With
+      // DUET_PREFILL_VHALF only the first half is read ahead (fewer live registers).
+#ifdef DUET_PREFILL_VHALF
+      constexpr int NV = NO / 2;
+#else
+      constexpr int NV = NO;
+#endif
+      bf16x8 vf[NO][4];
+#pragma unroll
+      for (int n = 0; n < NV; ++n) {
+        const int vrow = 32 * n + (lane & 31);
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2) {
+          const int ch = (2 * k2 + hh) ^ (vswz(vrow) & (VCH - 1));
+          vf[n][k2] = *reinterpret_cast<const bf16x8*>(vs + vrow * BN + ch * 8);
         }
       }
       // Only tiles that cross this wave's diagonal need the causal mask.
@@ -248,15 +279,25 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
           l_run = __builtin_amdgcn_fdot2_f32_bf16(two, ones, l_run, false);
         }
 #pragma unroll
-      for (int n = 0; n < NO; ++n) {
+      for (int n = NV; n < NO; ++n) {
         const int vrow = 32 * n + (lane & 31);
 #pragma unroll
         for (int k2 = 0; k2 < 4; ++k2) {
           const int ch = (2 * k2 + hh) ^ (vswz(vrow) & (VCH - 1));
-          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vs + vrow * BN + ch * 8);
-          oacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[k2], oacc[n], 0, 0, 0);
+          vf[n][k2] = *reinterpret_cast<const bf16x8*>(vs + vrow * BN + ch * 8);
         }
       }
+#ifdef DUET_PREFILL_SETPRIO
+      __builtin_amdgcn_s_setprio(1);
+#endif
+#pragma unroll
+      for (int n = 0; n < NO; ++n)
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2)
+          oacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n][k2], pb[k2], oacc[n], 0, 0, 0);
+#ifdef DUET_PREFILL_SETPRIO
+      __builtin_amdgcn_s_setprio(0);
+#endif
     }
     if (kt + 2 < n_tiles) store_tile((kt + 2) % kStages);
     if (kt + 3 < n_tiles) load_tile(kt + 3);
