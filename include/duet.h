@@ -194,9 +194,12 @@ int duet_gather_kv(duet_ctx* ctx, const duet_shape* shape, int32_t which, const 
                    int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
                    int32_t req, int32_t kv_len, void* out_contig, void* stream);
 
-/* Profiling: when on, every duet_attn_mixed_batch call records HIP events around each kernel on
- * the stream it runs on; duet_last_kernel_times() waits for them and returns the durations. */
-int duet_set_profiling(duet_ctx* ctx, int32_t enable);
+/* Profiling level: 0 off; 1 records HIP events at the fork and the join of every
+ * duet_attn_mixed_batch call on the caller's stream (iteration latency only); 2 also records
+ * events around each kernel on the stream it runs on (these add small gaps between kernels).
+ * duet_last_kernel_times() waits for the last call's events and returns the durations (kernel
+ * fields are 0 at level 1). */
+int duet_set_profiling(duet_ctx* ctx, int32_t level);
 int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out);
 
 /* ---- calibration probes (Section 3 "Opportunity", Section 4.2 profiling) -------------------- */

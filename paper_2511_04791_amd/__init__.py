@@ -232,8 +232,10 @@ class Context:
                                        kv_len, out.data_ptr(), ctypes.c_void_p(st)), "duet_gather_kv")
         return out
 
-    def set_profiling(self, on: bool):
-        N.check(N.lib().duet_set_profiling(self.handle, 1 if on else 0), "duet_set_profiling")
+    def set_profiling(self, level):
+        """0 off, 1 iteration events, 2 per-kernel events (True means 2)."""
+        level = 2 if level is True else int(level)
+        N.check(N.lib().duet_set_profiling(self.handle, level), "duet_set_profiling")
 
     def last_kernel_times(self) -> dict:
         t = N.KernelTimes()

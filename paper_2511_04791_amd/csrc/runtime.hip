@@ -165,9 +165,9 @@ struct duet_ctx {
   uint64_t use_clock = 0;
   hipEvent_t ev_fork = nullptr, ev_djoin = nullptr, ev_pjoin = nullptr;
   hipEvent_t prof[kNumProfEv] = {};
-  bool profiling = false;
+  int profiling = 0;  // 0 off, 1 iteration events only, 2 also per-kernel events
   bool prof_valid = false;
-  bool prof_decode = false, prof_prefill = false;
+  bool prof_decode = false, prof_prefill = false, prof_kernels = false;
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
   int32_t* dev_flag = nullptr;  // gather error word
@@ -417,10 +417,11 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
   w.n_dreq = (int)p.dreq.size();
   w.max_split = p.max_split;
   w.pages_per_split = p.pages_per_split;
-  const bool prof = ctx->profiling;
+  const bool prof_iter = ctx->profiling >= 1;
+  const bool prof = ctx->profiling >= 2;
   const bool has_decode = w.n_dreq > 0, has_prefill = w.n_pitems > 0;
 
-  if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
+  if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
   if ((rc = stage_upload(ctx, p, ws, order))) return rc;
   if (split.mode == DUET_SPLIT) {
     HIP_TRY(hipEventRecord(ctx->ev_fork, order));
@@ -446,8 +447,9 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
     HIP_TRY(hipStreamWaitEvent(order, ctx->ev_djoin, 0));
     HIP_TRY(hipStreamWaitEvent(order, ctx->ev_pjoin, 0));
   }
-  if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
-  ctx->prof_valid = prof;
+  if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
+  ctx->prof_valid = prof_iter;
+  ctx->prof_kernels = prof;
   ctx->prof_decode = has_decode;
   ctx->prof_prefill = has_prefill;
   return DUET_OK;
@@ -497,7 +499,7 @@ int duet_gather_kv(duet_ctx* ctx, const duet_shape* shape, int32_t which, const 
 int duet_set_profiling(duet_ctx* ctx, int32_t enable) {
   if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
   std::lock_guard<std::mutex> lock(ctx->mu);
-  ctx->profiling = enable != 0;
+  ctx->profiling = enable < 0 ? 0 : (enable > 2 ? 2 : enable);
   return DUET_OK;
 }
 
@@ -509,7 +511,7 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
   HIP_TRY(hipEventSynchronize(ctx->prof[kEvJoin]));
   float ms = 0.f;
   std::memset(out, 0, sizeof *out);
-  if (ctx->prof_decode) {
+  if (ctx->prof_kernels && ctx->prof_decode) {
     HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD1]));
     out->decode_partial_us = ms * 1e3;
     HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD1], ctx->prof[kEvD2]));
@@ -517,7 +519,7 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
     HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD2]));
     out->decode_total_us = ms * 1e3;
   }
-  if (ctx->prof_prefill) {
+  if (ctx->prof_kernels && ctx->prof_prefill) {
     HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvP0], ctx->prof[kEvP1]));
     out->prefill_us = ms * 1e3;
   }
