@@ -1,18 +1,21 @@
 #!/usr/bin/env python3
 """Mixed-batch attention iteration on one MI355X: latency, decode HBM GB/s, prefill MFMA TFLOP/s.
 
-Workload: one attention layer of Llama-3-8B (32 query heads, 8 kv heads, head_dim 128, bf16,
-page size 16) over a synthetic mixed batch -- a 2048-token prefill chunk at prefix 0 plus 64
-decode requests with contexts uniform in [512, 4096] -- with pages placed by a seeded random
-permutation.  Inputs are resident in HBM before timing starts.
+Workload: the attention of one serving iteration of a Llama-3-8B-shaped model -- 32 layers of
+32 query heads, 8 kv heads, head_dim 128, bf16, page size 16 -- over a synthetic mixed batch: a
+2048-token prefill chunk at prefix 0 plus 64 decode requests with contexts uniform in
+[512, 4096], pages placed by a seeded random permutation, each layer with its own Q and KV
+cache.  Inputs are resident in HBM before timing starts.
 
 A step is one pass of the whole hot path: the latency model and Algorithm 1's CU-split choice
-on the host, then duet_attn_mixed_batch (work lists, the decode split-K and reduce kernels and
-the prefill MFMA kernel on their CU-masked streams, the join).
+on the host, then duet_attn_iteration (work lists built and uploaded once, the decode split-K
+and reduce kernels and the prefill MFMA kernel of every layer on their CU-masked streams, the
+fork and the join).
 
-Prints one JSON line.  `value` is the mean iteration latency in microseconds measured with HIP
-events at the fork and the join on the caller's stream (lower is better).  A second pass with
-per-kernel events gives the kernel durations behind the roofline figures.
+Prints one JSON line.  `value` is the wall-clock time per step of K back-to-back steps between
+two device synchronisations (lower is better).  Further passes give the fork-to-join latency
+of one iteration (HIP events on the caller's stream) and per-kernel durations (HIP events on
+each kernel's own stream) behind the roofline figures.
 """
 from __future__ import annotations
 
@@ -131,8 +134,9 @@ def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--layers", type=int, default=32, help="attention layers per iteration (Llama-3-8B: 32)")
     ap.add_argument("--mode", choices=["adaptive", "agg", "split"], default="adaptive")
     ap.add_argument("--split", default="", help="Sp,Sd for --mode split")
     ap.add_argument("--tbt-slo-us", type=float, default=None,
@@ -141,12 +145,15 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the S_p = 24..232 step-8 split sweep")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibrate", action="store_true")
+    ap.add_argument("--copy-reference", action="store_true",
+                    help="end with a plain 1 GiB device-to-device copy, the reference for HBM counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path; "
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    import dataclasses
     import torch
     import paper_2511_04791_amd as duet
     from paper_2511_04791_amd import workloads as wl
@@ -155,24 +162,24 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    L = args.layers
     ctx = duet.Context(0)
     calib = {}
     if not args.no_calibrate:
         t0 = time.perf_counter()
         calib = calibrate_model(ctx)
-        cus, fl, by = ctx.model.tables()
-        calib.update(seconds=round(time.perf_counter() - t0, 2), read_tbps_256=round(by[-1] / 1e12, 3),
-                     read_tbps_64=round(by[7] / 1e12, 3), mfma_tflops_256=round(fl[-1] / 1e12, 1),
-                     mfma_tflops_64=round(fl[7] / 1e12, 1))
+        calib["seconds"] = round(time.perf_counter() - t0, 2)
 
     batch = wl.llama8b_mixed()
-    q, kc, vc = wl.make_tensors(batch, seed=2002, device="cuda")
+    layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
+    qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
+    del layers
     pt = torch.as_tensor(batch.page_table, device="cuda")
     meta = batch.seq_meta
     rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
-    out = torch.empty_like(q)
-    ws = ctx.workspace(duet.workspace_bytes(batch.shape, meta))
-    shape = batch.shape
+    outs = [torch.empty_like(q) for q in qs]
+    shape = dataclasses.replace(batch.shape, num_layers=L)
+    ws = ctx.workspace(duet.workspace_bytes(shape, meta))
     torch.cuda.synchronize()
 
     agg_pred = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), shape, ctx.model)
@@ -193,69 +200,106 @@ def main():
     else:
         fixed = None
 
-    def steps(n, warm, level, split=None):
+    def step(split=None):
+        sp = split if split is not None else (fixed if fixed is not None else choose())
+        ctx.attn_iteration(qs, kcs, vcs, pt, meta, sp, outs=outs, workspace=ws)
+        return sp
+
+    def profiled(n, warm, level, split):
+        """n steps at profiling level 1 or 2, each read back: mean of the event times."""
         ctx.set_profiling(level)
-        rec, wall, used = [], [], None
+        rec = []
         for i in range(warm + n):
-            t0 = time.perf_counter()
-            sp = split if split is not None else (fixed if fixed is not None else choose())
-            ctx.attn_mixed_batch(q, kc, vc, pt, meta, sp, out=out, workspace=ws)
+            step(split)
             kt = ctx.last_kernel_times()
-            wall.append(time.perf_counter() - t0)
             if i >= warm:
                 rec.append(kt)
-                used = sp
         ctx.set_profiling(0)
-        mean = {k: statistics.fmean(r[k] for r in rec) for k in rec[0]}
-        return mean, statistics.fmean(wall[warm:]), used
+        return {k: statistics.fmean(r[k] for r in rec) for k in rec[0]}
 
-    # timed region: the requested mode, fork/join events only
-    it, wall, used = steps(args.steps, args.warmup, 1)
+    # timed region: K back-to-back steps, host choice included, synchronised on both sides
+    for _ in range(args.warmup):
+        used = step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        used = step()
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / args.steps
     choose_mean = statistics.fmean(choose_us) if choose_us else 0.0
-    # aggregated reference and per-kernel durations (second pass, per-kernel events)
-    agg_it, _, _ = steps(max(10, args.steps // 2), 3, 1, duet.CuSplit.agg())
-    kern, _, _ = steps(max(10, args.steps // 2), 3, 2, used)
-    agg_kern, _, _ = steps(max(10, args.steps // 2), 3, 2, duet.CuSplit.agg())
+
+    n_prof = max(5, args.steps // 2)
+    it = profiled(n_prof, 2, 1, used)
+    agg_it = profiled(n_prof, 2, 1, duet.CuSplit.agg())
+    kern = profiled(n_prof, 2, 2, used)
+    agg_kern = profiled(n_prof, 2, 2, duet.CuSplit.agg())
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(duet.CuSplit.agg())
+    torch.cuda.synchronize()
+    agg_wall = (time.perf_counter() - t0) / args.steps
 
     sp_cus = used.cus_prefill if used.mode == duet.SPLIT else 256
     sd_cus = used.cus_decode if used.mode == duet.SPLIT else 256
-    dbytes = decode_bytes(batch)
-    pflops = prefill_causal_flops(batch)
-    k2, kdec, k1 = kern["decode_partial_us"], kern["decode_total_us"], kern["prefill_us"]
-    dec_gbps = dbytes / (kdec * 1e-6) / 1e9
+    dbytes = decode_bytes(batch)          # per layer = per decode-partial launch
+    pflops = prefill_causal_flops(batch)  # per layer = per prefill launch
+    k2, k1 = kern["decode_partial_us"], kern["prefill_us"]
     k2_gbps = dbytes / (k2 * 1e-6) / 1e9
+    dec_gbps = dbytes * L / (kern["decode_total_us"] * 1e-6) / 1e9
     pre_tflops = pflops / (k1 * 1e-6) / 1e12
-    cus_tab, fl_tab, by_tab = ctx.model.tables()
-    b_share = by_tab[sd_cus // 8 - 1] / 1e9
+    agg_k2_gbps = dbytes / (agg_kern["decode_partial_us"] * 1e-6) / 1e9
+    agg_pre_tflops = pflops / (agg_kern["prefill_us"] * 1e-6) / 1e12
+    # hardware ceiling of each share: the probes' streaming read and MFMA loop (nominal
+    # 8 TB/s and 2.5 PFLOP/s pro rata without calibration)
+    if calib:
+        b_share = calib["probe_read_tbps"][sd_cus // 8 - 1] * 1e3
+        p_share = calib["probe_mfma_tflops"][sp_cus // 8 - 1]
+    else:
+        b_share = PEAK_HBM_GBPS * sd_cus / 256
+        p_share = PEAK_BF16_TFLOPS * sp_cus / 256
 
     sweep = None
     if not args.no_sweep:
         sweep = []
         for s in range(24, 233, 8):
-            r_, _, _ = steps(5, 2, 1, duet.CuSplit.split(s, 256 - s))
+            sp = duet.CuSplit.split(s, 256 - s)
+            r_ = profiled(3, 1, 1, sp)
             sweep.append({"Sp": s, "Sd": 256 - s, "iteration_us": round(r_["iteration_us"], 1),
-                          "predicted_us": round(duet.predict_iter_latency(rows3, duet.CuSplit.split(s, 256 - s),
-                                                                          shape, ctx.model), 1)})
-    cpu = None if args.no_cpu_baseline else cpu_baseline(batch, q, kc, vc)
+                          "predicted_us": round(duet.predict_iter_latency(rows3, sp, shape, ctx.model), 1)})
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(batch, qs[0], kcs[0], vcs[0])
+        one_layer = cpu["value"]
+        cpu["value"] = round(one_layer * L, 1)
+        cpu["sample"] += f"; one layer's oracle time x {L} layers"
+    if args.copy_reference:
+        # an elementwise kernel (not a DMA copy) that reads 1 GiB and writes 1 GiB
+        src = torch.zeros(1 << 28, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     decode_dominant = k2 >= k1
     if decode_dominant:
         traffic = committed_traffic("decode_partial", "attn_decode.hip", 1)
         roofline = {"bound": "hbm", "achieved": round(k2_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                     "frac": round(k2_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic, "kernel": "decode_partial_bf16",
-                    "algorithmic_bytes": int(dbytes), "cus": sd_cus,
-                    "share_peak": round(b_share, 1), "share_frac": round(k2_gbps / b_share, 4)}
+                    "algorithmic_bytes_per_launch": int(dbytes), "launch_us": round(k2, 2), "cus": sd_cus,
+                    "share_peak": round(PEAK_HBM_GBPS * sd_cus / 256, 1),
+                    "share_frac": round(k2_gbps / (PEAK_HBM_GBPS * sd_cus / 256), 4)}
     else:
         traffic = committed_traffic("prefill", "attn_prefill.hip", 1)
-        share = PEAK_BF16_TFLOPS * sp_cus / 256
         roofline = {"bound": "mfma", "achieved": round(pre_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": "prefill_bf16",
-                    "algorithmic_flops": pflops, "cus": sp_cus, "share_peak": share,
-                    "share_frac": round(pre_tflops / share, 4)}
+                    "algorithmic_flops_per_launch": pflops, "launch_us": round(k1, 2), "cus": sp_cus,
+                    "share_peak": round(PEAK_BF16_TFLOPS * sp_cus / 256, 1),
+                    "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4)}
 
     line = {
         "metric": "mixed-batch attn iter latency (us) + decode HBM GB/s + prefill MFMA TFLOP/s",
-        "value": round(it["iteration_us"], 2),
+        "value": round(wall * 1e6, 1),
         "unit": "us",
         "n_gpus": 1,
         "steps": args.steps,
@@ -266,33 +310,44 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "llama3-8b attention, one layer: 1 prefill chunk of 2048 tokens at prefix 0 + 64 "
-                               "decodes (context U[512,4096]), 32 q-heads / 8 kv-heads / head_dim 128, page 16, "
-                               "pages randomly placed",
-                   "mode": args.mode, "split": str(used), "tbt_slo_us": round(tau, 2)},
-        "agg_us": round(agg_it["iteration_us"], 2),
-        "agg_pred_us": round(agg_pred, 2),
-        "chosen_pred_us": round(duet.predict_iter_latency(rows3, used, shape, ctx.model), 2),
+        "config": {"workload": f"llama3-8b attention, {L} layers per iteration: 1 prefill chunk of 2048 tokens at "
+                               "prefix 0 + 64 decodes (context U[512,4096]), 32 q-heads / 8 kv-heads / head_dim "
+                               "128, page 16, pages randomly placed",
+                   "layers": L, "mode": args.mode, "split": str(used), "tbt_slo_us": round(tau, 1)},
+        "iteration_us": round(it["iteration_us"], 1),
+        "agg_us": round(agg_wall * 1e6, 1),
+        "agg_iteration_us": round(agg_it["iteration_us"], 1),
+        "speedup_vs_agg": round(agg_wall / wall, 4),
+        "agg_pred_us": round(agg_pred, 1),
+        "chosen_pred_us": round(duet.predict_iter_latency(rows3, used, shape, ctx.model), 1),
         "host_choose_us": round(choose_mean, 2),
-        "decode_hbm_gbps": round(dec_gbps, 1),
+        "decode_half_hbm_gbps": round(dec_gbps, 1),
         "decode_partial_gbps": round(k2_gbps, 1),
         "prefill_mfma_tflops": round(pre_tflops, 1),
         "kernels_us": {k.replace("_us", ""): round(v, 2) for k, v in kern.items()},
         "agg_kernels_us": {k.replace("_us", ""): round(v, 2) for k, v in agg_kern.items()},
         "roofline": roofline,
-        "prefill_roofline": {"bound": "mfma", "achieved": round(pre_tflops, 1),
-                             "share_peak": PEAK_BF16_TFLOPS * sp_cus / 256,
-                             "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4), "cus": sp_cus,
-                             "algorithmic_flops": pflops},
-        "decode_roofline": {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS,
-                            "frac": round(dec_gbps / PEAK_HBM_GBPS, 4), "share_peak": round(b_share, 1),
-                            "share_frac": round(dec_gbps / b_share, 4), "cus": sd_cus},
+        "decode_roofline": {"bound": "hbm", "kernel": "decode_partial_bf16", "peak": PEAK_HBM_GBPS,
+                            "split": {"cus": sd_cus, "achieved": round(k2_gbps, 1),
+                                      "frac": round(k2_gbps / PEAK_HBM_GBPS, 4),
+                                      "share_peak": round(PEAK_HBM_GBPS * sd_cus / 256, 1),
+                                      "share_frac": round(k2_gbps / (PEAK_HBM_GBPS * sd_cus / 256), 4),
+                                      "probe_share_peak": round(b_share, 1),
+                                      "probe_share_frac": round(k2_gbps / b_share, 4)},
+                            "standalone_256": {"achieved": round(agg_k2_gbps, 1),
+                                               "frac": round(agg_k2_gbps / PEAK_HBM_GBPS, 4)}},
+        "prefill_roofline": {"bound": "mfma", "kernel": "prefill_bf16", "peak": PEAK_BF16_TFLOPS,
+                             "split": {"cus": sp_cus, "achieved": round(pre_tflops, 1),
+                                       "share_peak": round(PEAK_BF16_TFLOPS * sp_cus / 256, 1),
+                                       "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4),
+                                       "probe_share_peak": round(p_share, 1)},
+                             "standalone_256": {"achieved": round(agg_pre_tflops, 1),
+                                                "frac": round(agg_pre_tflops / PEAK_BF16_TFLOPS, 4)}},
         "calibration": calib,
         "cpu_baseline": cpu,
     }
     if sweep is not None:
-        best = min(sweep, key=lambda x: x["iteration_us"])
-        line["sweep_best"] = best
+        line["sweep_best"] = min(sweep, key=lambda x: x["iteration_us"])
         line["sweep"] = sweep
     print(json.dumps(line), flush=True)
     ctx.close()

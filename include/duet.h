@@ -82,7 +82,7 @@ typedef struct {
   int32_t head_dim;     /* d: 64 or 128 */
   int32_t page_size;    /* 16 */
   int32_t dtype;        /* DUET_BF16 or DUET_F32 */
-  int32_t num_layers;   /* L of the latency model: t_total = L * t_attn (attention kernels run one layer) */
+  int32_t num_layers;   /* L: t_total = L * t_attn in the latency model; layers run by duet_attn_iteration */
 } duet_shape;
 
 typedef struct {
@@ -105,13 +105,19 @@ typedef struct {
 } duet_cu_split;
 
 typedef struct {
-  /* Filled by duet_last_kernel_times() when profiling is on: durations of the last
-   * duet_attn_mixed_batch call, measured with HIP events on each kernel's own stream. */
-  double decode_partial_us; /* split-K paged decode kernel */
-  double decode_reduce_us;  /* partial merge kernel */
-  double prefill_us;        /* prefill attention kernel */
-  double decode_total_us;   /* decode stream: partial start to reduce end */
+  /* Filled by duet_last_kernel_times() when profiling is on, for the last duet_attn_mixed_batch
+   * or duet_attn_iteration call, from HIP events on each kernel's own stream.  Per-kernel
+   * durations are means over the call's layers. */
+  double decode_partial_us; /* split-K paged decode kernel, per launch */
+  double decode_reduce_us;  /* partial merge kernel, per launch */
+  double prefill_us;        /* prefill attention kernel, per launch */
+  double decode_total_us;   /* decode half: first partial start to last reduce end (with AGG the
+                               halves interleave on one stream, so the two spans overlap) */
   double iteration_us;      /* fork to join on the caller's stream */
+  double decode_start_us;   /* fork to the start of the first decode partial kernel */
+  double prefill_start_us;  /* fork to the start of the first prefill kernel */
+  double prefill_total_us;  /* prefill half: first prefill start to last prefill end */
+  double layers;            /* number of layers of the call */
 } duet_kernel_times;
 
 typedef struct duet_ctx duet_ctx;
@@ -124,6 +130,11 @@ typedef struct duet_model duet_model;
 int duet_model_create(duet_model** out);
 int duet_model_destroy(duet_model* m);
 
+/* The model's work accounting (Section 4.1): sums over the requests of `kind` (-1 = all) of
+ * F = 4 h_q q (q + c) d + 2 h_q q (q + c) and B = 2 h_q q d b + 2 h_kv (q + c) d b, times
+ * shape->num_layers.  Host only; used to turn measured kernel times into achieved rates. */
+int duet_batch_work(const duet_shape* shape, const duet_batch* batch, int32_t kind, double* flops, double* bytes);
+
 /* Replace the achievable-throughput tables (Section 4.2: profiled once per partition size).
  * cus[i] must be the 32 values 8, 16, ..., 256 in order; flops_per_s and bytes_per_s > 0.
  * Marks the model calibrated. */
@@ -131,9 +142,12 @@ int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const do
                           const double* bytes_per_s);
 int duet_model_get_tables(const duet_model* m, int32_t n, int32_t* cus, double* flops_per_s,
                           double* bytes_per_s);
-/* Kernel efficiencies in (0, 1]: Pi is multiplied by prefill_eff and B by decode_eff before use.
- * Calibrate them so decode latency is never under-predicted (appendix: under-prediction is the
- * harmful direction). */
+/* Spatial-sharing efficiencies in (0, 1]: when a SPLIT batch holds both kinds, the two halves
+ * run at the same time and slow each other down (shared HBM, L2 and power); the prefill half's
+ * Pi is then multiplied by prefill_eff and the decode half's B by decode_eff.  Aggregated
+ * predictions and single-kind batches use the tables as they are.  Calibrate decode_eff so that
+ * decode latency is never under-predicted (appendix: under-prediction is the harmful
+ * direction). */
 int duet_model_set_efficiency(duet_model* m, double prefill_eff, double decode_eff);
 int duet_model_save(const duet_model* m, const char* path); /* small JSON file */
 int duet_model_load(duet_model* m, const char* path);
@@ -166,23 +180,46 @@ int duet_destroy(duet_ctx* ctx);
 /* The context's own latency model (owned by the context; valid until duet_destroy). */
 duet_model* duet_ctx_model(duet_ctx* ctx);
 
-/* Bytes of device workspace duet_attn_mixed_batch needs for this shape and batch: metadata,
- * work lists, split-K partials and an error word.  Host only. */
+/* Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
+ * (shape->num_layers decode work counters) and batch: metadata, work lists, split-K partials
+ * and an error word.  Host only. */
 int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
 
-/* One iteration's attention.  q, k_cache, v_cache, page_table, workspace and out are device
- * pointers.  max_pages_per_req is the row stride of page_table.  Prefill requests go to the
- * MFMA prefill kernel, decode requests to the split-K decode kernel and its reduce kernel.
- * AGG runs decode then prefill on `stream` (all CUs).  SPLIT forks onto two CU-masked streams
- * (decode on the first cus_decode CUs, prefill on the last cus_prefill CUs), dispatching decode
- * first, and joins back onto `stream`.  The result is bit-identical for every split and every
- * placement of the pages: all reduction orders depend on logical token positions only.
- * Page ids read by a kernel outside [0, num_phys_pages) are not dereferenced; they set an error
- * word that duet_check_device_error() reports.  k_decode_steps is not used here (one step). */
+/* One layer's attention over a mixed batch (Section 4.3: prefill and decode of one iteration
+ * multiplexed in space).  q [T, h_q, d] (T = sum of q_len, requests' rows contiguous from
+ * q_start), k_cache [num_phys_pages, h_kv, 16, d] (token-major pages), v_cache
+ * [num_phys_pages, h_kv, d, 16] (dim-major pages), page_table [num_reqs, max_pages_per_req]
+ * int32, workspace and out [T, h_q, d] are device pointers owned by the caller; batch lives in
+ * host memory.  Prefill requests go to the MFMA prefill kernel, decode requests to the split-K
+ * decode kernel and its reduce kernel.  AGG runs decode then prefill on `stream` (all CUs).
+ * SPLIT forks onto two CU-masked streams (decode on the first cus_decode CUs, prefill on the last
+ * cus_prefill CUs) and joins back onto `stream`; work enqueued on `stream` before the call is complete before
+ * either half starts, and work enqueued after it sees the whole output.  The result is
+ * bit-identical for every split and every placement of the pages: all reduction orders depend
+ * on logical token positions only.  Page ids read by a kernel outside [0, num_phys_pages) are
+ * not dereferenced; they set an error word that duet_check_device_error() reports.  Invalid
+ * arguments return DUET_EINVAL / DUET_EUNSUPPORTED / DUET_EWORKSPACE before anything is enqueued.
+ * Calls on one context are serialised by the host (a mutex); the caller must not reuse a
+ * workspace before the call that uses it has finished on `stream`.  k_decode_steps is not used
+ * here (one step). */
 int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
                           const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
                           int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split,
                           void* workspace, size_t workspace_bytes, void* out, void* stream);
+
+/* The attention of a whole serving iteration: shape->num_layers layers (at most 1024) over the
+ * same batch and page table (Section 4.3: each partition runs its phase's layers as one stream of
+ * work; Section 4.1: t_total = L * t_attn).  q, k_cache, v_cache and out are host arrays of
+ * num_layers device pointers, each laid out as in duet_attn_mixed_batch.  The work lists are
+ * built and uploaded once; with SPLIT each half runs its kernels for every layer back to back on
+ * its CU-masked stream (the host enqueues the halves layer by layer, alternating), with one fork
+ * and one join per call; AGG runs layer by layer, decode then prefill, on `stream`.  Layer l's output is bit-identical
+ * to duet_attn_mixed_batch on layer l's pointers. */
+int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* const* q,
+                        const void* const* k_cache, const void* const* v_cache, int64_t num_phys_pages,
+                        const int32_t* page_table, int32_t max_pages_per_req, const duet_batch* batch,
+                        duet_cu_split split, void* workspace, size_t workspace_bytes, void* const* out,
+                        void* stream);
 
 /* Synchronises `stream`, reads the workspace's error word and clears it: DUET_OK or DUET_EPAGE. */
 int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream);
@@ -195,8 +232,9 @@ int duet_gather_kv(duet_ctx* ctx, const duet_shape* shape, int32_t which, const 
                    int32_t req, int32_t kv_len, void* out_contig, void* stream);
 
 /* Profiling level: 0 off; 1 records HIP events at the fork and the join of every
- * duet_attn_mixed_batch call on the caller's stream (iteration latency only); 2 also records
- * events around each kernel on the stream it runs on (these add small gaps between kernels).
+ * duet_attn_mixed_batch / duet_attn_iteration call on the caller's stream (iteration latency
+ * only); 2 also records events around each kernel on the stream it runs on (these add small
+ * gaps between kernels).
  * duet_last_kernel_times() waits for the last call's events and returns the durations (kernel
  * fields are 0 at level 1). */
 int duet_set_profiling(duet_ctx* ctx, int32_t level);

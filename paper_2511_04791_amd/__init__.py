@@ -139,6 +139,15 @@ def choose_cu_split(batch, tbt_slo_us: float, shape: AttnShape, model: Model | N
     return CuSplit(out.mode, out.cus_prefill, out.cus_decode, out.k_decode_steps), us.value, rho.value, flags.value
 
 
+def batch_work(batch, shape: AttnShape, kind: int = -1) -> tuple[float, float]:
+    """The model's (FLOPs, bytes) for the requests of `kind` (-1 = all), shape.num_layers layers."""
+    b = _BatchC(batch)
+    f, by = ctypes.c_double(), ctypes.c_double()
+    N.check(N.lib().duet_batch_work(ctypes.byref(_shape_c(shape)), ctypes.byref(b.c), int(kind), ctypes.byref(f),
+                                    ctypes.byref(by)), "duet_batch_work")
+    return f.value, by.value
+
+
 def workspace_bytes(shape: AttnShape, seq_meta) -> int:
     b = _BatchC(seq_meta)
     n = ctypes.c_size_t()
@@ -189,10 +198,9 @@ class Context:
             self._ws = torch.empty(max(nbytes, 1 << 20), dtype=torch.uint8, device=f"cuda:{self.device}")
         return self._ws
 
-    def attn_mixed_batch(self, q, k_cache, v_cache, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
-                         out=None, workspace=None, stream=None, num_layers: int = 1, check_errors: bool = False):
+    @staticmethod
+    def _check_layer(q, k_cache, v_cache, page_table, b):
         import torch
-        shape = shape_of(q, k_cache, num_layers)
         for t, name in ((q, "q"), (k_cache, "k_cache"), (v_cache, "v_cache"), (page_table, "page_table")):
             if not t.is_cuda or not t.is_contiguous():
                 raise ValueError(f"{name} must be a contiguous device tensor")
@@ -200,12 +208,19 @@ class Context:
             raise TypeError("page_table must be int32")
         if v_cache.shape != (k_cache.shape[0], k_cache.shape[1], k_cache.shape[3], k_cache.shape[2]):
             raise ValueError("v_cache must be [P, h_kv, d, page_size] for k_cache [P, h_kv, page_size, d]")
-        b = _BatchC(seq_meta)
         n_tok = int(b.rows[:, 2].sum()) if len(b.rows) else 0
         if q.shape[0] != n_tok:
             raise ValueError(f"q has {q.shape[0]} rows, the batch schedules {n_tok} tokens")
         if page_table.dim() != 2 or page_table.shape[0] < len(b.rows):
             raise ValueError("page_table must be [R, max_pages] with a row per request")
+
+    def attn_mixed_batch(self, q, k_cache, v_cache, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
+                         out=None, workspace=None, stream=None, num_layers: int = 1, check_errors: bool = False):
+        """One layer (duet_attn_mixed_batch).  num_layers only sizes the workspace and the model."""
+        import torch
+        shape = shape_of(q, k_cache, num_layers)
+        b = _BatchC(seq_meta)
+        self._check_layer(q, k_cache, v_cache, page_table, b)
         need = workspace_bytes(shape, b.rows)
         ws = self.workspace(need) if workspace is None else workspace
         if out is None:
@@ -220,6 +235,36 @@ class Context:
             N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
                     "duet_check_device_error")
         return out
+
+    def attn_iteration(self, qs, k_caches, v_caches, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
+                       outs=None, workspace=None, stream=None, check_errors: bool = False):
+        """All layers of one iteration (duet_attn_iteration): lists of per-layer tensors sharing the
+        batch and the page table.  Returns the list of per-layer outputs."""
+        import torch
+        L = len(qs)
+        if L < 1 or len(k_caches) != L or len(v_caches) != L or (outs is not None and len(outs) != L):
+            raise ValueError("qs, k_caches, v_caches (and outs) must be non-empty lists of equal length")
+        shape = shape_of(qs[0], k_caches[0], L)
+        b = _BatchC(seq_meta)
+        for l in range(L):
+            if qs[l].shape != qs[0].shape or qs[l].dtype != qs[0].dtype or k_caches[l].shape != k_caches[0].shape:
+                raise ValueError(f"layer {l}: shapes differ from layer 0")
+            self._check_layer(qs[l], k_caches[l], v_caches[l], page_table, b)
+        need = workspace_bytes(shape, b.rows)
+        ws = self.workspace(need) if workspace is None else workspace
+        if outs is None:
+            outs = [torch.empty_like(x) for x in qs]
+        arr = lambda ts: (ctypes.c_void_p * L)(*[t.data_ptr() for t in ts])
+        st = torch.cuda.current_stream(qs[0].device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_attn_iteration(self.handle, ctypes.byref(_shape_c(shape)), arr(qs), arr(k_caches),
+                                            arr(v_caches), int(k_caches[0].shape[0]), page_table.data_ptr(),
+                                            int(page_table.shape[1]), ctypes.byref(b.c), cu_split.to_c(),
+                                            ws.data_ptr(), ws.numel(), arr(outs), ctypes.c_void_p(st)),
+                "duet_attn_iteration")
+        if check_errors:
+            N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
+                    "duet_check_device_error")
+        return outs
 
     def gather_kv(self, cache, which: int, page_table, req: int, kv_len: int, shape: AttnShape):
         import torch

@@ -38,13 +38,16 @@ class CuSplit(ctypes.Structure):
 
 class KernelTimes(ctypes.Structure):
     _fields_ = [("decode_partial_us", c_double), ("decode_reduce_us", c_double), ("prefill_us", c_double),
-                ("decode_total_us", c_double), ("iteration_us", c_double)]
+                ("decode_total_us", c_double), ("iteration_us", c_double),
+                ("decode_start_us", c_double), ("prefill_start_us", c_double), ("prefill_total_us", c_double),
+                ("layers", c_double)]
 
 
 P = ctypes.POINTER
 _SIGS = {
     "duet_model_create": (c_int32, [P(c_void_p)]),
     "duet_model_destroy": (c_int32, [c_void_p]),
+    "duet_batch_work": (c_int32, [P(Shape), P(Batch), c_int32, P(c_double), P(c_double)]),
     "duet_model_set_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_get_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_set_efficiency": (c_int32, [c_void_p, c_double, c_double]),
@@ -59,6 +62,8 @@ _SIGS = {
     "duet_workspace_bytes": (c_int32, [P(Shape), P(Batch), P(c_size_t)]),
     "duet_attn_mixed_batch": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),
+    "duet_attn_iteration": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p,
+                                      c_int32, P(Batch), CuSplit, c_void_p, c_size_t, P(c_void_p), c_void_p]),
     "duet_check_device_error": (c_int32, [c_void_p, c_void_p, c_void_p]),
     "duet_gather_kv": (c_int32, [c_void_p, P(Shape), c_int32, c_void_p, c_int64, c_void_p, c_int32, c_int32, c_int32,
                                  c_void_p, c_void_p]),

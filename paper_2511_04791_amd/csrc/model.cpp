@@ -45,11 +45,13 @@ inline ReqCost request_cost(const duet_shape* s, const duet_seq_meta& r) {
 inline int cu_index(int cus) { return cus / DUET_CU_STEP - 1; }
 
 // Seconds for the attention of `num_layers` layers of the requests whose kind matches `kind`
-// (-1 = all) on `cus` CUs.
-double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b, int kind, int cus) {
+// (-1 = all) on `cus` CUs.  `shared`: the half runs while the other half runs on the other CUs,
+// so the spatial-sharing efficiencies apply.
+double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b, int kind, int cus,
+                  bool shared = false) {
   const int i = cu_index(cus);
-  const double pi = m->flops[i] * m->prefill_eff;
-  const double bw = m->bytes[i] * m->decode_eff;
+  const double pi = m->flops[i] * (shared ? m->prefill_eff : 1.0);
+  const double bw = m->bytes[i] * (shared ? m->decode_eff : 1.0);
   double t = 0.0;
   for (int r = 0; r < b->num_reqs; ++r) {
     const duet_seq_meta& rq = b->reqs[r];
@@ -58,6 +60,12 @@ double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b,
     t += std::fmax(rc.flops / pi, rc.bytes / bw);
   }
   return s->num_layers * t;
+}
+
+bool has_both_kinds(const duet_batch* b) {
+  bool d = false, p = false;
+  for (int r = 0; r < b->num_reqs; ++r) (b->reqs[r].kind == DUET_KIND_DECODE ? d : p) = true;
+  return d && p;
 }
 
 const duet_model* model_or_nominal(const duet_model* m, duet_model* storage) {
@@ -159,6 +167,25 @@ int duet_model_create(duet_model** out) {
 
 int duet_model_destroy(duet_model* m) {
   delete m;
+  return DUET_OK;
+}
+
+int duet_batch_work(const duet_shape* shape, const duet_batch* batch, int32_t kind, double* flops, double* bytes) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if (!flops || !bytes) return fail(DUET_EINVAL, "NULL output");
+  if (kind != -1 && kind != DUET_KIND_PREFILL && kind != DUET_KIND_DECODE) return fail(DUET_EINVAL, "kind %d", kind);
+  double f = 0.0, b = 0.0;
+  for (int r = 0; r < batch->num_reqs; ++r) {
+    if (kind >= 0 && batch->reqs[r].kind != kind) continue;
+    const ReqCost c = request_cost(shape, batch->reqs[r]);
+    f += c.flops;
+    b += c.bytes;
+  }
+  *flops = shape->num_layers * f;
+  *bytes = shape->num_layers * b;
   return DUET_OK;
 }
 
@@ -308,8 +335,9 @@ int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, cons
   if (split.mode == DUET_AGG) {
     t = f_roofline(mm, shape, batch, -1, DUET_TOTAL_CUS);
   } else {
-    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, split.cus_decode);
-    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, split.cus_prefill);
+    const bool shared = has_both_kinds(batch);
+    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, split.cus_decode, shared);
+    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, split.cus_prefill, shared);
     t = std::fmax(split.k_decode_steps * td, tp);
   }
   *us = t * 1e6;
@@ -345,11 +373,12 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
   }
   double best_rho = 0.0, best_t = 0.0;
   duet_cu_split best{-1, 0, 0, 0};
+  const bool shared = has_both_kinds(batch);
   for (int sd = DUET_CU_STEP; sd < DUET_TOTAL_CUS; sd += DUET_CU_STEP) {
-    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, sd);
+    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, sd, shared);
     if (td > tau) continue;
     const int sp = DUET_TOTAL_CUS - sd;
-    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, sp);
+    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, sp, shared);
     const double base = td > 0.0 ? std::floor(tp / td) : 1.0;
     for (int j = 0; j < 2; ++j) {
       const double k = base + j;

@@ -33,6 +33,10 @@ using namespace duet;
 constexpr int kStagingSlots = 4;
 constexpr size_t kMaxMaskedStreams = 6;  // each CU-masked stream owns a hardware queue
 constexpr size_t kAlign = 256;
+// Workspace head: the device error word at offset 0, one decode work counter per layer from
+// kCounterOffset on; the head is zeroed by every call's upload.
+constexpr size_t kCounterOffset = 64;
+constexpr int kMaxLayers = 1024;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
@@ -63,7 +67,7 @@ int pages_per_split_for(const duet_shape* s) {
   return s->dtype == DUET_F32 ? kDecodePagesPerSplitF32 : kDecodePagesPerSplit;
 }
 
-void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
+void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, bool fill) {
   const int g = s->num_q_heads / s->num_kv_heads;
   const int pps = pages_per_split_for(s);
   p->group = g;
@@ -134,7 +138,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
   }
   p->n_items_decode = (int)n_items;
   p->max_split = max_split;
-  size_t off = kAlign;  // error word lives at offset 0
+  size_t off = align_up(kCounterOffset + (size_t)layers * sizeof(int32_t));
   p->off_meta = off;
   off = align_up(off + (size_t)b->num_reqs * sizeof(int4));
   p->off_pitems = off;
@@ -151,7 +155,8 @@ void plan_batch(const duet_shape* s, const duet_batch* b, Plan* p, bool fill) {
   p->total = off;
 }
 
-enum ProfEv { kEvFork, kEvD0, kEvD1, kEvD2, kEvP0, kEvP1, kEvJoin, kNumProfEv };
+// Fork and join of a profiled call on the caller's stream; A and B bracket probe kernels.
+enum ProfEv { kEvFork, kEvJoin, kEvA, kEvB, kNumProfEv };
 
 }  // namespace
 
@@ -168,6 +173,11 @@ struct duet_ctx {
   int profiling = 0;  // 0 off, 1 iteration events only, 2 also per-kernel events
   bool prof_valid = false;
   bool prof_decode = false, prof_prefill = false, prof_kernels = false;
+  int prof_layers = 0;
+  // Per-layer kernel brackets of a profiled call: decode layer l uses events 3l (before the
+  // partial kernel), 3l+1 (between partial and reduce) and 3l+2 (after the reduce); prefill
+  // layer l uses 2l (before) and 2l+1 (after).
+  std::vector<hipEvent_t> ev_dec, ev_pre;
   StagingSlot slots[kStagingSlots];
   int next_slot = 0;
   int32_t* dev_flag = nullptr;  // gather error word
@@ -212,6 +222,20 @@ int get_stream(duet_ctx* ctx, int cus, int high_end, hipStream_t* out) {
   return DUET_OK;
 }
 
+int ensure_layer_events(duet_ctx* ctx, int layers) {
+  while (ctx->ev_dec.size() < (size_t)(3 * layers)) {
+    hipEvent_t e = nullptr;
+    HIP_TRY(hipEventCreate(&e));
+    ctx->ev_dec.push_back(e);
+  }
+  while (ctx->ev_pre.size() < (size_t)(2 * layers)) {
+    hipEvent_t e = nullptr;
+    HIP_TRY(hipEventCreate(&e));
+    ctx->ev_pre.push_back(e);
+  }
+  return DUET_OK;
+}
+
 int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
   StagingSlot& slot = ctx->slots[ctx->next_slot];
   ctx->next_slot = (ctx->next_slot + 1) % kStagingSlots;
@@ -229,7 +253,7 @@ int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
     slot.cap = cap;
   }
   char* h = static_cast<char*>(slot.host);
-  std::memset(h, 0, kAlign);  // clears the error word and the decode work counter
+  std::memset(h, 0, p.off_meta);  // clears the error word and the decode work counters
   std::memcpy(h + p.off_meta, p.meta.data(), p.meta.size() * sizeof(int4));
   std::memcpy(h + p.off_pitems, p.pitems.data(), p.pitems.size() * sizeof(int4));
   std::memcpy(h + p.off_dreq, p.dreq.data(), p.dreq.size() * sizeof(int4));
@@ -245,104 +269,29 @@ int check_device_ptr(const void* p, const char* name) {
   return DUET_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-int duet_init(int device, duet_ctx** out) {
-  clear_error();
-  if (!out) return fail(DUET_EINVAL, "out is NULL");
-  *out = nullptr;
-  int n = 0;
-  HIP_TRY(hipGetDeviceCount(&n));
-  if (device < 0 || device >= n) return fail(DUET_EINVAL, "device %d not in [0, %d)", device, n);
-  hipDeviceProp_t prop;
-  HIP_TRY(hipGetDeviceProperties(&prop, device));
-  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
-    return fail(DUET_EUNSUPPORTED, "device %d is %s, the kernels are built for gfx950", device, prop.gcnArchName);
-  if (prop.multiProcessorCount != DUET_TOTAL_CUS)
-    return fail(DUET_EUNSUPPORTED, "device has %d CUs; CU splits assume %d (single-partition mode)",
-                prop.multiProcessorCount, DUET_TOTAL_CUS);
-  duet_ctx* ctx = new (std::nothrow) duet_ctx;
-  if (!ctx) return fail(DUET_ENOMEM, "context allocation failed");
-  ctx->device = device;
-  ctx->num_cus = prop.multiProcessorCount;
-  model_init_nominal(&ctx->model);
-  auto cleanup = [&](int rc) {
-    duet_destroy(ctx);
-    return rc;
-  };
-  if (hipSetDevice(device) != hipSuccess) return cleanup(fail(DUET_EHIP, "hipSetDevice failed"));
-  if (hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_djoin, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ctx->ev_pjoin, hipEventDisableTiming) != hipSuccess)
-    return cleanup(fail(DUET_EHIP, "event creation failed"));
-  for (auto& e : ctx->prof)
-    if (hipEventCreate(&e) != hipSuccess) return cleanup(fail(DUET_EHIP, "event creation failed"));
-  for (auto& s : ctx->slots)
-    if (hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
-      return cleanup(fail(DUET_EHIP, "event creation failed"));
-  if (hipMalloc(&ctx->dev_flag, 256) != hipSuccess || hipMemset(ctx->dev_flag, 0, 256) != hipSuccess)
-    return cleanup(fail(DUET_EHIP, "device flag allocation failed"));
-  ctx->dev_sink = reinterpret_cast<unsigned*>(ctx->dev_flag) + 16;
-  *out = ctx;
-  return DUET_OK;
-}
-
-int duet_destroy(duet_ctx* ctx) {
-  if (!ctx) return DUET_OK;
-  (void)hipSetDevice(ctx->device);
-  for (auto& kv : ctx->streams) {
-    (void)hipStreamSynchronize(kv.second);
-    (void)hipStreamDestroy(kv.second);
-  }
-  for (auto& s : ctx->slots) {
-    if (s.done) {
-      if (s.pending) (void)hipEventSynchronize(s.done);
-      (void)hipEventDestroy(s.done);
-    }
-    if (s.host) (void)hipHostFree(s.host);
-  }
-  for (auto& e : ctx->prof)
-    if (e) (void)hipEventDestroy(e);
-  if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
-  if (ctx->ev_djoin) (void)hipEventDestroy(ctx->ev_djoin);
-  if (ctx->ev_pjoin) (void)hipEventDestroy(ctx->ev_pjoin);
-  if (ctx->dev_flag) (void)hipFree(ctx->dev_flag);
-  delete ctx;
-  return DUET_OK;
-}
-
-duet_model* duet_ctx_model(duet_ctx* ctx) { return ctx ? &ctx->model : nullptr; }
-
-int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes) {
-  clear_error();
-  int rc = check_shape(shape);
-  if (rc) return rc;
-  if ((rc = check_batch(shape, batch, false))) return rc;
-  if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
-  Plan p;
-  plan_batch(shape, batch, &p, false);
-  *bytes = p.total;
-  return DUET_OK;
-}
-
-int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
-                          const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
-                          int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
-                          size_t workspace_bytes, void* out, void* stream) {
-  clear_error();
+// One call over `layers` layers that share the batch, its page table and its work lists.  Each
+// half runs its kernels for every layer back to back on its own stream; one fork and one join
+// per call.
+int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* const* q_l,
+                const void* const* k_l, const void* const* v_l, int64_t num_phys_pages, const int32_t* page_table,
+                int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                size_t workspace_bytes, void* const* out_l, void* stream) {
   if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_batch(shape, batch, true))) return rc;
-  if ((rc = check_device_ptr(q, "q")) || (rc = check_device_ptr(k_cache, "k_cache")) ||
-      (rc = check_device_ptr(v_cache, "v_cache")) || (rc = check_device_ptr(page_table, "page_table")) ||
-      (rc = check_device_ptr(workspace, "workspace")) || (rc = check_device_ptr(out, "out")))
+  if (layers < 1 || layers > kMaxLayers) return fail(DUET_EINVAL, "num_layers %d not in [1, %d]", layers, kMaxLayers);
+  if ((rc = check_device_ptr(page_table, "page_table")) || (rc = check_device_ptr(workspace, "workspace")))
     return rc;
+  for (int l = 0; l < layers; ++l) {
+    if ((rc = check_device_ptr(q_l[l], "q")) || (rc = check_device_ptr(k_l[l], "k_cache")) ||
+        (rc = check_device_ptr(v_l[l], "v_cache")) || (rc = check_device_ptr(out_l[l], "out")))
+      return rc;
+    if (out_l[l] == q_l[l] || out_l[l] == k_l[l] || out_l[l] == v_l[l])
+      return fail(DUET_EINVAL, "layer %d: out aliases an input", l);
+  }
   if (num_phys_pages < 1 || num_phys_pages > (int64_t)INT32_MAX)
     return fail(DUET_EINVAL, "num_phys_pages %lld out of range", (long long)num_phys_pages);
-  if (out == q || out == k_cache || out == v_cache) return fail(DUET_EINVAL, "out aliases an input");
   for (int r = 0; r < batch->num_reqs; ++r) {
     const int64_t L = (int64_t)batch->reqs[r].cached_len + batch->reqs[r].q_len;
     if ((L + 15) / 16 > max_pages_per_req)
@@ -375,7 +324,7 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
 
   std::lock_guard<std::mutex> lock(ctx->mu);
   Plan& p = ctx->plan;
-  plan_batch(shape, batch, &p, true);
+  plan_batch(shape, batch, layers, &p, true);
   if (workspace_bytes < p.total)
     return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, p.total);
 
@@ -389,11 +338,7 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
 
   char* ws = static_cast<char*>(workspace);
   AttnArgs a;
-  a.q = q;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
   a.page_table = page_table;
-  a.out = out;
   a.num_phys_pages = num_phys_pages;
   a.max_pages = max_pages_per_req;
   a.h_q = shape->num_q_heads;
@@ -410,7 +355,6 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
   w.pml = reinterpret_cast<float*>(ws + p.off_pml);
   w.ditems = reinterpret_cast<const int32_t*>(ws + p.off_ditems);
   w.err = reinterpret_cast<int32_t*>(ws);
-  w.work_counter = reinterpret_cast<int32_t*>(ws) + 16;
   w.n_ditems = (int)p.ditems.size();
   w.decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
   w.n_pitems = (int)p.pitems.size();
@@ -423,23 +367,40 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
 
   if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
   if ((rc = stage_upload(ctx, p, ws, order))) return rc;
+  auto layer_args = [&](int l) {
+    AttnArgs al = a;
+    al.q = q_l[l];
+    al.k_cache = k_l[l];
+    al.v_cache = v_l[l];
+    al.out = out_l[l];
+    return al;
+  };
+  if (prof && (rc = ensure_layer_events(ctx, layers))) return rc;
+  // Aggregated execution runs each layer's decode kernels, then its prefill kernel, on the
+  // caller's stream.  Spatial sharing forks both CU-masked streams off the caller's stream and
+  // enqueues the two halves layer by layer, alternating, so neither half waits for the host to
+  // finish enqueueing the other.
   if (split.mode == DUET_SPLIT) {
     HIP_TRY(hipEventRecord(ctx->ev_fork, order));
-    HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
-    HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
+    if (has_decode) HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
+    if (has_prefill) HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
   }
-  // Decode first (Section 4.3), then prefill.
-  if (has_decode) {
-    if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvD0], sd));
-    HIP_TRY(launch_decode_partial(a, w, sd));
-    if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvD1], sd));
-    HIP_TRY(launch_decode_reduce(a, w, sd));
-    if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvD2], sd));
-  }
-  if (has_prefill) {
-    if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvP0], sp));
-    HIP_TRY(launch_prefill(a, w, sp));
-    if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvP1], sp));
+  for (int l = 0; l < layers; ++l) {
+    const AttnArgs al = layer_args(l);
+    if (has_decode) {
+      WorkArgs wl = w;
+      wl.work_counter = reinterpret_cast<int32_t*>(ws + kCounterOffset) + l;
+      if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l], sd));
+      HIP_TRY(launch_decode_partial(al, wl, sd));
+      if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 1], sd));
+      HIP_TRY(launch_decode_reduce(al, wl, sd));
+      if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 2], sd));
+    }
+    if (has_prefill) {
+      if (prof) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l], sp));
+      HIP_TRY(launch_prefill(al, w, sp));
+      if (prof) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l + 1], sp));
+    }
   }
   if (split.mode == DUET_SPLIT) {
     HIP_TRY(hipEventRecord(ctx->ev_djoin, sd));
@@ -452,7 +413,113 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
   ctx->prof_kernels = prof;
   ctx->prof_decode = has_decode;
   ctx->prof_prefill = has_prefill;
+  ctx->prof_layers = layers;
   return DUET_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int duet_init(int device, duet_ctx** out) {
+  clear_error();
+  if (!out) return fail(DUET_EINVAL, "out is NULL");
+  *out = nullptr;
+  int n = 0;
+  HIP_TRY(hipGetDeviceCount(&n));
+  if (device < 0 || device >= n) return fail(DUET_EINVAL, "device %d not in [0, %d)", device, n);
+  hipDeviceProp_t prop;
+  HIP_TRY(hipGetDeviceProperties(&prop, device));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(DUET_EUNSUPPORTED, "device %d is %s, the kernels are built for gfx950", device, prop.gcnArchName);
+  if (prop.multiProcessorCount != DUET_TOTAL_CUS)
+    return fail(DUET_EUNSUPPORTED, "device has %d CUs; CU splits assume %d (single-partition mode)",
+                prop.multiProcessorCount, DUET_TOTAL_CUS);
+  duet_ctx* ctx = new (std::nothrow) duet_ctx;
+  if (!ctx) return fail(DUET_ENOMEM, "context allocation failed");
+  ctx->device = device;
+  ctx->num_cus = prop.multiProcessorCount;
+  model_init_nominal(&ctx->model);
+  auto cleanup = [&](int rc) {
+    duet_destroy(ctx);
+    return rc;
+  };
+  if (hipSetDevice(device) != hipSuccess) return cleanup(fail(DUET_EHIP, "hipSetDevice failed"));
+  const unsigned ev_flags = hipEventDisableTiming;
+  if (hipEventCreateWithFlags(&ctx->ev_fork, ev_flags) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_djoin, ev_flags) != hipSuccess ||
+      hipEventCreateWithFlags(&ctx->ev_pjoin, ev_flags) != hipSuccess)
+    return cleanup(fail(DUET_EHIP, "event creation failed"));
+  for (auto& e : ctx->prof)
+    if (hipEventCreate(&e) != hipSuccess) return cleanup(fail(DUET_EHIP, "event creation failed"));
+  for (auto& s : ctx->slots)
+    if (hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
+      return cleanup(fail(DUET_EHIP, "event creation failed"));
+  if (hipMalloc(&ctx->dev_flag, 256) != hipSuccess || hipMemset(ctx->dev_flag, 0, 256) != hipSuccess)
+    return cleanup(fail(DUET_EHIP, "device flag allocation failed"));
+  ctx->dev_sink = reinterpret_cast<unsigned*>(ctx->dev_flag) + 16;
+  *out = ctx;
+  return DUET_OK;
+}
+
+int duet_destroy(duet_ctx* ctx) {
+  if (!ctx) return DUET_OK;
+  (void)hipSetDevice(ctx->device);
+  for (auto& kv : ctx->streams) {
+    (void)hipStreamSynchronize(kv.second);
+    (void)hipStreamDestroy(kv.second);
+  }
+  for (auto& s : ctx->slots) {
+    if (s.done) {
+      if (s.pending) (void)hipEventSynchronize(s.done);
+      (void)hipEventDestroy(s.done);
+    }
+    if (s.host) (void)hipHostFree(s.host);
+  }
+  for (auto& e : ctx->prof)
+    if (e) (void)hipEventDestroy(e);
+  for (auto& e : ctx->ev_dec) (void)hipEventDestroy(e);
+  for (auto& e : ctx->ev_pre) (void)hipEventDestroy(e);
+  if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
+  if (ctx->ev_djoin) (void)hipEventDestroy(ctx->ev_djoin);
+  if (ctx->ev_pjoin) (void)hipEventDestroy(ctx->ev_pjoin);
+  if (ctx->dev_flag) (void)hipFree(ctx->dev_flag);
+  delete ctx;
+  return DUET_OK;
+}
+
+duet_model* duet_ctx_model(duet_ctx* ctx) { return ctx ? &ctx->model : nullptr; }
+
+int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
+  Plan p;
+  plan_batch(shape, batch, shape->num_layers, &p, false);
+  *bytes = p.total;
+  return DUET_OK;
+}
+
+int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
+                          const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                          int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                          size_t workspace_bytes, void* out, void* stream) {
+  clear_error();
+  return attn_layers(ctx, shape, 1, &q, &k_cache, &v_cache, num_phys_pages, page_table, max_pages_per_req, batch,
+                     split, workspace, workspace_bytes, &out, stream);
+}
+
+int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* const* q, const void* const* k_cache,
+                        const void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                        size_t workspace_bytes, void* const* out, void* stream) {
+  clear_error();
+  if (!shape) return fail(DUET_EINVAL, "shape is NULL");
+  if (!q || !k_cache || !v_cache || !out) return fail(DUET_EINVAL, "per-layer pointer array is NULL");
+  return attn_layers(ctx, shape, shape->num_layers, q, k_cache, v_cache, num_phys_pages, page_table,
+                     max_pages_per_req, batch, split, workspace, workspace_bytes, out, stream);
 }
 
 int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream) {
@@ -510,22 +577,39 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
   if (!ctx->prof_valid) return fail(DUET_EINVAL, "no profiled call recorded");
   HIP_TRY(hipEventSynchronize(ctx->prof[kEvJoin]));
   float ms = 0.f;
+  auto span_us = [&](hipEvent_t x, hipEvent_t y, double* us) -> int {
+    HIP_TRY(hipEventElapsedTime(&ms, x, y));
+    *us = ms * 1e3;
+    return DUET_OK;
+  };
   std::memset(out, 0, sizeof *out);
+  const int L = ctx->prof_layers;
+  out->layers = L;
+  int rc;
   if (ctx->prof_kernels && ctx->prof_decode) {
-    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD1]));
-    out->decode_partial_us = ms * 1e3;
-    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD1], ctx->prof[kEvD2]));
-    out->decode_reduce_us = ms * 1e3;
-    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD2]));
-    out->decode_total_us = ms * 1e3;
+    const std::vector<hipEvent_t>& e = ctx->ev_dec;
+    for (int l = 0; l < L; ++l) {
+      double part = 0.0, red = 0.0;
+      if ((rc = span_us(e[3 * l], e[3 * l + 1], &part)) || (rc = span_us(e[3 * l + 1], e[3 * l + 2], &red))) return rc;
+      out->decode_partial_us += part / L;
+      out->decode_reduce_us += red / L;
+    }
+    if ((rc = span_us(e[0], e[3 * L - 1], &out->decode_total_us)) ||
+        (rc = span_us(ctx->prof[kEvFork], e[0], &out->decode_start_us)))
+      return rc;
   }
   if (ctx->prof_kernels && ctx->prof_prefill) {
-    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvP0], ctx->prof[kEvP1]));
-    out->prefill_us = ms * 1e3;
+    const std::vector<hipEvent_t>& e = ctx->ev_pre;
+    for (int l = 0; l < L; ++l) {
+      double t = 0.0;
+      if ((rc = span_us(e[2 * l], e[2 * l + 1], &t))) return rc;
+      out->prefill_us += t / L;
+    }
+    if ((rc = span_us(e[0], e[2 * L - 1], &out->prefill_total_us)) ||
+        (rc = span_us(ctx->prof[kEvFork], e[0], &out->prefill_start_us)))
+      return rc;
   }
-  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvFork], ctx->prof[kEvJoin]));
-  out->iteration_us = ms * 1e3;
-  return DUET_OK;
+  return span_us(ctx->prof[kEvFork], ctx->prof[kEvJoin], &out->iteration_us);
 }
 
 int duet_probe_read_bw(duet_ctx* ctx, int32_t cus, const void* buf, size_t bytes, int32_t iters,
@@ -539,12 +623,12 @@ int duet_probe_read_bw(duet_ctx* ctx, int32_t cus, const void* buf, size_t bytes
   if (rc) return rc;
   const int blocks = cus * 8;
   HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));  // warm-up
-  HIP_TRY(hipEventRecord(ctx->prof[kEvD0], st));
+  HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
   for (int i = 0; i < iters; ++i) HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvD1], st));
-  HIP_TRY(hipEventSynchronize(ctx->prof[kEvD1]));
+  HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
+  HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
   float ms = 0.f;
-  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD1]));
+  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
   ctx->prof_valid = false;
   *bytes_per_s = (double)(bytes / 16 * 16) * iters / (ms * 1e-3);
   return DUET_OK;
@@ -561,12 +645,12 @@ int duet_probe_mfma(duet_ctx* ctx, int32_t cus, int32_t iters, double* flops_per
   const int blocks = cus * 2;  // 8 waves per CU, two per SIMD
   float* sink = reinterpret_cast<float*>(ctx->dev_sink);
   HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvD0], st));
+  HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
   HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvD1], st));
-  HIP_TRY(hipEventSynchronize(ctx->prof[kEvD1]));
+  HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
+  HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
   float ms = 0.f;
-  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvD0], ctx->prof[kEvD1]));
+  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
   ctx->prof_valid = false;
   const double flops = (double)blocks * 4 /*waves*/ * iters * 4 /*chains*/ * (32.0 * 32 * 16 * 2);
   *flops_per_s = flops / (ms * 1e-3);

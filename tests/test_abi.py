@@ -78,3 +78,24 @@ def test_workspace_grows_with_decode_splits(native):
     # 30001 keys = 1876 pages = 59 splits of 32 pages (the library's fixed bf16 split length);
     # each split stores 4 heads x (128 + 2) floats per kv head
     assert c.value - a.value >= (59 - 1) * 8 * 4 * 130 * 4
+
+
+def test_iteration_rejects_bad_layer_arguments(native):
+    arr, b = _batch([(1, 0, 1, 10)])
+    ptrs = (ctypes.c_void_p * 2)(1, 1)
+    args = (1, 1, ctypes.byref(b), N.CuSplit(0, 256, 0, 1), 1, 1 << 20, ptrs, None)
+    assert native.duet_attn_iteration(None, ctypes.byref(_shape(num_layers=2)), ptrs, ptrs, ptrs, 10, *args) == -1
+    assert b"ctx" in native.duet_last_error()
+    assert native.duet_attn_iteration(None, None, ptrs, ptrs, ptrs, 10, *args) == -1
+    assert b"shape" in native.duet_last_error()
+    assert native.duet_attn_iteration(None, ctypes.byref(_shape(num_layers=2)), None, ptrs, ptrs, 10, *args) == -1
+    assert b"array" in native.duet_last_error()
+
+
+def test_workspace_holds_a_counter_per_layer(native):
+    arr, b = _batch([(1, 0, 1, 100)])
+    one, many = ctypes.c_size_t(), ctypes.c_size_t()
+    assert native.duet_workspace_bytes(ctypes.byref(_shape(num_layers=1)), ctypes.byref(b), ctypes.byref(one)) == 0
+    assert native.duet_workspace_bytes(ctypes.byref(_shape(num_layers=200)), ctypes.byref(b), ctypes.byref(many)) == 0
+    # 200 four-byte counters where one layer's counter fits the 256-byte head
+    assert many.value - one.value >= 200 * 4 - 256

@@ -180,3 +180,34 @@ def test_host_validation_launches_nothing(ctx):
         ctx.attn_mixed_batch(q, kc, vc, pt, b.seq_meta, duet.CuSplit.split(200, 100), out=out)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_iteration_layers_match_single_layer_calls(ctx, dtype):
+    """duet_attn_iteration over L layers with distinct inputs equals L single-layer calls bit for
+    bit, aggregated and split; layer 0 also against the oracle."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    sh = wl.LLAMA3_8B if dtype == "bf16" else wl.TINY_F32
+    b = wl.make_batch(sh, [(0, 300, 37), (1, 1, 700), (1, 1, 16), (1, 1, 2100), (0, 5, 0)], page_seed=77)
+    L = 3
+    layers = [_case(b, seed=3300 + l, gen_device="cpu") for l in range(L)]
+    qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
+    pt = layers[0][3]
+    singles = [_run(ctx, b, *layers[l]) for l in range(L)]
+    for sp in (duet.CuSplit.agg(), duet.CuSplit.split(96, 160)):
+        ctx.set_profiling(2)
+        outs = ctx.attn_iteration(qs, kcs, vcs, pt, b.seq_meta, sp, check_errors=True)
+        t = ctx.last_kernel_times()
+        ctx.set_profiling(0)
+        torch.cuda.synchronize()
+        for l in range(L):
+            assert torch.equal(outs[l], singles[l]), f"layer {l} {sp}"
+        assert t["layers"] == L and t["decode_partial_us"] > 0 and t["prefill_us"] > 0
+        assert t["iteration_us"] >= max(t["decode_total_us"], t["prefill_total_us"])
+    mx, mean = errors(singles[0], oracle_out(b, qs[0], kcs[0], vcs[0]))
+    _report(f"iteration layer 0 {dtype}", mx, mean)
+    if dtype == "f32":
+        assert mx <= F32_MAX_ABS
+    else:
+        assert mx <= BF16_MAX_ABS and mean <= BF16_MEAN_ABS

@@ -86,13 +86,21 @@ def test_null_model_is_nominal_and_flagged():
     assert sp.mode == duet.AGG and flags & duet.STATUS_UNCALIBRATED
 
 
-def test_efficiency_scales_prediction():
+def test_sharing_efficiency_scales_split_halves_only():
     shape = wl.LLAMA3_8B
-    rows = [(1, 1, 3000)] * 16
+    dec = [(1, 1, 3000)] * 16
+    pre = [(0, 4096, 0)]
     m = duet.Model()
-    base = duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape, m)
-    m.set_efficiency(1.0, 0.5)
-    assert duet.predict_iter_latency(rows, duet.CuSplit.agg(), shape, m) == pytest.approx(2 * base, rel=1e-12)
+    sp = duet.CuSplit.split(128, 128)
+    agg = duet.predict_iter_latency(dec + pre, duet.CuSplit.agg(), shape, m)
+    t_d = duet.predict_iter_latency(dec, sp, shape, m)
+    t_p = duet.predict_iter_latency(pre, sp, shape, m)
+    m.set_efficiency(0.5, 0.25)
+    # both kinds: each half slowed by its efficiency, the iteration by the slower half
+    assert duet.predict_iter_latency(dec + pre, sp, shape, m) == pytest.approx(max(4 * t_d, 2 * t_p), rel=1e-12)
+    # aggregated execution and single-kind batches are not shared
+    assert duet.predict_iter_latency(dec + pre, duet.CuSplit.agg(), shape, m) == pytest.approx(agg, rel=1e-12)
+    assert duet.predict_iter_latency(dec, sp, shape, m) == pytest.approx(t_d, rel=1e-12)
     with pytest.raises(duet.DuetError):
         m.set_efficiency(0.0, 1.0)
 
@@ -126,3 +134,18 @@ def test_choose_is_fast():
     for _ in range(50):
         duet.choose_cu_split(rows, 1000.0, shape)
     assert (time.perf_counter() - t0) / 50 < 1e-3
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_batch_work_matches_oracle_accounting(seed):
+    """duet_batch_work sums the oracle's per-request F and B (Section 4.1) over a kind, x L."""
+    rng = np.random.default_rng(300 + seed)
+    rows = _batch(rng)
+    sh = wl.AttnShape(32, 8, 128, "bf16", num_layers=int(rng.integers(1, 40)))
+    for kind in (-1, 0, 1):
+        sel = [r for r in rows if kind < 0 or r[0] == kind]
+        f_want = sh.num_layers * sum(orf.attn_flops(q, c, 32, 128) for _, q, c in sel)
+        b_want = sh.num_layers * sum(orf.attn_bytes(q, c, 32, 8, 128, 2) for _, q, c in sel)
+        f, b = duet.batch_work(rows, sh, kind)
+        assert f == pytest.approx(f_want, rel=1e-12, abs=0.0)
+        assert b == pytest.approx(b_want, rel=1e-12, abs=0.0)
