@@ -145,6 +145,8 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the S_p = 24..232 step-8 split sweep")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibrate", action="store_true")
+    ap.add_argument("--no-agg", action="store_true",
+                    help="skip the aggregated reference passes (every launch then runs in the timed mode)")
     ap.add_argument("--copy-reference", action="store_true",
                     help="end with a plain 1 GiB device-to-device copy, the reference for HBM counters")
     args = ap.parse_args()
@@ -230,15 +232,18 @@ def main():
 
     n_prof = max(5, args.steps // 2)
     it = profiled(n_prof, 2, 1, used)
-    agg_it = profiled(n_prof, 2, 1, duet.CuSplit.agg())
     kern = profiled(n_prof, 2, 2, used)
-    agg_kern = profiled(n_prof, 2, 2, duet.CuSplit.agg())
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(duet.CuSplit.agg())
-    torch.cuda.synchronize()
-    agg_wall = (time.perf_counter() - t0) / args.steps
+    if args.no_agg:
+        agg_it = agg_kern = agg_wall = None
+    else:
+        agg_it = profiled(n_prof, 2, 1, duet.CuSplit.agg())
+        agg_kern = profiled(n_prof, 2, 2, duet.CuSplit.agg())
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step(duet.CuSplit.agg())
+        torch.cuda.synchronize()
+        agg_wall = (time.perf_counter() - t0) / args.steps
 
     sp_cus = used.cus_prefill if used.mode == duet.SPLIT else 256
     sd_cus = used.cus_decode if used.mode == duet.SPLIT else 256
@@ -248,8 +253,9 @@ def main():
     k2_gbps = dbytes / (k2 * 1e-6) / 1e9
     dec_gbps = dbytes * L / (kern["decode_total_us"] * 1e-6) / 1e9
     pre_tflops = pflops / (k1 * 1e-6) / 1e12
-    agg_k2_gbps = dbytes / (agg_kern["decode_partial_us"] * 1e-6) / 1e9
-    agg_pre_tflops = pflops / (agg_kern["prefill_us"] * 1e-6) / 1e12
+    agg_k2_gbps = dbytes / (agg_kern["decode_partial_us"] * 1e-6) / 1e9 if agg_kern else None
+    agg_pre_tflops = pflops / (agg_kern["prefill_us"] * 1e-6) / 1e12 if agg_kern else None
+    rnd = lambda x, n: None if x is None else round(x, n)
     # hardware ceiling of each share: the probes' streaming read and MFMA loop (nominal
     # 8 TB/s and 2.5 PFLOP/s pro rata without calibration)
     if calib:
@@ -315,9 +321,9 @@ def main():
                                "128, page 16, pages randomly placed",
                    "layers": L, "mode": args.mode, "split": str(used), "tbt_slo_us": round(tau, 1)},
         "iteration_us": round(it["iteration_us"], 1),
-        "agg_us": round(agg_wall * 1e6, 1),
-        "agg_iteration_us": round(agg_it["iteration_us"], 1),
-        "speedup_vs_agg": round(agg_wall / wall, 4),
+        "agg_us": rnd(agg_wall and agg_wall * 1e6, 1),
+        "agg_iteration_us": rnd(agg_it and agg_it["iteration_us"], 1),
+        "speedup_vs_agg": rnd(agg_wall and agg_wall / wall, 4),
         "agg_pred_us": round(agg_pred, 1),
         "chosen_pred_us": round(duet.predict_iter_latency(rows3, used, shape, ctx.model), 1),
         "host_choose_us": round(choose_mean, 2),
@@ -325,7 +331,7 @@ def main():
         "decode_partial_gbps": round(k2_gbps, 1),
         "prefill_mfma_tflops": round(pre_tflops, 1),
         "kernels_us": {k.replace("_us", ""): round(v, 2) for k, v in kern.items()},
-        "agg_kernels_us": {k.replace("_us", ""): round(v, 2) for k, v in agg_kern.items()},
+        "agg_kernels_us": agg_kern and {k.replace("_us", ""): round(v, 2) for k, v in agg_kern.items()},
         "roofline": roofline,
         "decode_roofline": {"bound": "hbm", "kernel": "decode_partial_bf16", "peak": PEAK_HBM_GBPS,
                             "split": {"cus": sd_cus, "achieved": round(k2_gbps, 1),
@@ -334,15 +340,15 @@ def main():
                                       "share_frac": round(k2_gbps / (PEAK_HBM_GBPS * sd_cus / 256), 4),
                                       "probe_share_peak": round(b_share, 1),
                                       "probe_share_frac": round(k2_gbps / b_share, 4)},
-                            "standalone_256": {"achieved": round(agg_k2_gbps, 1),
-                                               "frac": round(agg_k2_gbps / PEAK_HBM_GBPS, 4)}},
+                            "standalone_256": {"achieved": rnd(agg_k2_gbps, 1),
+                                               "frac": rnd(agg_k2_gbps and agg_k2_gbps / PEAK_HBM_GBPS, 4)}},
         "prefill_roofline": {"bound": "mfma", "kernel": "prefill_bf16", "peak": PEAK_BF16_TFLOPS,
                              "split": {"cus": sp_cus, "achieved": round(pre_tflops, 1),
                                        "share_peak": round(PEAK_BF16_TFLOPS * sp_cus / 256, 1),
                                        "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4),
                                        "probe_share_peak": round(p_share, 1)},
-                             "standalone_256": {"achieved": round(agg_pre_tflops, 1),
-                                                "frac": round(agg_pre_tflops / PEAK_BF16_TFLOPS, 4)}},
+                             "standalone_256": {"achieved": rnd(agg_pre_tflops, 1),
+                                                "frac": rnd(agg_pre_tflops and agg_pre_tflops / PEAK_BF16_TFLOPS, 4)}},
         "calibration": calib,
         "cpu_baseline": cpu,
     }

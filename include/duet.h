@@ -137,14 +137,25 @@ int duet_batch_work(const duet_shape* shape, const duet_batch* batch, int32_t ki
 
 /* Replace the achievable-throughput tables (Section 4.2: profiled once per partition size).
  * cus[i] must be the 32 values 8, 16, ..., 256 in order; flops_per_s and bytes_per_s > 0.
- * Marks the model calibrated. */
+ * Marks the model calibrated and clears any sharing tables. */
 int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
                           const double* bytes_per_s);
 int duet_model_get_tables(const duet_model* m, int32_t n, int32_t* cus, double* flops_per_s,
                           double* bytes_per_s);
+/* Sharing tables: Pi(S) and B(S) of each share measured while the other half runs on the other
+ * CUs.  When set, the halves of a SPLIT batch holding both kinds use them instead of the
+ * standalone tables (an extension of Section 4.2: the two partitions of a spatially shared GPU
+ * slow each other down through HBM, L2 and power).  Same layout and checks as
+ * duet_model_set_tables.  get returns the standalone tables and *is_set = 0 when none are set. */
+int duet_model_set_sharing_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
+                                  const double* bytes_per_s);
+int duet_model_get_sharing_tables(const duet_model* m, int32_t n, int32_t* cus, double* flops_per_s,
+                                  double* bytes_per_s, int32_t* is_set);
+
 /* Spatial-sharing efficiencies in (0, 1]: when a SPLIT batch holds both kinds, the two halves
  * run at the same time and slow each other down (shared HBM, L2 and power); the prefill half's
- * Pi is then multiplied by prefill_eff and the decode half's B by decode_eff.  Aggregated
+ * Pi (from the sharing tables if set) is then multiplied by prefill_eff and the decode half's B
+ * by decode_eff.  Aggregated
  * predictions and single-kind batches use the tables as they are.  Calibrate decode_eff so that
  * decode latency is never under-predicted (appendix: under-prediction is the harmful
  * direction). */

@@ -106,6 +106,22 @@ class Model:
         N.check(N.lib().duet_model_get_tables(self.handle, n, cus, fl, by), "duet_model_get_tables")
         return list(cus), list(fl), list(by)
 
+    def set_sharing_tables(self, flops_per_s, bytes_per_s):
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus = (ctypes.c_int32 * n)(*range(N.CU_STEP, N.TOTAL_CUS + 1, N.CU_STEP))
+        fl = (ctypes.c_double * n)(*[float(x) for x in flops_per_s])
+        by = (ctypes.c_double * n)(*[float(x) for x in bytes_per_s])
+        N.check(N.lib().duet_model_set_sharing_tables(self.handle, n, cus, fl, by), "duet_model_set_sharing_tables")
+
+    def sharing_tables(self):
+        """(cus, flops, bytes, is_set): the standalone tables when no sharing tables are set."""
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus, fl, by = (ctypes.c_int32 * n)(), (ctypes.c_double * n)(), (ctypes.c_double * n)()
+        flag = ctypes.c_int32()
+        N.check(N.lib().duet_model_get_sharing_tables(self.handle, n, cus, fl, by, ctypes.byref(flag)),
+                "duet_model_get_sharing_tables")
+        return list(cus), list(fl), list(by), bool(flag.value)
+
     def set_efficiency(self, prefill_eff: float, decode_eff: float):
         N.check(N.lib().duet_model_set_efficiency(self.handle, prefill_eff, decode_eff), "duet_model_set_efficiency")
 

@@ -48,6 +48,9 @@ _SIGS = {
     "duet_model_create": (c_int32, [P(c_void_p)]),
     "duet_model_destroy": (c_int32, [c_void_p]),
     "duet_batch_work": (c_int32, [P(Shape), P(Batch), c_int32, P(c_double), P(c_double)]),
+    "duet_model_set_sharing_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
+    "duet_model_get_sharing_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double),
+                                                P(c_int32)]),
     "duet_model_set_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_get_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_set_efficiency": (c_int32, [c_void_p, c_double, c_double]),

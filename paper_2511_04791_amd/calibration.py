@@ -12,15 +12,13 @@ tables; appendix: decode latency must not be under-predicted).
    reproduces both kernels' measured times on every share, including the effects of how
    workgroups are dealt to the shader engines at shares that are not multiples of 32 CUs.
 
-3. Spatial-sharing efficiencies: the mixed batch (the prefill chunk and the decodes together)
-   runs split near the balance point of its two halves, several layers per call, and each
-   half's per-launch time is compared with the same half alone on the same share.  The prefill
-   efficiency is the median ratio, the decode efficiency the smallest (largest slowdown).  The
-   model applies them only to the halves of a split batch that holds both kinds.
+3. Sharing tables: the mixed batch (the prefill chunk and the decodes together) runs on every
+   split S_p + S_d = 256, several layers per call, and each half's per-launch time gives the
+   rate of its share while the other half runs (Pi_shared(S_p), B_shared(S_d)).  The two halves
+   slow each other down through HBM, L2 and power, and how much depends on the split, so the
+   model uses these tables for the halves of a split batch that holds both kinds.
 
-Each share's rates take the median of the repetitions; the decode half's margin against
-under-prediction comes from the sharing efficiency, which takes the largest slowdown seen.
-All kernel launches and the model arithmetic happen in libduet.so; this module only drives
+Each share's rates take the median of the repetitions.  All kernel launches and the model arithmetic happen in libduet.so; this module only drives
 them and divides.
 """
 from __future__ import annotations
@@ -82,17 +80,17 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, prefill_
     model.set_tables(flops, bytes_)
     model.set_efficiency(1.0, 1.0)
 
-    # 3. both halves at once, near the balance point of the two halves
+    # 3. both halves at once, on every split
     q, kc, vc = wl.make_tensors(mixed, seed=seed, device="cuda")
     pt = torch.as_tensor(mixed.page_table, device="cuda")
     out = torch.empty_like(q)
-    idx = {s: i for i, s in enumerate(SHARES)}
-    balance = min(SHARES[:-1], key=lambda s: max(t_pre[idx[s]], t_dec[idx[N.TOTAL_CUS - s]]))
-    shares = sorted({min(max(balance + d, 2 * N.CU_STEP), N.TOTAL_CUS - 2 * N.CU_STEP)
-                     for d in (-16, -8, 0, 8, 16)})
-    r_pre, r_dec = [], []
-    for s in shares:
-        split = CuSplit.split(s, N.TOTAL_CUS - s)
+    f_mix, _ = batch_work(mixed.seq_meta, sh, wl.KIND_PREFILL)
+    _, b_mix = batch_work(mixed.seq_meta, sh, wl.KIND_DECODE)
+    sh_flops, sh_bytes = list(flops), list(bytes_)   # share 256 never runs split: keep standalone
+    t_pre_sh, t_dec_sh = {}, {}
+    for sp in SHARES[:-1]:
+        sd = N.TOTAL_CUS - sp
+        split = CuSplit.split(sp, sd)
         ctx.set_profiling(2)
         rows = []
         for i in range(1 + reps):
@@ -101,16 +99,16 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, prefill_
             if i >= 1:
                 rows.append(ctx.last_kernel_times())
         ctx.set_profiling(0)
-        conc_p = statistics.median(r["prefill_us"] for r in rows)
-        conc_d = max(r["decode_partial_us"] + r["decode_reduce_us"] for r in rows)
-        r_pre.append(min(1.0, t_pre[idx[s]] / conc_p))
-        r_dec.append(min(1.0, t_dec[idx[N.TOTAL_CUS - s]] / conc_d))
+        t_pre_sh[sp] = statistics.median(r["prefill_us"] for r in rows)
+        t_dec_sh[sd] = statistics.median(r["decode_partial_us"] + r["decode_reduce_us"] for r in rows)
+        sh_flops[sp // N.CU_STEP - 1] = f_mix / (t_pre_sh[sp] * 1e-6)
+        sh_bytes[sd // N.CU_STEP - 1] = b_mix / (t_dec_sh[sd] * 1e-6)
     del q, kc, vc, out
-    pe, de = statistics.median(r_pre), min(r_dec)
-    model.set_efficiency(pe, de)
-    return {"prefill_eff": round(pe, 4), "decode_eff": round(de, 4), "sharing_splits": shares,
-            "prefill_sharing_ratio": [round(x, 4) for x in r_pre],
-            "decode_sharing_ratio": [round(x, 4) for x in r_dec], "shares": list(SHARES),
+    model.set_sharing_tables(sh_flops, sh_bytes)
+    return {"shared_layers": shared_layers,
+            "shared_prefill_us": [round(t_pre_sh.get(s, 0.0), 1) for s in SHARES],
+            "shared_decode_us": [round(t_dec_sh.get(s, 0.0), 1) for s in SHARES],
+            "shares": list(SHARES),
             "prefill_batch": f"1 prefill chunk of {prefill_len} tokens at prefix 0",
             "decode_batch": f"{dec.num_reqs} decodes, contexts U[512,4096]",
             "prefill_us": [round(t, 1) for t in t_pre], "decode_us": [round(t, 1) for t in t_dec],

@@ -24,6 +24,11 @@ int check_batch(const duet_shape* s, const duet_batch* b, bool need_q_start);
 struct duet_model {
   double flops[duet::kNumCuSteps];  // Pi(S), FLOP/s, S = 8 (i + 1)
   double bytes[duet::kNumCuSteps];  // B(S), bytes/s
+  // Rates of each share while the other half runs on the other CUs (spatial sharing); used
+  // for the halves of a split batch holding both kinds when has_shared is set.
+  double flops_shared[duet::kNumCuSteps];
+  double bytes_shared[duet::kNumCuSteps];
+  bool has_shared = false;
   double prefill_eff = 1.0;
   double decode_eff = 1.0;
   bool calibrated = false;

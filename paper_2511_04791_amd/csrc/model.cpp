@@ -50,8 +50,9 @@ inline int cu_index(int cus) { return cus / DUET_CU_STEP - 1; }
 double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b, int kind, int cus,
                   bool shared = false) {
   const int i = cu_index(cus);
-  const double pi = m->flops[i] * (shared ? m->prefill_eff : 1.0);
-  const double bw = m->bytes[i] * (shared ? m->decode_eff : 1.0);
+  const bool tab = shared && m->has_shared;
+  const double pi = (tab ? m->flops_shared[i] : m->flops[i]) * (shared ? m->prefill_eff : 1.0);
+  const double bw = (tab ? m->bytes_shared[i] : m->bytes[i]) * (shared ? m->decode_eff : 1.0);
   double t = 0.0;
   for (int r = 0; r < b->num_reqs; ++r) {
     const duet_seq_meta& rq = b->reqs[r];
@@ -143,6 +144,7 @@ void model_init_nominal(duet_model* m) {
     m->flops[i] = kNominalBf16Flops * frac;
     m->bytes[i] = kNominalHbmBytes * frac;
   }
+  m->has_shared = false;
   m->prefill_eff = 1.0;
   m->decode_eff = 1.0;
   m->calibrated = false;
@@ -189,9 +191,9 @@ int duet_batch_work(const duet_shape* shape, const duet_batch* batch, int32_t ki
   return DUET_OK;
 }
 
-int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
-                          const double* bytes_per_s) {
-  if (!m || !cus || !flops_per_s || !bytes_per_s) return fail(DUET_EINVAL, "NULL argument");
+namespace {
+int check_tables(int32_t n, const int32_t* cus, const double* flops_per_s, const double* bytes_per_s) {
+  if (!cus || !flops_per_s || !bytes_per_s) return fail(DUET_EINVAL, "NULL argument");
   if (n != kNumCuSteps) return fail(DUET_EINVAL, "expected %d table entries, got %d", kNumCuSteps, n);
   for (int i = 0; i < n; ++i) {
     if (cus[i] != DUET_CU_STEP * (i + 1)) return fail(DUET_EINVAL, "cus[%d] = %d, expected %d", i, cus[i],
@@ -200,11 +202,47 @@ int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const do
         !std::isfinite(bytes_per_s[i]))
       return fail(DUET_EINVAL, "table entry %d not positive and finite", i);
   }
+  return DUET_OK;
+}
+}  // namespace
+
+int duet_model_set_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
+                          const double* bytes_per_s) {
+  if (!m) return fail(DUET_EINVAL, "model is NULL");
+  int rc = check_tables(n, cus, flops_per_s, bytes_per_s);
+  if (rc) return rc;
   for (int i = 0; i < n; ++i) {
     m->flops[i] = flops_per_s[i];
     m->bytes[i] = bytes_per_s[i];
   }
+  m->has_shared = false;
   m->calibrated = true;
+  return DUET_OK;
+}
+
+int duet_model_set_sharing_tables(duet_model* m, int32_t n, const int32_t* cus, const double* flops_per_s,
+                                  const double* bytes_per_s) {
+  if (!m) return fail(DUET_EINVAL, "model is NULL");
+  int rc = check_tables(n, cus, flops_per_s, bytes_per_s);
+  if (rc) return rc;
+  for (int i = 0; i < n; ++i) {
+    m->flops_shared[i] = flops_per_s[i];
+    m->bytes_shared[i] = bytes_per_s[i];
+  }
+  m->has_shared = true;
+  return DUET_OK;
+}
+
+int duet_model_get_sharing_tables(const duet_model* m, int32_t n, int32_t* cus, double* flops_per_s,
+                                  double* bytes_per_s, int32_t* is_set) {
+  if (!m || !cus || !flops_per_s || !bytes_per_s || !is_set) return fail(DUET_EINVAL, "NULL argument");
+  if (n != kNumCuSteps) return fail(DUET_EINVAL, "expected %d table entries", kNumCuSteps);
+  for (int i = 0; i < n; ++i) {
+    cus[i] = DUET_CU_STEP * (i + 1);
+    flops_per_s[i] = m->has_shared ? m->flops_shared[i] : m->flops[i];
+    bytes_per_s[i] = m->has_shared ? m->bytes_shared[i] : m->bytes[i];
+  }
+  *is_set = m->has_shared ? 1 : 0;
   return DUET_OK;
 }
 
@@ -232,17 +270,19 @@ int duet_model_save(const duet_model* m, const char* path) {
   if (!m || !path) return fail(DUET_EINVAL, "NULL argument");
   FILE* f = std::fopen(path, "w");
   if (!f) return fail(DUET_EIO, "cannot open %s for writing", path);
-  std::fprintf(f, "{\"version\": 1, \"calibrated\": %d, \"prefill_eff\": %.17g, \"decode_eff\": %.17g,\n",
+  std::fprintf(f, "{\"version\": 2, \"calibrated\": %d, \"prefill_eff\": %.17g, \"decode_eff\": %.17g,\n",
                m->calibrated ? 1 : 0, m->prefill_eff, m->decode_eff);
-  const char* names[3] = {"cus", "flops_per_s", "bytes_per_s"};
-  for (int k = 0; k < 3; ++k) {
+  const char* names[5] = {"cus", "flops_per_s", "bytes_per_s", "shared_flops_per_s", "shared_bytes_per_s"};
+  const double* tabs[5] = {nullptr, m->flops, m->bytes, m->flops_shared, m->bytes_shared};
+  const int n_arrays = m->has_shared ? 5 : 3;
+  for (int k = 0; k < n_arrays; ++k) {
     std::fprintf(f, " \"%s\": [", names[k]);
     for (int i = 0; i < kNumCuSteps; ++i) {
       if (k == 0) std::fprintf(f, "%d", DUET_CU_STEP * (i + 1));
-      else std::fprintf(f, "%.17g", k == 1 ? m->flops[i] : m->bytes[i]);
+      else std::fprintf(f, "%.17g", tabs[k][i]);
       std::fprintf(f, i + 1 < kNumCuSteps ? ", " : "]");
     }
-    std::fprintf(f, k < 2 ? ",\n" : "}\n");
+    std::fprintf(f, k + 1 < n_arrays ? ",\n" : "}\n");
   }
   const bool ok = std::fclose(f) == 0;
   return ok ? DUET_OK : fail(DUET_EIO, "write to %s failed", path);
@@ -315,6 +355,12 @@ int duet_model_load(duet_model* m, const char* path) {
   duet_model tmp = *m;
   int rc = duet_model_set_tables(&tmp, kNumCuSteps, ci.data(), fl.data(), by.data());
   if (rc) return rc;
+  std::vector<double> sfl, sby;
+  if (read_array(s, "shared_flops_per_s", &sfl) && read_array(s, "shared_bytes_per_s", &sby)) {
+    if (sfl.size() != cus.size() || sby.size() != cus.size())
+      return fail(DUET_EIO, "%s: sharing tables must hold %d entries", path, kNumCuSteps);
+    if ((rc = duet_model_set_sharing_tables(&tmp, kNumCuSteps, ci.data(), sfl.data(), sby.data()))) return rc;
+  }
   rc = duet_model_set_efficiency(&tmp, pe, de);
   if (rc) return rc;
   tmp.calibrated = cal != 0.0;

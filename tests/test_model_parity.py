@@ -149,3 +149,34 @@ def test_batch_work_matches_oracle_accounting(seed):
         f, b = duet.batch_work(rows, sh, kind)
         assert f == pytest.approx(f_want, rel=1e-12, abs=0.0)
         assert b == pytest.approx(b_want, rel=1e-12, abs=0.0)
+
+
+def test_sharing_tables_replace_standalone_rates_for_mixed_splits(tmp_path):
+    rng = np.random.default_rng(41)
+    pis, bws = _tables(rng)
+    spis, sbws = pis * 0.7, bws * 0.5
+    shape = wl.LLAMA3_8B
+    dec, pre = [(1, 1, 3000)] * 16, [(0, 4096, 0)]
+    sp = duet.CuSplit.split(96, 160)
+    m = duet.Model()
+    m.set_tables(pis, bws)
+    agg = duet.predict_iter_latency(dec + pre, duet.CuSplit.agg(), shape, m)
+    alone = duet.predict_iter_latency(dec, sp, shape, m)
+    plain = duet.predict_iter_latency(dec + pre, sp, shape, m)
+    assert m.sharing_tables()[3] is False
+    m.set_sharing_tables(spis, sbws)
+    # the model with the sharing tables equals the oracle's model on those tables
+    shared = duet.predict_iter_latency(dec + pre, sp, shape, m)
+    want = 1e6 * orf.predict(dec + pre, orf.SPLIT, 96, 160, 1, orf.Tables(dict(zip(CUS, spis)), dict(zip(CUS, sbws))),
+                             **_kw(shape))
+    assert shared == pytest.approx(want, rel=1e-12) and shared > plain
+    assert duet.predict_iter_latency(dec + pre, duet.CuSplit.agg(), shape, m) == pytest.approx(agg, rel=1e-12)
+    assert duet.predict_iter_latency(dec, sp, shape, m) == pytest.approx(alone, rel=1e-12)
+    path = os.path.join(tmp_path, "m.json")
+    m.save(path)
+    m2 = duet.Model()
+    m2.load(path)
+    cus, fl, by, is_set = m2.sharing_tables()
+    assert is_set and np.array_equal(fl, spis) and np.array_equal(by, sbws)
+    m2.set_tables(pis, bws)          # new standalone tables drop stale sharing tables
+    assert m2.sharing_tables()[3] is False
