@@ -34,12 +34,20 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = 8;
+#ifndef DUET_PREFILL_WAVES
+#define DUET_PREFILL_WAVES 8
+#endif
+constexpr int kWaves = DUET_PREFILL_WAVES;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kStages = 3;
+constexpr int kStages = 4;  // LDS ring: loads run three tiles ahead of the tile in use
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// Direct global-to-LDS load of 16 bytes per lane: lane i of the wave writes lds_block + 16 i.
+// lds_block must be the same for the whole wave.
+__device__ __forceinline__ void load_lds16(const char* src, __bf16* lds_block) {
+  __builtin_amdgcn_global_load_lds(src, lds_block, 16, 0, 0);
+}
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 __device__ __forceinline__ bool page_ok(int id, long long num_phys) { return id >= 0 && (long long)id < num_phys; }
 
@@ -62,13 +70,16 @@ __device__ __forceinline__ uint32_t keep_pairs(uint32_t word, int n_valid_in_pai
   return n_valid_in_pair >= 2 ? word : (n_valid_in_pair == 1 ? (word & 0xffffu) : 0u);
 }
 
-constexpr int kIdCap = kMaxPrefillKeys / 16;  // page ids staged in LDS for a whole unit
+constexpr int kIdCap = kMaxPrefillKeys / 16;  // most page ids a unit can stage in LDS
 
+// Dynamic LDS: the K/V ring, then the page ids of the unit (sized per launch for the longest
+// prefill request, so short requests leave room for a second workgroup per CU).
 template <int D>
 struct PrefillSmem {
   static constexpr int kStageElems = 2 * kPrefillKeys * D;  // K tile + V^T tile, bf16
   static constexpr size_t kTileBytes = (size_t)kStages * kStageElems * 2;
-  static constexpr size_t kBytes = kTileBytes + kIdCap * sizeof(int);
+  static constexpr size_t kMaxBytes = kTileBytes + kIdCap * sizeof(int);
+  static size_t bytes(int id_cap) { return kTileBytes + (((size_t)id_cap + 3) & ~(size_t)3) * sizeof(int); }
 };
 
 template <int D, int NH>
@@ -76,7 +87,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   constexpr int BN = kPrefillKeys;       // keys per stage
   constexpr int KCH = D / 8;             // 16-byte chunks per K row
   constexpr int VCH = BN / 8;            // 16-byte chunks per V^T row
-  constexpr int CH = (BN * D / 8) / kThreads;  // chunks per thread per tensor per stage
   constexpr int NK = D / 16;             // MFMA k-steps over the head dim
   constexpr int NO = D / 32;             // 32-dim output tiles
   constexpr int WPH = kWaves / NH;       // waves per head
@@ -127,48 +137,93 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   for (int i = tid; i < n_used_pages; i += kThreads) ids[i] = prow[i];
   __syncthreads();
 
-  uint4 kst[CH], vst[CH];
-  auto load_tile = [&](int kt) {
+  // Tiles arrive by direct global-to-LDS loads (16 bytes per lane; lane i of a wave writes bytes
+  // 16 i .. 16 i + 15 of a 1 KiB LDS block).  Each tile is KB blocks of K and KB blocks of V^T;
+  // wave w loads blocks w, w + kWaves, ...  A lane's source is fixed by the block and the lane
+  // (the inverse of the LDS chunk swizzle) except for the page id, so only the id changes per
+  // tile.  Loads run three tiles ahead through a four-stage ring.
+  constexpr int KB = BN * D * 2 / 1024;   // 1 KiB blocks per tile per tensor
+  constexpr int BPW = KB / kWaves;        // blocks per wave per tensor
+  static_assert(BPW >= 1 && KB % kWaves == 0, "tile blocks must divide evenly among waves");
+  int k_pi[BPW], k_off[BPW], v_pi[BPW], v_off[BPW];
 #pragma unroll
-    for (int x = 0; x < CH; ++x) {
-      const int chunk = tid + kThreads * x;
-      const int pi = chunk / (2 * D);
-      const int y = chunk - pi * (2 * D);
-      const int lp = 4 * kt + pi;
-      const bool in_range = lp < n_pages;
-      const int id = in_range ? ids[lp] : 0;
-      const bool ok = in_range && page_ok(id, a.num_phys_pages);
+  for (int i = 0; i < BPW; ++i) {
+    const int blk = wave + kWaves * i;
+    const int krow = (64 / KCH) * blk + lane / KCH;           // key row of the K tile
+    const int kc = (lane % KCH) ^ (kswz(krow) & (KCH - 1));   // logical 16-byte chunk of the row
+    k_pi[i] = krow >> 4;
+    k_off[i] = (krow & 15) * (D * 2) + kc * 16;
+    const int vrow = 8 * blk + lane / 8;                      // dim row of the V^T tile
+    const int vc = (lane % 8) ^ (vswz(vrow) & (VCH - 1));     // logical chunk: 8 keys
+    v_pi[i] = vc >> 1;
+    v_off[i] = vrow * 32 + (vc & 1) * 16;
+  }
+  auto issue_tile = [&](int kt) {
+    __bf16* kdst = lds + (kt % kStages) * PrefillSmem<D>::kStageElems;
+    __bf16* vdst = kdst + BN * D;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int blk = wave + kWaves * i;
+      int lp = 4 * kt + k_pi[i];
+      bool in_range = lp < n_pages;
+      int id = in_range ? ids[min(lp, n_pages - 1)] : 0;  // the LDS read stays inside the table
+      bool ok = in_range && page_ok(id, a.num_phys_pages);
       bad |= in_range & !ok;
-      // Loads are unconditional (page 0 stands in for a missing page); keys of a missing page
-      // lie past the end and are masked, so only their values need zeroing.
-      const size_t off = ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + (size_t)y * 16;
-      kst[x] = *reinterpret_cast<const uint4*>(kbase + off);
-      uint4 v = *reinterpret_cast<const uint4*>(vbase + off);
-      // Values of keys >= L are NaN-poisoned slots: they must not reach the MFMA.
-      const int nv = ok ? L - (BN * kt + 16 * pi + 8 * (y & 1)) : 0;
-      if (nv < 8) {
+      // A missing page reads page 0: its keys lie past the end (masked) or the request is
+      // already flagged; values past the end are zeroed once the last tile has landed.
+      load_lds16(kbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + k_off[i], kdst + blk * 512);
+      lp = 4 * kt + v_pi[i];
+      in_range = lp < n_pages;
+      id = in_range ? ids[min(lp, n_pages - 1)] : 0;
+      ok = in_range && page_ok(id, a.num_phys_pages);
+      bad |= in_range & !ok;
+      load_lds16(vbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + v_off[i], vdst + blk * 512);
+    }
+  };
+  // Waits until this wave's loads of all but the `later` most recent tiles have landed.
+  auto wait_tiles = [&](int later) {
+    constexpr int kLoadsPerTile = 2 * BPW;
+    // s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima
+    if (later >= 2) __builtin_amdgcn_s_waitcnt(((2 * kLoadsPerTile) & 15) | (((2 * kLoadsPerTile) >> 4) << 14) | 0x0F70);
+    else if (later == 1) __builtin_amdgcn_s_waitcnt((kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14) | 0x0F70);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+  };
+  // Values of keys >= L (NaN-poisoned tail slots, stand-in pages) must not reach the MFMA: the
+  // tile holding key L - 1 has them zeroed in LDS before first use.
+  const int kt_tail = (L - 1) / BN;
+  const int tail_keys = L - BN * kt_tail;  // valid keys of that tile, 1 .. BN
+  auto zero_tail = [&](int kt) {
+    if (kt != kt_tail || tail_keys == BN) return false;
+    __bf16* vs = lds + (kt % kStages) * PrefillSmem<D>::kStageElems + BN * D;
+    for (int x = tid; x < D * VCH; x += kThreads) {
+      const int vrow = x / VCH;
+      const int sc = x % VCH;
+      const int c = sc ^ (vswz(vrow) & (VCH - 1));
+      const int first = 8 * c;
+      if (first + 8 <= tail_keys) continue;
+      uint4* p = reinterpret_cast<uint4*>(vs + vrow * BN + sc * 8);
+      if (first >= tail_keys) {
+        *p = make_uint4(0, 0, 0, 0);
+      } else {
+        uint4 v = *p;
+        const int nv = tail_keys - first;
         v.x = keep_pairs(v.x, nv);
         v.y = keep_pairs(v.y, nv - 2);
         v.z = keep_pairs(v.z, nv - 4);
         v.w = keep_pairs(v.w, nv - 6);
+        *p = v;
       }
-      vst[x] = v;
     }
+    return true;
   };
-  auto store_tile = [&](int buf) {
-    __bf16* ks = lds + buf * PrefillSmem<D>::kStageElems;
-    __bf16* vs = ks + BN * D;
-#pragma unroll
-    for (int x = 0; x < CH; ++x) {
-      const int chunk = tid + kThreads * x;
-      const int pi = chunk / (2 * D);
-      const int y = chunk - pi * (2 * D);
-      const int krow = 16 * pi + y / KCH;
-      const int kch = (y % KCH) ^ (kswz(krow) & (KCH - 1));
-      *reinterpret_cast<uint4*>(ks + krow * D + kch * 8) = kst[x];
-      const int vrow = y >> 1;
-      const int vch = (2 * pi + (y & 1)) ^ (vswz(vrow) & (VCH - 1));
-      *reinterpret_cast<uint4*>(vs + vrow * BN + vch * 8) = vst[x];
+  // Makes tile kt visible to every wave: this wave's loads of it have landed (the `later`
+  // newer tiles may still be in flight), then a barrier; the tail tile gets its fix-up.
+  auto publish = [&](int kt, int later) {
+    wait_tiles(later);
+    __builtin_amdgcn_s_barrier();
+    if (zero_tail(kt)) {
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the fix-up's LDS writes are done
+      __builtin_amdgcn_s_barrier();
     }
   };
 
@@ -179,56 +234,43 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     for (int v = 0; v < 16; ++v) oacc[n][v] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
 
-  load_tile(0);
-  store_tile(0);
-  if (n_tiles > 1) {
-    load_tile(1);
-    store_tile(1);
-  }
-  __syncthreads();
-  if (n_tiles > 2) load_tile(2);
+  for (int t = 0; t < 3 && t < n_tiles; ++t) issue_tile(t);
+  publish(0, min(n_tiles - 1, 2));
+
+  // S^T of key tile kt for this wave's 32 rows: K fragments from LDS, Q^T from registers.
+  auto scores = [&](int kt, f32x16 (&sacc)[2]) {
+    const __bf16* ks = lds + (kt % kStages) * PrefillSmem<D>::kStageElems;
+    // All K fragments of the step are read before the first MFMA, so LDS latency is paid once.
+    bf16x8 kf[2][NK];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int row = 32 * nb + swap_bits23(lane & 31);
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        const int ch = (2 * kk + hh) ^ (kswz(row) & (KCH - 1));
+        kf[nb][kk] = *reinterpret_cast<const bf16x8*>(ks + row * D + ch * 8);
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[nb][v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[nb][kk], qf[kk], sacc[nb], 0, 0, 0);
+  };
 
   for (int kt = 0; kt < n_tiles; ++kt) {
     if (kt < w_tiles) {
-      const __bf16* ks = lds + (kt % kStages) * PrefillSmem<D>::kStageElems;
-      const __bf16* vs = ks + BN * D;
-      // All K fragments of the step are read before the first MFMA, so LDS latency is paid once.
-      bf16x8 kf[2][NK];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const int row = 32 * nb + swap_bits23(lane & 31);
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-          const int ch = (2 * kk + hh) ^ (kswz(row) & (KCH - 1));
-          kf[nb][kk] = *reinterpret_cast<const bf16x8*>(ks + row * D + ch * 8);
-        }
-      }
       f32x16 sacc[2];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) sacc[nb][v] = 0.f;
-#ifdef DUET_PREFILL_SETPRIO
-      __builtin_amdgcn_s_setprio(1);
-#endif
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[nb][kk], qf[kk], sacc[nb], 0, 0, 0);
-#ifdef DUET_PREFILL_SETPRIO
-      __builtin_amdgcn_s_setprio(0);
-#endif
-      // V fragments are read now; their LDS latency hides behind the softmax below.  With
-      // DUET_PREFILL_VHALF only the first half is read ahead (fewer live registers).
-#ifdef DUET_PREFILL_VHALF
-      constexpr int NV = NO / 2;
-#else
-      constexpr int NV = NO;
-#endif
+      scores(kt, sacc);
+      const __bf16* vs = lds + (kt % kStages) * PrefillSmem<D>::kStageElems + BN * D;
+      // V fragments are read now; their LDS latency hides behind the softmax below.
       bf16x8 vf[NO][4];
 #pragma unroll
-      for (int n = 0; n < NV; ++n) {
+      for (int n = 0; n < NO; ++n) {
         const int vrow = 32 * n + (lane & 31);
 #pragma unroll
         for (int k2 = 0; k2 < 4; ++k2) {
@@ -279,29 +321,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
           l_run = __builtin_amdgcn_fdot2_f32_bf16(two, ones, l_run, false);
         }
 #pragma unroll
-      for (int n = NV; n < NO; ++n) {
-        const int vrow = 32 * n + (lane & 31);
-#pragma unroll
-        for (int k2 = 0; k2 < 4; ++k2) {
-          const int ch = (2 * k2 + hh) ^ (vswz(vrow) & (VCH - 1));
-          vf[n][k2] = *reinterpret_cast<const bf16x8*>(vs + vrow * BN + ch * 8);
-        }
-      }
-#ifdef DUET_PREFILL_SETPRIO
-      __builtin_amdgcn_s_setprio(1);
-#endif
-#pragma unroll
       for (int n = 0; n < NO; ++n)
 #pragma unroll
         for (int k2 = 0; k2 < 4; ++k2)
           oacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n][k2], pb[k2], oacc[n], 0, 0, 0);
-#ifdef DUET_PREFILL_SETPRIO
-      __builtin_amdgcn_s_setprio(0);
-#endif
     }
-    if (kt + 2 < n_tiles) store_tile((kt + 2) % kStages);
-    if (kt + 3 < n_tiles) load_tile(kt + 3);
-    __syncthreads();
+    if (kt + 1 < n_tiles) {
+      // Stage (kt + 3) % 4 was last read in step kt - 1, which every wave has left.
+      if (kt + 3 < n_tiles) issue_tile(kt + 3);
+      publish(kt + 1, min(n_tiles - 1, kt + 3) - (kt + 1));
+    }
   }
 
   if (bad) atomicOr(w.err, 1);
@@ -381,11 +410,12 @@ hipError_t launch_bf16(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   static bool attr_set = false;  // the attribute is per function and process
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&prefill_bf16<D, NH>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)PrefillSmem<D>::kBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)PrefillSmem<D>::kMaxBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL((prefill_bf16<D, NH>), dim3(w.n_pitems), dim3(kThreads), PrefillSmem<D>::kBytes, s, a, w);
+  hipLaunchKernelGGL((prefill_bf16<D, NH>), dim3(w.n_pitems), dim3(kThreads), PrefillSmem<D>::bytes(w.prefill_id_cap),
+                     s, a, w);
   return hipGetLastError();
 }
 
@@ -394,22 +424,26 @@ hipError_t launch_bf16_nh(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   switch (prefill_heads_per_unit(a.group)) {
     case 1: return launch_bf16<D, 1>(a, w, s);
     case 2: return launch_bf16<D, 2>(a, w, s);
+#if DUET_PREFILL_WAVES >= 8
     case 4: return launch_bf16<D, 4>(a, w, s);
     default: return launch_bf16<D, 8>(a, w, s);
+#else
+    default: return launch_bf16<D, 4>(a, w, s);
+#endif
   }
 }
 
 }  // namespace
 
 int prefill_heads_per_unit(int group) {
-  // largest power of two <= min(group, 8) that divides the group
+  // largest power of two <= min(group, waves per workgroup) that divides the group
   int nh = 1;
-  while (nh * 2 <= 8 && group % (nh * 2) == 0) nh *= 2;
+  while (nh * 2 <= kWaves && group % (nh * 2) == 0) nh *= 2;
   return nh;
 }
 
 int prefill_rows_per_unit(int group, int dtype) {
-  return dtype == 0 ? 256 / prefill_heads_per_unit(group) : kPrefillRows;
+  return dtype == 0 ? 32 * kWaves / prefill_heads_per_unit(group) : kPrefillRows;
 }
 
 hipError_t launch_prefill(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {

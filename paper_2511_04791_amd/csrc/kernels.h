@@ -33,6 +33,7 @@ struct WorkArgs {
   int32_t n_pitems, n_dreq, max_split, n_ditems;
   int32_t pages_per_split;
   int32_t decode_cus;   // CUs the decode stream may use (sizes the persistent grid)
+  int32_t prefill_id_cap;  // most pages of any prefill request (sizes the LDS page-id table)
 };
 
 #ifndef DUET_DECODE_PAGES_PER_SPLIT

@@ -57,7 +57,7 @@ struct StagingSlot {
 struct Plan {
   std::vector<int4> meta, pitems, dreq;
   std::vector<int32_t> ditems;
-  int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0;
+  int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0, prefill_id_cap = 0;
   size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, off_pacc = 0, off_pml = 0, upload_bytes = 0,
          total = 0;
 };
@@ -72,6 +72,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, b
   const int pps = pages_per_split_for(s);
   p->group = g;
   p->pages_per_split = pps;
+  p->prefill_id_cap = 0;
   p->meta.clear();
   p->pitems.clear();
   p->dreq.clear();
@@ -88,6 +89,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, b
     if (fill) p->meta.push_back(make_int4(q.kind, q.q_start, q.q_len, q.cached_len));
     const int64_t L = (int64_t)q.cached_len + q.q_len;
     if (q.kind == DUET_KIND_PREFILL) {
+      p->prefill_id_cap = std::max(p->prefill_id_cap, (int)((L + 15) / 16));
       // bf16: a unit is nh heads of one group x rows queries; fp32: one head x rows queries.
       const int nh = s->dtype == DUET_BF16 ? prefill_heads_per_unit(g) : 1;
       const int rows = prefill_rows_per_unit(g, s->dtype == DUET_BF16 ? 0 : 1);
@@ -361,6 +363,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   w.n_dreq = (int)p.dreq.size();
   w.max_split = p.max_split;
   w.pages_per_split = p.pages_per_split;
+  w.prefill_id_cap = p.prefill_id_cap;
   const bool prof_iter = ctx->profiling >= 1;
   const bool prof = ctx->profiling >= 2;
   const bool has_decode = w.n_dreq > 0, has_prefill = w.n_pitems > 0;
