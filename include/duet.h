@@ -67,6 +67,9 @@ extern "C" {
 
 #define DUET_AGG 0   /* temporal sharing: both halves on the caller's stream, all CUs */
 #define DUET_SPLIT 1 /* spatial sharing: decode on cus_decode CUs, prefill on cus_prefill CUs */
+#define DUET_CONCURRENT 2 /* control for measurements: both halves at once on two streams that may
+                             each use every CU (concurrency without partitioning); accepted by the
+                             attention calls only, not by the latency model */
 
 /* status_flags of duet_choose_cu_split (bit set) */
 #define DUET_STATUS_SLO_INFEASIBLE 1 /* no decode share meets the TBT bound; aggregated returned */
@@ -98,7 +101,7 @@ typedef struct {
 } duet_batch;
 
 typedef struct {
-  int32_t mode;           /* DUET_AGG or DUET_SPLIT */
+  int32_t mode;           /* DUET_AGG, DUET_SPLIT or (attention calls only) DUET_CONCURRENT */
   int32_t cus_prefill;    /* S_p, multiple of 8 (SPLIT) */
   int32_t cus_decode;     /* S_d, multiple of 8 (SPLIT), S_p + S_d <= 256 */
   int32_t k_decode_steps; /* k of Section 4.2: decode steps planned per prefill step (>= 1) */
@@ -175,7 +178,9 @@ int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, cons
  * maximising (k T_decode + T_prefill) / max(k t_d, t_p) subject to t_d <= tbt_slo_us, with S_d in
  * 8, 16, ..., 248 and k in {floor(t_p/t_d), floor(t_p/t_d) + 1} minus 0.  Ties keep the first
  * (smallest S_d, then smaller k).  max_decode_steps > 0 caps k at the number of decode steps the
- * caller can launch ahead (Section 4.3, look-ahead decode); <= 0 leaves k uncapped.  predicted_us,
+ * caller can launch ahead (Section 4.3, look-ahead decode): both candidates are clamped to the
+ * cap, which keeps the best allowed k because rho rises in k up to floor(t_p/t_d) and falls after
+ * it; <= 0 leaves k uncapped.  predicted_us,
  * rho and status_flags may be NULL; rho is 0 for aggregated.  m may be NULL (nominal tables). */
 int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
                          double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,

@@ -96,7 +96,8 @@ def predict(batch, mode, s_p, s_d, k, tables, *, h_q, h_kv, d_h, b, layers, tota
 
 def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP, kmax=None):
     """Algorithm 1.  Returns dict(mode, s_p, s_d, k, rho, t, flags).  kmax caps k at the number of
-    decode steps the engine can launch ahead (Section 4.3); None leaves it uncapped."""
+    decode steps the engine can launch ahead (Section 4.3): the two candidates are clamped to it;
+    None leaves them as the paper states."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
     mixed = [(q, c) for _, q, c in batch]
     t_mixed = f_roofline(mixed, total, tables, **kw)
@@ -113,8 +114,11 @@ def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, st
         s_p = total - s_d
         t_p = f_roofline(pre, s_p, tables, **kw)
         base = math.floor(t_p / t_d) if t_d > 0 else 1
-        for k in (base, base + 1):
-            if k < 1 or (kmax is not None and k > kmax):
+        # rho(k) rises up to k = base and falls from k = base + 1 on, so under a cap on the
+        # decode steps the best allowed candidates are base and base + 1 clamped to the cap
+        cands = (base, base + 1) if kmax is None else tuple(sorted({min(base, kmax), min(base + 1, kmax)}))
+        for k in cands:
+            if k < 1:
                 continue
             t = max(k * t_d, t_p)
             rho = (k * t_decode_tokens + t_prefill_tokens) / t

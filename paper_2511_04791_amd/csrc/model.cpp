@@ -426,10 +426,15 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
     const int sp = DUET_TOTAL_CUS - sd;
     const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, sp, shared);
     const double base = td > 0.0 ? std::floor(tp / td) : 1.0;
+    // rho(k) rises up to k = base and falls from base + 1 on: under a cap on the decode steps
+    // the candidates are clamped to it (the second is skipped when both clamp to the cap).
     for (int j = 0; j < 2; ++j) {
-      const double k = base + j;
+      double k = base + j;
+      if (max_decode_steps > 0 && k > max_decode_steps) {
+        if (j == 1 && base >= max_decode_steps) continue;
+        k = max_decode_steps;
+      }
       if (k < 1.0 || k > 1e9) continue;
-      if (max_decode_steps > 0 && k > max_decode_steps) continue;
       const double t = std::fmax(k * td, tp);
       const double r = (k * t_decode_tokens + t_prefill_tokens) / t;
       if (r > best_rho) {

@@ -52,8 +52,9 @@ def test_predict_matches_oracle(shape):
         assert got == pytest.approx(want * 1e6, rel=1e-12)
 
 
-def test_choose_matches_oracle():
-    rng = np.random.default_rng(31)
+@pytest.mark.parametrize("cap", [0, 1, 3])
+def test_choose_matches_oracle(cap):
+    rng = np.random.default_rng(31 + cap)
     shape = wl.AttnShape(32, 8, 128, "bf16", num_layers=32)
     n_split = 0
     for _ in range(80):
@@ -64,8 +65,8 @@ def test_choose_matches_oracle():
         rows = _batch(rng)
         t_mixed = orf.predict(rows, orf.AGG, 256, 0, 1, tab, **_kw(shape))
         tau = t_mixed * float(rng.uniform(0.05, 1.2))
-        want = orf.choose(rows, tau, tab, **_kw(shape))
-        sp, us, rho, flags = duet.choose_cu_split(rows, tau * 1e6, shape, model)
+        want = orf.choose(rows, tau, tab, kmax=cap or None, **_kw(shape))
+        sp, us, rho, flags = duet.choose_cu_split(rows, tau * 1e6, shape, model, max_decode_steps=cap)
         assert sp.mode == want["mode"]
         assert flags == want["flags"]
         assert us == pytest.approx(want["t"] * 1e6, rel=1e-12)

@@ -197,3 +197,27 @@ def test_predict_split_is_max_of_k_decode_steps_and_prefill():
     t_p = orf.f_roofline([(1024, 0)], 192, tab, **kw)
     for k in (1, 3, 50):
         assert orf.predict(batch, orf.SPLIT, 192, 64, k, tab, **kw) == max(k * t_d, t_p)
+
+
+@pytest.mark.parametrize("kmax", [1, 2, 5])
+def test_capped_algorithm1_equals_exhaustive_search_over_allowed_k(kmax):
+    """With k capped (Section 4.3: only so many decode steps can be launched ahead), the clamped
+    candidates find the best (S_d, k <= cap) that brute force over every allowed k finds."""
+    rng = np.random.default_rng(30 + kmax)
+    kw = dict(h_q=32, h_kv=8, d_h=128, b=2, layers=32)
+    checked = 0
+    for trial in range(60):
+        tab = _monotone_tables(rng)
+        batch = _random_batch(rng)
+        t_mixed = orf.f_roofline([(q, c) for _, q, c in batch], 256, tab, **kw)
+        tau = t_mixed * float(rng.uniform(0.05, 0.95))
+        got = orf.choose(batch, tau, tab, kmax=kmax, **kw)
+        rho, cfg = _exhaustive(batch, tau, tab, kw, kmax=kmax)
+        if cfg is None:
+            assert got["mode"] == orf.AGG and got["flags"] == orf.SLO_INFEASIBLE
+            continue
+        checked += 1
+        assert got["mode"] == orf.SPLIT and got["k"] <= kmax
+        assert got["rho"] == pytest.approx(rho, rel=1e-12)
+        assert (got["s_p"], got["s_d"], got["k"]) == cfg
+    assert checked >= 20
