@@ -131,6 +131,105 @@ def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
             "measured_s": round(t_dec + t_pre, 3)}
 
 
+def trace_main(args):
+    """The serving-trace configuration: 200 consecutive iterations of a Sarathi-style batch
+    former (decode first, chunked prefill up to an 8192-token budget) over Poisson arrivals
+    (4 req/s) with lognormal prompts (mean 4096, sigma 1.0, capped at 32768) and outputs (mean
+    256, sigma 0.7), 32 attention layers per iteration at Llama-3-8B shapes, bf16.  Every
+    iteration runs in always-aggregated mode and in adaptive mode (Algorithm 1 on the calibrated
+    model) at the TBT SLO of 50 ms; a third pass uses, per iteration, a bound 1% under the
+    aggregated prediction, so the spatial branch is taken whenever the model finds a split that
+    helps (an attention-only iteration is far below 50 ms).  Latencies are fork-to-join events;
+    the decode-ready time (fork to the end of the last decode kernel) is when the iteration's
+    decode tokens exist, the attention share of their time between tokens.  KV pages come from
+    one seeded random pool per layer."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from paper_2511_04791_amd.calibration import calibrate_model
+
+    L = args.layers
+    ctx = duet.Context(0)
+    if not args.no_calibrate:
+        calibrate_model(ctx)
+    batches = wl.serving_trace(num_iters=args.trace_iters)
+    sh = dataclasses.replace(wl.LLAMA3_8B, num_layers=L)
+    max_tok = max(sum(q for _, q, _ in b) for b in batches)
+    max_pages = max(sum(-(-(q + c) // 16) for _, q, c in b) for b in batches)
+    max_row = max(-(-(q + c) // 16) for b in batches for _, q, c in b)
+    pool = int(max_pages * 1.25) + 16
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1005)
+    kcs = [(torch.randn(pool, 8, 16, 128, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
+    vcs = [(torch.randn(pool, 8, 128, 16, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
+    qs = [(torch.randn(max_tok, 32, 128, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
+    outs = [torch.empty_like(q) for q in qs]
+    rng = np.random.default_rng(1005)
+    modes = {"agg": [], "adaptive_50ms": [], "adaptive_tight": []}
+    ready = {name: [] for name in modes}   # fork to the end of the last decode kernel (TBT)
+    chosen = {"adaptive_50ms": [], "adaptive_tight": []}
+    tokens = []
+    ctx.set_profiling(2)
+    for bi, rows in enumerate(batches):
+        n_tok = sum(q for _, q, _ in rows)
+        starts = np.cumsum([0] + [q for _, q, _ in rows])[:-1]
+        meta = np.array([(k, s, q, c) for (k, q, c), s in zip(rows, starts)], dtype=np.int32)
+        pages = rng.permutation(pool)
+        table = np.full((len(rows), max_row), -1, dtype=np.int32)
+        off = 0
+        for r, (_, q, c) in enumerate(rows):
+            n = -(-(q + c) // 16)
+            table[r, :n] = pages[off:off + n]
+            off += n
+        pt = torch.as_tensor(table, device="cuda")
+        q_l = [q[:n_tok] for q in qs]
+        o_l = [o[:n_tok] for o in outs]
+        rows3 = [(int(k), int(q), int(c)) for k, q, c in rows]
+        t_agg = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), sh, ctx.model)
+        for name in modes:
+            if name == "agg":
+                sp = duet.CuSplit.agg()
+            else:
+                tau = 50000.0 if name == "adaptive_50ms" else 0.99 * t_agg
+                sp = duet.choose_cu_split(rows3, tau, sh, ctx.model, max_decode_steps=1)[0]
+                chosen[name].append(sp.mode == duet.SPLIT)
+            for rep in range(2):  # the first call on a new CU split creates its streams
+                ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
+                kt = ctx.last_kernel_times()
+            modes[name].append(kt["iteration_us"])
+            ready[name].append(kt["decode_start_us"] + kt["decode_total_us"] if kt["decode_total_us"] > 0
+                               else kt["iteration_us"])
+        tokens.append(n_tok)
+    ctx.set_profiling(0)
+    tot_tok = float(sum(tokens))
+    res = {}
+    for name, lat in modes.items():
+        a = np.array(lat)
+        r = np.array(ready[name])
+        res[name] = {"p50_us": round(float(np.percentile(a, 50)), 1), "p99_us": round(float(np.percentile(a, 99)), 1),
+                     "mean_us": round(float(a.mean()), 1), "tokens_per_s": round(tot_tok / (a.sum() * 1e-6), 1),
+                     "decode_ready_p50_us": round(float(np.percentile(r, 50)), 1),
+                     "decode_ready_p99_us": round(float(np.percentile(r, 99)), 1),
+                     "decode_ready_max_us": round(float(r.max()), 1),
+                     "tbt_slo_attainment": round(float(np.mean(r <= 50000.0)), 4)}
+        if name in chosen:
+            res[name]["split_fraction"] = round(float(np.mean(chosen[name])), 3)
+    n_pre = sum(1 for b in batches if any(k == 0 for k, _, _ in b))
+    line = {"metric": "serving-trace decode TBT p99, attention share (us)", "value": res["adaptive_50ms"]["decode_ready_p99_us"],
+            "unit": "us", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"serving trace: {len(batches)} iterations, Poisson 4 req/s, prompts LogN(mean 4096, "
+                                   f"sigma 1.0) <= 32768, outputs LogN(mean 256, sigma 0.7), budget 8192, {L} layers, "
+                                   "llama3-8b attention shapes", "iterations_with_prefill": n_pre,
+                       "mean_decodes": round(float(np.mean([sum(1 for k, _, _ in b if k == 1) for b in batches])), 1),
+                       "mean_tokens": round(float(np.mean(tokens)), 1)},
+            "modes": res, "agg_decode_ready_p99_us": res["agg"]["decode_ready_p99_us"],
+            "throughput_ratio_50ms_vs_agg": round(res["adaptive_50ms"]["tokens_per_s"] / res["agg"]["tokens_per_s"], 4)}
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +248,9 @@ def main():
                     help="skip the aggregated reference passes (every launch then runs in the timed mode)")
     ap.add_argument("--copy-reference", action="store_true",
                     help="end with a plain 1 GiB device-to-device copy, the reference for HBM counters")
+    ap.add_argument("--trace", action="store_true",
+                    help="run the serving-trace configuration instead (adaptive vs always-aggregated)")
+    ap.add_argument("--trace-iters", type=int, default=200)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path; "
@@ -164,6 +266,9 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.trace:
+        trace_main(args)
+        return
     L = args.layers
     ctx = duet.Context(0)
     calib = {}

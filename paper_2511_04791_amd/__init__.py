@@ -16,11 +16,11 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import _native as N
-from ._native import (AGG, BF16, CU_STEP, F32, KIND_DECODE, KIND_PREFILL, SPLIT, STATUS_SLO_INFEASIBLE,
+from ._native import (AGG, BF16, CONCURRENT, CU_STEP, F32, KIND_DECODE, KIND_PREFILL, SPLIT, STATUS_SLO_INFEASIBLE,
                       STATUS_UNCALIBRATED, TOTAL_CUS, DuetError)
 from .workloads import AttnShape
 
-__all__ = ["AGG", "SPLIT", "CuSplit", "Context", "Model", "DuetError", "attn_mixed_batch", "predict_iter_latency",
+__all__ = ["AGG", "SPLIT", "CONCURRENT", "CuSplit", "Context", "Model", "DuetError", "attn_mixed_batch", "predict_iter_latency",
            "choose_cu_split", "default_context", "AttnShape", "STATUS_SLO_INFEASIBLE", "STATUS_UNCALIBRATED"]
 
 
@@ -39,11 +39,20 @@ class CuSplit:
     def split(cus_prefill: int, cus_decode: int, k: int = 1) -> "CuSplit":
         return CuSplit(SPLIT, cus_prefill, cus_decode, k)
 
+    @staticmethod
+    def concurrent() -> "CuSplit":
+        """Control for measurements: both halves at once on two unpartitioned streams."""
+        return CuSplit(CONCURRENT, TOTAL_CUS, TOTAL_CUS, 1)
+
     def to_c(self) -> N.CuSplit:
         return N.CuSplit(self.mode, self.cus_prefill, self.cus_decode, self.k_decode_steps)
 
     def __str__(self):
-        return "AGG" if self.mode == AGG else f"SPLIT(Sp={self.cus_prefill},Sd={self.cus_decode},k={self.k_decode_steps})"
+        if self.mode == AGG:
+            return "AGG"
+        if self.mode == CONCURRENT:
+            return "CONCURRENT"
+        return f"SPLIT(Sp={self.cus_prefill},Sd={self.cus_decode},k={self.k_decode_steps})"
 
 
 def _shape_c(shape: AttnShape) -> N.Shape:

@@ -14,7 +14,7 @@ OK = 0
 ERRORS = {-1: "EINVAL", -2: "EUNSUPPORTED", -3: "EWORKSPACE", -4: "EHIP", -5: "ENOMEM", -6: "EPAGE", -7: "EIO"}
 BF16, F32 = 0, 1
 KIND_PREFILL, KIND_DECODE = 0, 1
-AGG, SPLIT = 0, 1
+AGG, SPLIT, CONCURRENT = 0, 1, 2
 STATUS_SLO_INFEASIBLE, STATUS_UNCALIBRATED = 1, 2
 TOTAL_CUS, CU_STEP = 256, 8
 

@@ -320,7 +320,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
         split.cus_decode % DUET_CU_STEP || split.cus_prefill + split.cus_decode > ctx->num_cus)
       return fail(DUET_EINVAL, "split %d/%d: CU shares must be multiples of %d summing to at most %d",
                   split.cus_prefill, split.cus_decode, DUET_CU_STEP, ctx->num_cus);
-  } else if (split.mode != DUET_AGG) {
+  } else if (split.mode != DUET_AGG && split.mode != DUET_CONCURRENT) {
     return fail(DUET_EINVAL, "split mode %d", split.mode);
   }
 
@@ -336,7 +336,12 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   if (split.mode == DUET_SPLIT) {
     if ((rc = get_stream(ctx, split.cus_decode, 0, &sd))) return rc;
     if ((rc = get_stream(ctx, split.cus_prefill, 1, &sp))) return rc;
+  } else if (split.mode == DUET_CONCURRENT) {
+    // two streams whose masks both cover every CU
+    if ((rc = get_stream(ctx, ctx->num_cus, 0, &sd))) return rc;
+    if ((rc = get_stream(ctx, ctx->num_cus, 1, &sp))) return rc;
   }
+  const bool forked = split.mode != DUET_AGG;
 
   char* ws = static_cast<char*>(workspace);
   AttnArgs a;
@@ -383,7 +388,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   // caller's stream.  Spatial sharing forks both CU-masked streams off the caller's stream and
   // enqueues the two halves layer by layer, alternating, so neither half waits for the host to
   // finish enqueueing the other.
-  if (split.mode == DUET_SPLIT) {
+  if (forked) {
     HIP_TRY(hipEventRecord(ctx->ev_fork, order));
     if (has_decode) HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
     if (has_prefill) HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
@@ -405,7 +410,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l + 1], sp));
     }
   }
-  if (split.mode == DUET_SPLIT) {
+  if (forked) {
     HIP_TRY(hipEventRecord(ctx->ev_djoin, sd));
     HIP_TRY(hipEventRecord(ctx->ev_pjoin, sp));
     HIP_TRY(hipStreamWaitEvent(order, ctx->ev_djoin, 0));

@@ -99,3 +99,10 @@ def test_workspace_holds_a_counter_per_layer(native):
     assert native.duet_workspace_bytes(ctypes.byref(_shape(num_layers=200)), ctypes.byref(b), ctypes.byref(many)) == 0
     # 200 four-byte counters where one layer's counter fits the 256-byte head
     assert many.value - one.value >= 200 * 4 - 256
+
+
+def test_model_rejects_concurrent_control_mode(native):
+    arr, b = _batch([(1, 0, 1, 10)])
+    us = ctypes.c_double()
+    assert native.duet_predict_iter_latency(None, ctypes.byref(_shape()), ctypes.byref(b), N.CuSplit(N.CONCURRENT, 256, 256, 1),
+                                            ctypes.byref(us)) == -1

@@ -211,3 +211,14 @@ def test_iteration_layers_match_single_layer_calls(ctx, dtype):
         assert mx <= F32_MAX_ABS
     else:
         assert mx <= BF16_MAX_ABS and mean <= BF16_MEAN_ABS
+
+
+def test_concurrent_control_mode_matches_aggregated(ctx):
+    """The unpartitioned two-stream control computes the same bits as aggregated execution."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    b = wl.make_batch(wl.LLAMA3_8B, [(0, 200, 50), (1, 1, 1000), (1, 1, 77)], page_seed=12)
+    q, kc, vc, pt = _case(b, seed=3400, gen_device="cpu")
+    agg = _run(ctx, b, q, kc, vc, pt, duet.CuSplit.agg())
+    con = _run(ctx, b, q, kc, vc, pt, duet.CuSplit.concurrent())
+    assert torch.equal(agg, con)
