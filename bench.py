@@ -339,8 +339,10 @@ def main():
     it = profiled(n_prof, 2, 1, used)
     kern = profiled(n_prof, 2, 2, used)
     if args.no_agg:
-        agg_it = agg_kern = agg_wall = None
+        agg_it = agg_kern = agg_wall = conc_it = None
     else:
+        # control: both halves at once on two unpartitioned streams
+        conc_it = profiled(n_prof, 2, 1, duet.CuSplit.concurrent())
         agg_it = profiled(n_prof, 2, 1, duet.CuSplit.agg())
         agg_kern = profiled(n_prof, 2, 2, duet.CuSplit.agg())
         torch.cuda.synchronize()
@@ -428,6 +430,7 @@ def main():
         "iteration_us": round(it["iteration_us"], 1),
         "agg_us": rnd(agg_wall and agg_wall * 1e6, 1),
         "agg_iteration_us": rnd(agg_it and agg_it["iteration_us"], 1),
+        "concurrent_unpartitioned_iteration_us": rnd(conc_it and conc_it["iteration_us"], 1),
         "speedup_vs_agg": rnd(agg_wall and agg_wall / wall, 4),
         "agg_pred_us": round(agg_pred, 1),
         "chosen_pred_us": round(duet.predict_iter_latency(rows3, used, shape, ctx.model), 1),

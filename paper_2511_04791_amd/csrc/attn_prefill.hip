@@ -39,7 +39,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #endif
 constexpr int kWaves = DUET_PREFILL_WAVES;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kStages = 4;  // LDS ring: loads run three tiles ahead of the tile in use
+#ifndef DUET_PREFILL_STAGES
+#define DUET_PREFILL_STAGES 4
+#endif
+// LDS ring of kStages tiles: the tile in use plus kStages - 1 in flight.
+constexpr int kStages = DUET_PREFILL_STAGES;
+static_assert(kStages >= 2, "the ring needs a tile in use and one in flight");
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -141,7 +146,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   // 16 i .. 16 i + 15 of a 1 KiB LDS block).  Each tile is KB blocks of K and KB blocks of V^T;
   // wave w loads blocks w, w + kWaves, ...  A lane's source is fixed by the block and the lane
   // (the inverse of the LDS chunk swizzle) except for the page id, so only the id changes per
-  // tile.  Loads run three tiles ahead through a four-stage ring.
+  // tile.  Loads run kStages - 1 tiles ahead of the tile in use.
   constexpr int KB = BN * D * 2 / 1024;   // 1 KiB blocks per tile per tensor
   constexpr int BPW = KB / kWaves;        // blocks per wave per tensor
   static_assert(BPW >= 1 && KB % kWaves == 0, "tile blocks must divide evenly among waves");
@@ -180,12 +185,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       load_lds16(vbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + v_off[i], vdst + blk * 512);
     }
   };
-  // Waits until this wave's loads of all but the `later` most recent tiles have landed.
+  // Waits until this wave's loads of all but the `later` most recent tiles have landed
+  // (later <= kStages - 2).
   auto wait_tiles = [&](int later) {
-    constexpr int kLoadsPerTile = 2 * BPW;
+    constexpr int L1 = 2 * BPW, L2 = 4 * BPW;  // loads of one and of two tiles
+    static_assert(kStages <= 4 && L2 < 64, "wait counts are spelled out for up to two later tiles");
     // s_waitcnt: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt left at their maxima
-    if (later >= 2) __builtin_amdgcn_s_waitcnt(((2 * kLoadsPerTile) & 15) | (((2 * kLoadsPerTile) >> 4) << 14) | 0x0F70);
-    else if (later == 1) __builtin_amdgcn_s_waitcnt((kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14) | 0x0F70);
+    if (kStages >= 4 && later >= 2) __builtin_amdgcn_s_waitcnt((L2 & 15) | ((L2 >> 4) << 14) | 0x0F70);
+    else if (kStages >= 3 && later >= 1) __builtin_amdgcn_s_waitcnt((L1 & 15) | ((L1 >> 4) << 14) | 0x0F70);
     else __builtin_amdgcn_s_waitcnt(0x0F70);
   };
   // Values of keys >= L (NaN-poisoned tail slots, stand-in pages) must not reach the MFMA: the
@@ -234,8 +241,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     for (int v = 0; v < 16; ++v) oacc[n][v] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
 
-  for (int t = 0; t < 3 && t < n_tiles; ++t) issue_tile(t);
-  publish(0, min(n_tiles - 1, 2));
+  for (int t = 0; t < kStages - 1 && t < n_tiles; ++t) issue_tile(t);
+  publish(0, min(n_tiles - 1, kStages - 2));
 
   // S^T of key tile kt for this wave's 32 rows: K fragments from LDS, Q^T from registers.
   auto scores = [&](int kt, f32x16 (&sacc)[2]) {
@@ -327,9 +334,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
           oacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n][k2], pb[k2], oacc[n], 0, 0, 0);
     }
     if (kt + 1 < n_tiles) {
-      // Stage (kt + 3) % 4 was last read in step kt - 1, which every wave has left.
-      if (kt + 3 < n_tiles) issue_tile(kt + 3);
-      publish(kt + 1, min(n_tiles - 1, kt + 3) - (kt + 1));
+      // Stage (kt + kStages - 1) % kStages was last read in step kt - 1, which every wave has
+      // left (the barrier that published tile kt); tiles kt + 2 .. stay in flight.
+      if (kt + kStages - 1 < n_tiles) issue_tile(kt + kStages - 1);
+      publish(kt + 1, min(n_tiles - 1, kt + kStages - 1) - (kt + 1));
     }
   }
 
