@@ -34,6 +34,10 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
+#ifndef DUET_DECODE_RING
+#define DUET_DECODE_RING 3
+#endif
+constexpr int kRing = DUET_DECODE_RING;  // page buffers per wave: kRing - 1 pages in flight
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
@@ -186,22 +190,24 @@ __device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w
     }
   };
 
-  // Three page buffers used in turn: the next two pages are in flight while one page is
+  // kRing page buffers used in turn: the next kRing - 1 pages are in flight while one page is
   // computed.  The split has at most PPS pages and the loop is fully unrolled, so no buffer is
   // ever copied and every wait counts exactly the loads still needed.
-  Page<D> buf[3];
-  Ids ids[3];
-  ids[0] = page_id(pb);
-  load_page<D>(buf[0], kbase, vbase, ids[0].slab, lane);
-  ids[1] = page_id(pb + 1);
-  load_page<D>(buf[1], kbase, vbase, ids[1].slab, lane);
+  constexpr int R = kRing;
+  Page<D> buf[R];
+  Ids ids[R];
+#pragma unroll
+  for (int k = 0; k < R - 1 && k < PPS; ++k) {
+    ids[k] = page_id(pb + k);
+    load_page<D>(buf[k], kbase, vbase, ids[k].slab, lane);
+  }
 #pragma unroll
   for (int k = 0; k < PPS; ++k) {
-    if (k + 2 < PPS) {
-      ids[(k + 2) % 3] = page_id(pb + k + 2);
-      load_page<D>(buf[(k + 2) % 3], kbase, vbase, ids[(k + 2) % 3].slab, lane);
+    if (k + R - 1 < PPS) {
+      ids[(k + R - 1) % R] = page_id(pb + k + R - 1);
+      load_page<D>(buf[(k + R - 1) % R], kbase, vbase, ids[(k + R - 1) % R].slab, lane);
     }
-    compute(buf[k % 3], pb + k, ids[k % 3]);
+    compute(buf[k % R], pb + k, ids[k % R]);
     if (pb + k + 1 >= pe) break;
   }
 
