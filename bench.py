@@ -81,8 +81,9 @@ def committed_traffic(kernel: str, source: str, units: float):
 
 
 def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
-    """The fp64 oracle on the host cores over the same inputs: all decode requests plus as many
-    prefill query heads as fit the time budget, extrapolated to one full iteration."""
+    """The fp64 oracle on the host cores over the same inputs: decode requests (all of them, or as
+    many as fit half the time budget) plus as many prefill query heads as fit the rest, each
+    extrapolated to all requests / heads of one layer."""
     import numpy as np
     import torch
     from oracle import attention as oa
@@ -95,7 +96,6 @@ def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
     dec = [r for r in range(batch.num_reqs) if batch.kinds[r] == 1]
     pre = [r for r in range(batch.num_reqs) if batch.kinds[r] == 0]
     to64 = lambda t: t.detach().to("cpu", torch.float64).numpy()
-    qh = to64(q)
 
     def logical(r):
         L = int(batch.kv_lens[r])
@@ -106,29 +106,51 @@ def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
         return K, V
 
     t0 = time.perf_counter()
+    dec_done = 0
     for r in dec:
+        if dec_done > 0 and time.perf_counter() - t0 > budget_s / 2:
+            break
         K, V = logical(r)
         s = int(batch.q_starts[r])
-        oa.attend(qh[s:s + 1], K, V, int(batch.kv_lens[r]) - 1)
+        oa.attend(to64(q[s:s + 1]), K, V, int(batch.kv_lens[r]) - 1)
+        dec_done += 1
     t_dec = time.perf_counter() - t0
     t_pre, heads_done, heads_total = 0.0, 0, 0
     for r in pre:
         K, V = logical(r)
         s, ql, c = int(batch.q_starts[r]), int(batch.q_lens[r]), int(batch.cached_lens[r])
+        qh = to64(q[s:s + ql])
         heads_total += sh.num_q_heads
         g = sh.num_q_heads // sh.num_kv_heads
         for h in range(sh.num_q_heads):
             if t_dec + t_pre > budget_s and heads_done > 0:
                 break
             t1 = time.perf_counter()
-            oa.attend(qh[s:s + ql, h:h + 1], K[:, h // g:h // g + 1], V[:, h // g:h // g + 1], c)
+            oa.attend(qh[:, h:h + 1], K[:, h // g:h // g + 1], V[:, h // g:h // g + 1], c)
             t_pre += time.perf_counter() - t1
             heads_done += 1
-    full = t_dec + (t_pre * heads_total / heads_done if heads_done else 0.0)
-    sample = (f"all {len(dec)} decode requests and {heads_done}/{heads_total} prefill query heads of the "
-              f"benchmark iteration, fp64 numpy oracle, extrapolated to the full iteration")
+    full = (t_dec * len(dec) / dec_done if dec_done else 0.0) + (t_pre * heads_total / heads_done if heads_done else 0.0)
+    sample = (f"{dec_done}/{len(dec)} decode requests and {heads_done}/{heads_total} prefill query heads of one layer, "
+              f"fp64 numpy oracle, extrapolated to the full layer")
     return {"value": round(full * 1e6, 1), "unit": "us", "cores": int(threads), "kind": "oracle", "sample": sample,
             "measured_s": round(t_dec + t_pre, 3)}
+
+
+WORKLOADS = {
+    "llama8b-mixed": "llama3-8b attention, {L} layers per iteration: 1 prefill chunk of 2048 tokens at prefix 0 + "
+                     "64 decodes (context U[512,4096]), 32 q-heads / 8 kv-heads / head_dim 128, page 16, pages "
+                     "randomly placed",
+    "decode-heavy": "llama3-8b attention, {L} layer: 256 decodes (context min(32768, LogN(median 8192, sigma 0.8))) "
+                    "+ 1 prefill chunk of 512 tokens after 16384 cached, pages scattered through a ~70 GB pool",
+    "prefill-heavy-70b": "llama3-70b attention (64 q-heads / 8 kv-heads / head_dim 128), {L} layer: 1 prefill chunk "
+                         "of 8192 tokens after 24576 cached + 32 decodes at context 2048, pages randomly placed",
+}
+
+
+def make_workload(name):
+    from paper_2511_04791_amd import workloads as wl
+    return {"llama8b-mixed": wl.llama8b_mixed, "decode-heavy": wl.decode_heavy,
+            "prefill-heavy-70b": wl.prefill_heavy_70b}[name]()
 
 
 def trace_main(args):
@@ -139,7 +161,8 @@ def trace_main(args):
     iteration runs in always-aggregated mode and in adaptive mode (Algorithm 1 on the calibrated
     model) at the TBT SLO of 50 ms; a third pass uses, per iteration, a bound 1% under the
     aggregated prediction, so the spatial branch is taken whenever the model finds a split that
-    helps (an attention-only iteration is far below 50 ms).  Latencies are fork-to-join events;
+    helps and keeps aggregated execution when the model predicts the split to be slower (an
+    attention-only iteration is far below 50 ms).  Latencies are fork-to-join events;
     the decode-ready time (fork to the end of the last decode kernel) is when the iteration's
     decode tokens exist, the attention share of their time between tokens.  KV pages come from
     one seeded random pool per layer."""
@@ -150,7 +173,7 @@ def trace_main(args):
     from paper_2511_04791_amd import workloads as wl
     from paper_2511_04791_amd.calibration import calibrate_model
 
-    L = args.layers
+    L = args.layers if args.layers is not None else 32
     ctx = duet.Context(0)
     if not args.no_calibrate:
         calibrate_model(ctx)
@@ -193,7 +216,9 @@ def trace_main(args):
                 sp = duet.CuSplit.agg()
             else:
                 tau = 50000.0 if name == "adaptive_50ms" else 0.99 * t_agg
-                sp = duet.choose_cu_split(rows3, tau, sh, ctx.model, max_decode_steps=1)[0]
+                sp, pred = duet.choose_cu_split(rows3, tau, sh, ctx.model, max_decode_steps=1)[:2]
+                if name == "adaptive_tight" and sp.mode == duet.SPLIT and pred >= t_agg:
+                    sp = duet.CuSplit.agg()   # this mode only splits when the model predicts a gain
                 chosen[name].append(sp.mode == duet.SPLIT)
             for rep in range(2):  # the first call on a new CU split creates its streams
                 ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
@@ -235,7 +260,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--layers", type=int, default=32, help="attention layers per iteration (Llama-3-8B: 32)")
+    ap.add_argument("--layers", type=int, default=None,
+                    help="attention layers per iteration (default 32 for the Llama-3-8B mixed batch, 1 otherwise)")
+    ap.add_argument("--workload", choices=list(WORKLOADS), default="llama8b-mixed",
+                    help="the mixed batch (default), the decode-heavy batch in a ~70 GB pool, or the prefill-heavy "
+                         "Llama-3-70B batch")
     ap.add_argument("--mode", choices=["adaptive", "agg", "split"], default="adaptive")
     ap.add_argument("--split", default="", help="Sp,Sd for --mode split")
     ap.add_argument("--tbt-slo-us", type=float, default=None,
@@ -269,15 +298,18 @@ def main():
     if args.trace:
         trace_main(args)
         return
-    L = args.layers
+    L = args.layers if args.layers is not None else (32 if args.workload == "llama8b-mixed" else 1)
+    if args.workload == "decode-heavy" and L != 1:
+        print("the decode-heavy batch holds a ~70 GB page pool: one layer only", file=sys.stderr)
+        sys.exit(2)
+    batch = make_workload(args.workload)
     ctx = duet.Context(0)
     calib = {}
     if not args.no_calibrate:
         t0 = time.perf_counter()
-        calib = calibrate_model(ctx)
+        calib = calibrate_model(ctx, shape=batch.shape)
         calib["seconds"] = round(time.perf_counter() - t0, 2)
 
-    batch = wl.llama8b_mixed()
     layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
     qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
     del layers
@@ -294,8 +326,12 @@ def main():
     choose_us = []
 
     def choose():
+        # Algorithm 1 proposes a split once the aggregated estimate passes tau; the benchmark keeps
+        # aggregated execution when the model predicts the proposed split to be slower.
         t0 = time.perf_counter()
         sp, pred, rho, flags = duet.choose_cu_split(rows3, tau, shape, ctx.model, max_decode_steps=1)
+        if sp.mode == duet.SPLIT and pred >= agg_pred:
+            sp = duet.CuSplit.agg()
         choose_us.append((time.perf_counter() - t0) * 1e6)
         return sp
 
@@ -423,9 +459,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"llama3-8b attention, {L} layers per iteration: 1 prefill chunk of 2048 tokens at "
-                               "prefix 0 + 64 decodes (context U[512,4096]), 32 q-heads / 8 kv-heads / head_dim "
-                               "128, page 16, pages randomly placed",
+        "config": {"workload": WORKLOADS[args.workload].format(L=L),
                    "layers": L, "mode": args.mode, "split": str(used), "tbt_slo_us": round(tau, 1)},
         "iteration_us": round(it["iteration_us"], 1),
         "agg_us": rnd(agg_wall and agg_wall * 1e6, 1),

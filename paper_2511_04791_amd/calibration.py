@@ -43,15 +43,18 @@ def _times(ctx, batch, q, kc, vc, pt, split, reps, warmup=1):
 
 
 def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, prefill_len: int = 2048,
-                    shared_layers: int = 6) -> dict:
-    """Probe tables, then kernel-calibrated tables written into ctx.model.  Returns a report."""
+                    shared_layers: int = 6, shape=None) -> dict:
+    """Probe tables, then kernel-calibrated tables written into ctx.model.  Returns a report.
+    `shape` (default Llama-3-8B attention) sets the head counts of the calibration batches."""
     import torch
     ctx.calibrate(scratch)
     model = ctx.model
     _, probe_fl, probe_by = model.tables()
-    sh = wl.LLAMA3_8B
+    sh = wl.LLAMA3_8B if shape is None else shape
     pre = wl.make_batch(sh, [(wl.KIND_PREFILL, prefill_len, 0)], page_seed=seed)
-    mixed = wl.llama8b_mixed(seed=seed)
+    mixed8b = wl.llama8b_mixed(seed=seed)
+    mixed = wl.make_batch(sh, [(int(k), int(q), int(c)) for k, q, c in
+                               zip(mixed8b.kinds, mixed8b.q_lens, mixed8b.cached_lens)], page_seed=seed)
     dec = wl.make_batch(sh, [(wl.KIND_DECODE, 1, int(c)) for c in mixed.cached_lens[1:]], page_seed=seed + 1)
     f_pre, _ = batch_work(pre.seq_meta, sh, wl.KIND_PREFILL)
     _, b_dec = batch_work(dec.seq_meta, sh, wl.KIND_DECODE)
