@@ -15,6 +15,12 @@ Operators"):
 * Grouped-query attention: h_q query heads share h_kv key/value heads, query head h reading
   key/value head h // (h_q / h_kv).
 
+Look-ahead decode (Section 4.3, interruption-free dispatch): the KV slots of k future decode
+steps are allocated before the steps run. Decode step s (s = 1 .. k - 1) of a request with c
+cached tokens first writes its new token's key and value rows at absolute position c + s. It
+then attends over the c + s + 1 keys 0 .. c + s. Step 0 is the ordinary decode, whose token at
+position c is already in the cache.
+
 Cache layouts: K pages are [page, kv_head, slot, dim], V pages are [page, kv_head, dim, slot].
 Token t of a request is slot t % page_size of physical page page_table[r, t // page_size].
 All inputs are widened to float64 exactly before any arithmetic.
@@ -95,3 +101,45 @@ def mixed_batch(q, k_cache, v_cache, page_table, seq_meta, page_size: int = 16, 
         V = gather_kv(v_cache, page_table[r], L, page_size, dim_major=True)
         out[q_start:q_start + q_len] = attend(q[q_start:q_start + q_len], K, V, cached, row_block=row_block)
     return out
+
+
+def append_token(k_cache, v_cache, page_row, pos: int, k_row, v_row, page_size: int) -> None:
+    """Write one token's key row and value row ([h_kv, d] each) into the paged cache, in place.
+    The token goes to slot pos % page_size of physical page page_row[pos // page_size]. K pages
+    are token-major, so the key row fills [page, :, slot, :]. V pages are dim-major, so the value
+    row fills the column [page, :, :, slot]. A pure copy."""
+    page = int(np.asarray(page_row)[pos // page_size])
+    if page < 0:
+        raise ValueError(f"position {pos} has no page in this row")
+    slot = pos % page_size
+    k_cache[page, :, slot, :] = k_row
+    v_cache[page, :, :, slot] = v_row
+
+
+def lookahead_decode(q_ahead, k_ahead, v_ahead, k_cache, v_cache, page_table, seq_meta, k: int,
+                     page_size: int = 16):
+    """Decode steps 1 .. k - 1 of one layer of a look-ahead call (Section 4.3).
+
+    The decode requests are the rows of seq_meta with kind 1, in order; decode request i of step s
+    uses q_ahead[s - 1][i] ([h_q, d]) and writes k_ahead[s - 1][i] / v_ahead[s - 1][i] ([h_kv, d])
+    at position c + s. Steps run in order, so step s sees the tokens of steps 1 .. s - 1.
+    Returns (outs, k_cache', v_cache'): outs[s - 1] is [R_d, h_q, d] in float64, and the caches
+    are float64 copies holding the written tokens. The inputs are left unchanged.
+    """
+    meta = np.asarray(seq_meta)
+    kc = np.array(k_cache, dtype=np.float64)
+    vc = np.array(v_cache, dtype=np.float64)
+    dec = [r for r in range(meta.shape[0]) if int(meta[r, 0]) == 1]
+    outs = []
+    for s in range(1, k):
+        q_s = np.asarray(q_ahead[s - 1], dtype=np.float64)
+        out = np.empty(q_s.shape)
+        for i, r in enumerate(dec):
+            pos = int(meta[r, 3]) + s
+            append_token(kc, vc, page_table[r], pos, np.asarray(k_ahead[s - 1][i], dtype=np.float64),
+                         np.asarray(v_ahead[s - 1][i], dtype=np.float64), page_size)
+            K = gather_kv(kc, page_table[r], pos + 1, page_size, dim_major=False)
+            V = gather_kv(vc, page_table[r], pos + 1, page_size, dim_major=True)
+            out[i] = attend(q_s[i][None], K, V, pos)[0]
+        outs.append(out)
+    return outs, kc, vc

@@ -219,3 +219,93 @@ def test_attend_row_matches_full():
     full = oa.attend(q, K, V, 20)
     for i in (0, 4, 9):
         assert np.max(np.abs(oa.attend_row(q[i], K, V, 20 + i) - full[i])) < 1e-13
+
+
+def _lookahead_case(rng, ctxs, k, h_q=4, h_kv=2, d=8, prefill=(5, 7)):
+    """Decode requests with c cached tokens each (the token at position c already in the cache),
+    page rows preallocated for c + k tokens, one prefill request in front, and the new rows of
+    look-ahead steps 1 .. k - 1.  Returns the oracle's inputs plus the logical sequences."""
+    pq, pc = prefill
+    lens = [pq + pc] + [c + k for c in ctxs]            # tokens each row must have pages for
+    n_pages = [-(-n // PS) for n in lens]
+    total = sum(n_pages) + 3
+    perm = rng.permutation(total)
+    table = np.full((len(lens), max(n_pages)), -1, dtype=np.int64)
+    off = 0
+    for r, n in enumerate(n_pages):
+        table[r, :n] = perm[off:off + n]
+        off += n
+    Ks = [rng.standard_normal((pq + pc, h_kv, d))] + [rng.standard_normal((c + 1, h_kv, d)) for c in ctxs]
+    Vs = [rng.standard_normal((pq + pc, h_kv, d))] + [rng.standard_normal((c + 1, h_kv, d)) for c in ctxs]
+    kc = _scatter(Ks, table, total, dim_major=False)
+    vc = _scatter(Vs, table, total, dim_major=True)
+    meta = np.array([(0, 0, pq, pc)] + [(1, pq + i, 1, c) for i, c in enumerate(ctxs)])
+    R_d = len(ctxs)
+    q_ahead = [rng.standard_normal((R_d, h_q, d)) for _ in range(k - 1)]
+    k_ahead = [rng.standard_normal((R_d, h_kv, d)) for _ in range(k - 1)]
+    v_ahead = [rng.standard_normal((R_d, h_kv, d)) for _ in range(k - 1)]
+    return kc, vc, table, meta, Ks, Vs, q_ahead, k_ahead, v_ahead
+
+
+def test_lookahead_matches_brute_force_on_concatenated_sequences():
+    """Step s of a decode request equals the definition evaluated on its logical sequence built by
+    concatenation: the c + 1 cached tokens, then the new tokens of steps 1 .. s (Section 4.3).
+    Contexts put c + s across page boundaries."""
+    rng = np.random.default_rng(40)
+    ctxs, k = [14, 30, 0, 47], 5
+    kc, vc, table, meta, Ks, Vs, qa, ka, va = _lookahead_case(rng, ctxs, k)
+    outs, _, _ = oa.lookahead_decode(qa, ka, va, kc, vc, table, meta, k, PS)
+    assert len(outs) == k - 1
+    for s in range(1, k):
+        for i, c in enumerate(ctxs):
+            K = np.concatenate([Ks[1 + i]] + [ka[t - 1][i][None] for t in range(1, s + 1)])
+            V = np.concatenate([Vs[1 + i]] + [va[t - 1][i][None] for t in range(1, s + 1)])
+            want = _brute(qa[s - 1][i][None], [K], [V], [(1, 0, 1, c + s)], 4, 2)
+            assert np.max(np.abs(outs[s - 1][i] - want[0])) < 1e-12, (s, i)
+
+
+def test_lookahead_cache_holds_exactly_the_written_tokens():
+    """After the call the caches equal a fresh scatter of the full logical sequences: each new
+    token in its own slot (K token-major, V dim-major), every other slot unchanged (NaN stays NaN)."""
+    rng = np.random.default_rng(41)
+    ctxs, k = [15, 31, 2], 4
+    kc, vc, table, meta, Ks, Vs, qa, ka, va = _lookahead_case(rng, ctxs, k)
+    _, kc2, vc2 = oa.lookahead_decode(qa, ka, va, kc, vc, table, meta, k, PS)
+    fullK = [Ks[0]] + [np.concatenate([Ks[1 + i]] + [ka[t][i][None] for t in range(k - 1)]) for i in range(len(ctxs))]
+    fullV = [Vs[0]] + [np.concatenate([Vs[1 + i]] + [va[t][i][None] for t in range(k - 1)]) for i in range(len(ctxs))]
+    assert np.array_equal(kc2, _scatter(fullK, table, kc.shape[0], dim_major=False), equal_nan=True)
+    assert np.array_equal(vc2, _scatter(fullV, table, vc.shape[0], dim_major=True), equal_nan=True)
+    # the inputs are not modified
+    assert np.array_equal(kc, _scatter(Ks, table, kc.shape[0], dim_major=False), equal_nan=True)
+
+
+def test_lookahead_single_step_writes_nothing():
+    rng = np.random.default_rng(42)
+    kc, vc, table, meta, *_ = _lookahead_case(rng, [20, 3], 1)
+    outs, kc2, vc2 = oa.lookahead_decode([], [], [], kc, vc, table, meta, 1, PS)
+    assert outs == []
+    assert np.array_equal(kc2, kc, equal_nan=True) and np.array_equal(vc2, vc, equal_nan=True)
+
+
+def test_lookahead_step_with_repeated_token_is_uniform_over_the_new_keys():
+    """Closed form: with a zero query every visible key has the same weight, so step s returns the
+    mean of the c + s + 1 visible values."""
+    rng = np.random.default_rng(43)
+    ctxs, k = [9, 16], 3
+    kc, vc, table, meta, Ks, Vs, qa, ka, va = _lookahead_case(rng, ctxs, k)
+    qa = [np.zeros_like(x) for x in qa]
+    outs, _, _ = oa.lookahead_decode(qa, ka, va, kc, vc, table, meta, k, PS)
+    for s in range(1, k):
+        for i in range(len(ctxs)):
+            V = np.concatenate([Vs[1 + i]] + [va[t - 1][i][None] for t in range(1, s + 1)])
+            for h in range(4):
+                assert np.allclose(outs[s - 1][i, h], V[:, h // 2].mean(axis=0), atol=1e-13)
+
+
+def test_lookahead_rejects_a_missing_slot():
+    rng = np.random.default_rng(44)
+    kc, vc, table, meta, Ks, Vs, qa, ka, va = _lookahead_case(rng, [15], 2)
+    table = table.copy()
+    table[1, 1] = -1          # the page that position 16 needs
+    with pytest.raises(ValueError):
+        oa.lookahead_decode(qa, ka, va, kc, vc, table, meta, 2, PS)
