@@ -121,6 +121,11 @@ typedef struct {
   double prefill_start_us;  /* fork to the start of the first prefill kernel */
   double prefill_total_us;  /* prefill half: first prefill start to last prefill end */
   double layers;            /* number of layers of the call */
+  /* duet_attn_lookahead calls only (0 otherwise; the decode_partial/reduce fields are then 0,
+   * since the decode kernels run inside graphs): */
+  double decode_steps;         /* k */
+  double decode_step_us;       /* decode half span / k (with AGG the span includes the prefill) */
+  double decode_first_step_us; /* start of decode step 0 to its end: when step 0's tokens are ready */
 } duet_kernel_times;
 
 typedef struct duet_ctx duet_ctx;
@@ -236,6 +241,58 @@ int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* cons
                         const int32_t* page_table, int32_t max_pages_per_req, const duet_batch* batch,
                         duet_cu_split split, void* workspace, size_t workspace_bytes, void* const* out,
                         void* stream);
+
+/* ---- look-ahead decode (Section 4.3, interruption-free dispatch) -------------------------------
+ *
+ * Decode requests get KV slots for k future steps ahead of time, and the k decode steps run back
+ * to back with no host synchronisation between them; the decode kernels of a step are replayed
+ * from a graph recorded once, while the prefill kernels are launched one by one.  Here one call
+ * is one prefill step plus k = split.k_decode_steps decode steps (Algorithm 1 sizes k so that k
+ * decode steps fit in one prefill step: t = max(k t_d, t_p)). */
+
+/* Workspace for duet_attn_lookahead with k_decode_steps steps (shape->num_layers layers):
+ * duet_workspace_bytes' layout plus a decode work counter per (step, layer) and the metadata
+ * and work lists of steps 1 .. k - 1.  Host only. */
+int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* batch, int32_t k_decode_steps,
+                                   size_t* bytes);
+
+/* One prefill step and k = split.k_decode_steps (1 .. 64) decode steps over shape->num_layers
+ * layers (num_layers * k <= 16384).
+ *   Step 0 is duet_attn_iteration on (q, k_cache, v_cache, out): every request of the batch,
+ *   the decode tokens at position cached_len already in the cache.
+ *   Decode step s = 1 .. k - 1, layer l, uses index x = (s - 1) * num_layers + l of the
+ *   look-ahead arrays.  Decode request i (the i-th kind-DECODE row of batch, in order) first
+ *   writes its new token's key row k_ahead[x][i] and value row v_ahead[x][i] (each [h_kv, d])
+ *   at position p = cached_len + s: slot p % 16 of physical page page_table[r][p / 16]; keys
+ *   into the token-major k_cache[l], values into the dim-major v_cache[l] column.  It then
+ *   attends over the p + 1 keys 0 .. p with query q_ahead[x][i] ([h_q, d]) into out_ahead[x][i].
+ *   q_ahead, k_ahead, v_ahead and out_ahead are host arrays of (k - 1) * num_layers device
+ *   pointers to [R_d, h_q or h_kv, d] tensors (R_d = number of decode requests), caller-owned;
+ *   they may be NULL when k == 1 or R_d == 0.
+ * Steps run in order, so step s reads the tokens steps 1 .. s - 1 wrote.  Every decode request's
+ * page_table row must hold pages for cached_len + k tokens; the slots written must not be read
+ * by any other request of the batch (the prefill half runs at the same time).
+ * SPLIT / CONCURRENT: every decode step is enqueued (decode first) on the decode stream, then the
+ * prefill layers on the prefill stream; one fork and one join on `stream`.  AGG: decode step 0,
+ * then the prefill layers, then decode steps 1 .. k - 1, on `stream`.
+ * Decode steps run from graphs by default: a step's kernels are captured on first use and the
+ * graph is replayed on later calls whose launch arguments (pointers, work-list sizes, CU share)
+ * are the same; at most 128 graphs are kept per context (least recently used evicted, after a
+ * device synchronisation).  Outputs and cache writes are bit-identical with graphs on or off,
+ * and step 0 is bit-identical to duet_attn_iteration.  Errors as duet_attn_iteration; a page id
+ * outside [0, num_phys_pages) at a written slot skips the write and sets the error word. */
+int duet_attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q, const void* const* q_ahead,
+                        const void* const* k_ahead, const void* const* v_ahead, void* const* k_cache,
+                        void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                        size_t workspace_bytes, void* const* out, void* const* out_ahead, void* stream);
+
+/* Decode steps of duet_attn_lookahead from graphs (enable != 0, the default) or launched one
+ * kernel at a time (enable == 0). */
+int duet_set_decode_graphs(duet_ctx* ctx, int32_t enable);
+
+/* Graphs held by the context, and how many decode steps were captured / replayed so far. */
+int duet_decode_graph_stats(duet_ctx* ctx, int64_t* cached, int64_t* captured, int64_t* replayed);
 
 /* Synchronises `stream`, reads the workspace's error word and clears it: DUET_OK or DUET_EPAGE. */
 int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream);

@@ -32,26 +32,27 @@ class CuSplit:
     k_decode_steps: int = 1
 
     @staticmethod
-    def agg() -> "CuSplit":
-        return CuSplit(AGG, TOTAL_CUS, 0, 1)
+    def agg(k: int = 1) -> "CuSplit":
+        """Aggregated execution; k > 1 only matters to duet_attn_lookahead (k decode steps)."""
+        return CuSplit(AGG, TOTAL_CUS, 0, k)
 
     @staticmethod
     def split(cus_prefill: int, cus_decode: int, k: int = 1) -> "CuSplit":
         return CuSplit(SPLIT, cus_prefill, cus_decode, k)
 
     @staticmethod
-    def concurrent() -> "CuSplit":
+    def concurrent(k: int = 1) -> "CuSplit":
         """Control for measurements: both halves at once on two unpartitioned streams."""
-        return CuSplit(CONCURRENT, TOTAL_CUS, TOTAL_CUS, 1)
+        return CuSplit(CONCURRENT, TOTAL_CUS, TOTAL_CUS, k)
 
     def to_c(self) -> N.CuSplit:
         return N.CuSplit(self.mode, self.cus_prefill, self.cus_decode, self.k_decode_steps)
 
     def __str__(self):
         if self.mode == AGG:
-            return "AGG"
+            return "AGG" if self.k_decode_steps == 1 else f"AGG(k={self.k_decode_steps})"
         if self.mode == CONCURRENT:
-            return "CONCURRENT"
+            return "CONCURRENT" if self.k_decode_steps == 1 else f"CONCURRENT(k={self.k_decode_steps})"
         return f"SPLIT(Sp={self.cus_prefill},Sd={self.cus_decode},k={self.k_decode_steps})"
 
 
@@ -181,6 +182,15 @@ def workspace_bytes(shape: AttnShape, seq_meta) -> int:
     return n.value
 
 
+def lookahead_workspace_bytes(shape: AttnShape, seq_meta, k_decode_steps: int) -> int:
+    b = _BatchC(seq_meta)
+    n = ctypes.c_size_t()
+    N.check(N.lib().duet_lookahead_workspace_bytes(ctypes.byref(_shape_c(shape)), ctypes.byref(b.c),
+                                                   int(k_decode_steps), ctypes.byref(n)),
+            "duet_lookahead_workspace_bytes")
+    return n.value
+
+
 def shape_of(q, k_cache, num_layers: int = 1) -> AttnShape:
     import torch
     if q.dtype == torch.bfloat16:
@@ -290,6 +300,67 @@ class Context:
             N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
                     "duet_check_device_error")
         return outs
+
+    def attn_lookahead(self, qs, q_ahead, k_ahead, v_ahead, k_caches, v_caches, page_table, seq_meta,
+                       cu_split: CuSplit, *, outs=None, outs_ahead=None, workspace=None, stream=None,
+                       check_errors: bool = False):
+        """One prefill step and k = cu_split.k_decode_steps decode steps (duet_attn_lookahead).
+
+        qs, k_caches, v_caches, outs: per-layer lists as in attn_iteration (step 0).  q_ahead,
+        k_ahead, v_ahead, outs_ahead: lists of (k - 1) * L tensors, index (s - 1) * L + l, of shape
+        [R_d, h_q or h_kv, d] with the decode requests in seq_meta order.  The caches are written
+        (steps >= 1 append their tokens).  Returns (outs, outs_ahead)."""
+        import torch
+        L = len(qs)
+        k = int(cu_split.k_decode_steps)
+        n_ahead = (k - 1) * L
+        if L < 1 or len(k_caches) != L or len(v_caches) != L or (outs is not None and len(outs) != L):
+            raise ValueError("qs, k_caches, v_caches (and outs) must be non-empty lists of equal length")
+        if len(q_ahead) != n_ahead or len(k_ahead) != n_ahead or len(v_ahead) != n_ahead:
+            raise ValueError(f"q_ahead, k_ahead and v_ahead need (k - 1) * L = {n_ahead} tensors")
+        shape = shape_of(qs[0], k_caches[0], L)
+        b = _BatchC(seq_meta)
+        n_dec = int((b.rows[:, 0] == 1).sum()) if len(b.rows) else 0
+        for l in range(L):
+            if qs[l].shape != qs[0].shape or qs[l].dtype != qs[0].dtype or k_caches[l].shape != k_caches[0].shape:
+                raise ValueError(f"layer {l}: shapes differ from layer 0")
+            self._check_layer(qs[l], k_caches[l], v_caches[l], page_table, b)
+        for x in range(n_ahead):
+            for t, name, h in ((q_ahead[x], "q_ahead", shape.num_q_heads), (k_ahead[x], "k_ahead", shape.num_kv_heads),
+                               (v_ahead[x], "v_ahead", shape.num_kv_heads)):
+                if not t.is_cuda or not t.is_contiguous() or t.dtype != qs[0].dtype or \
+                        tuple(t.shape) != (n_dec, h, shape.head_dim):
+                    raise ValueError(f"{name}[{x}] must be a contiguous {qs[0].dtype} device tensor "
+                                     f"[{n_dec}, {h}, {shape.head_dim}]")
+        need = lookahead_workspace_bytes(shape, b.rows, k)
+        ws = self.workspace(need) if workspace is None else workspace
+        if outs is None:
+            outs = [torch.empty_like(x) for x in qs]
+        if outs_ahead is None:
+            outs_ahead = [torch.empty_like(x) for x in q_ahead]
+        if len(outs_ahead) != n_ahead:
+            raise ValueError(f"outs_ahead needs {n_ahead} tensors")
+        arr = lambda ts, n: (ctypes.c_void_p * max(n, 1))(*[t.data_ptr() for t in ts])
+        st = torch.cuda.current_stream(qs[0].device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_attn_lookahead(self.handle, ctypes.byref(_shape_c(shape)), arr(qs, L),
+                                            arr(q_ahead, n_ahead), arr(k_ahead, n_ahead), arr(v_ahead, n_ahead),
+                                            arr(k_caches, L), arr(v_caches, L), int(k_caches[0].shape[0]),
+                                            page_table.data_ptr(), int(page_table.shape[1]), ctypes.byref(b.c),
+                                            cu_split.to_c(), ws.data_ptr(), ws.numel(), arr(outs, L),
+                                            arr(outs_ahead, n_ahead), ctypes.c_void_p(st)), "duet_attn_lookahead")
+        if check_errors:
+            N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
+                    "duet_check_device_error")
+        return outs, outs_ahead
+
+    def set_decode_graphs(self, enable: bool):
+        N.check(N.lib().duet_set_decode_graphs(self.handle, 1 if enable else 0), "duet_set_decode_graphs")
+
+    def decode_graph_stats(self) -> dict:
+        c, cap, rep = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        N.check(N.lib().duet_decode_graph_stats(self.handle, ctypes.byref(c), ctypes.byref(cap), ctypes.byref(rep)),
+                "duet_decode_graph_stats")
+        return {"cached": c.value, "captured": cap.value, "replayed": rep.value}
 
     def gather_kv(self, cache, which: int, page_table, req: int, kv_len: int, shape: AttnShape):
         import torch

@@ -40,7 +40,8 @@ class KernelTimes(ctypes.Structure):
     _fields_ = [("decode_partial_us", c_double), ("decode_reduce_us", c_double), ("prefill_us", c_double),
                 ("decode_total_us", c_double), ("iteration_us", c_double),
                 ("decode_start_us", c_double), ("prefill_start_us", c_double), ("prefill_total_us", c_double),
-                ("layers", c_double)]
+                ("layers", c_double), ("decode_steps", c_double), ("decode_step_us", c_double),
+                ("decode_first_step_us", c_double)]
 
 
 P = ctypes.POINTER
@@ -67,6 +68,12 @@ _SIGS = {
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),
     "duet_attn_iteration": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p,
                                       c_int32, P(Batch), CuSplit, c_void_p, c_size_t, P(c_void_p), c_void_p]),
+    "duet_lookahead_workspace_bytes": (c_int32, [P(Shape), P(Batch), c_int32, P(c_size_t)]),
+    "duet_attn_lookahead": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), P(c_void_p),
+                                      P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,
+                                      c_void_p, c_size_t, P(c_void_p), P(c_void_p), c_void_p]),
+    "duet_set_decode_graphs": (c_int32, [c_void_p, c_int32]),
+    "duet_decode_graph_stats": (c_int32, [c_void_p, P(c_int64), P(c_int64), P(c_int64)]),
     "duet_check_device_error": (c_int32, [c_void_p, c_void_p, c_void_p]),
     "duet_gather_kv": (c_int32, [c_void_p, P(Shape), c_int32, c_void_p, c_int64, c_void_p, c_int32, c_int32, c_int32,
                                  c_void_p, c_void_p]),

@@ -36,6 +36,18 @@ struct WorkArgs {
   int32_t prefill_id_cap;  // most pages of any prefill request (sizes the LDS page-id table)
 };
 
+// One decode step's cache write (look-ahead decode): new key and value rows in, paged cache out.
+struct AppendArgs {
+  void* k_cache;         // [P, h_kv, 16, d], written
+  void* v_cache;         // [P, h_kv, d, 16], written
+  const void* k_new;     // [R_d, h_kv, d]: row = the request's q_start in the step's metadata
+  const void* v_new;     // [R_d, h_kv, d]
+  const int32_t* page_table;
+  long long num_phys_pages;
+  int32_t max_pages;
+  int32_t h_kv, head_dim, dtype;
+};
+
 #ifndef DUET_DECODE_PAGES_PER_SPLIT
 #define DUET_DECODE_PAGES_PER_SPLIT 32
 #endif
@@ -57,6 +69,8 @@ int prefill_rows_per_unit(int group, int dtype);
 hipError_t launch_decode_partial(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
 hipError_t launch_decode_reduce(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
 hipError_t launch_prefill(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
+// Writes the new token of every decode request in w.dreq (position = meta cached_len).
+hipError_t launch_kv_append(const AppendArgs& a, const WorkArgs& w, hipStream_t s);
 
 hipError_t launch_gather(const void* cache, int which, int elem_bytes, int h_kv, int d, const int32_t* page_table,
                          int max_pages, long long num_phys, int req, int kv_len, void* out, int32_t* err,

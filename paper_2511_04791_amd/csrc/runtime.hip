@@ -21,6 +21,7 @@
 #include <map>
 #include <mutex>
 #include <new>
+#include <unordered_map>
 #include <vector>
 
 #include "duet_internal.h"
@@ -37,6 +38,8 @@ constexpr size_t kAlign = 256;
 // kCounterOffset on; the head is zeroed by every call's upload.
 constexpr size_t kCounterOffset = 64;
 constexpr int kMaxLayers = 1024;
+constexpr int kMaxLookahead = 64;     // decode steps per look-ahead call
+constexpr size_t kMaxGraphs = 128;    // cached decode-step graphs per context
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
@@ -53,10 +56,21 @@ struct StagingSlot {
   bool pending = false;
 };
 
+// Decode work lists of one look-ahead step s >= 1 (its own metadata: decode request r becomes
+// (decode, i, 1, cached_len + s), i = its index among the decode requests).
+struct StepPlan {
+  std::vector<int4> meta, dreq;
+  std::vector<int32_t> ditems;
+  int n_items = 0, max_split = 0;
+  size_t off_meta = 0, off_dreq = 0, off_ditems = 0;
+};
+
 // Work lists of one iteration and where they live in the caller's workspace.
 struct Plan {
   std::vector<int4> meta, pitems, dreq;
   std::vector<int32_t> ditems;
+  std::vector<StepPlan> ahead;  // look-ahead decode steps 1 .. steps - 1
+  int steps = 1;
   int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0, prefill_id_cap = 0;
   size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, off_pacc = 0, off_pml = 0, upload_bytes = 0,
          total = 0;
@@ -67,7 +81,47 @@ int pages_per_split_for(const duet_shape* s) {
   return s->dtype == DUET_F32 ? kDecodePagesPerSplitF32 : kDecodePagesPerSplit;
 }
 
-void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, bool fill) {
+// Decode work of the batch's decode requests when each holds `extra` more tokens than seq_meta
+// states: per request (req, item_base, n_split, n_pages), and for bf16 the work items in
+// execution order -- every full split first, then the shorter last splits (longest first),
+// packed as i | j << 16 | s << 22.
+void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool fill, std::vector<int4>* dreq,
+                  std::vector<int32_t>* ditems, int64_t* n_dreq, int64_t* n_items, int* max_split) {
+  const int pps = pages_per_split_for(s);
+  dreq->clear();
+  ditems->clear();
+  *n_dreq = 0;
+  *n_items = 0;
+  *max_split = 0;
+  for (int r = 0; r < b->num_reqs; ++r) {
+    const duet_seq_meta& q = b->reqs[r];
+    if (q.kind != DUET_KIND_DECODE) continue;
+    const int64_t L = (int64_t)q.cached_len + q.q_len + extra;
+    const int n_pages = (int)((L + 15) / 16);
+    const int n_split = (n_pages + pps - 1) / pps;
+    if (fill) dreq->push_back(make_int4(r, (int)*n_items, n_split, n_pages));
+    *n_items += (int64_t)s->num_kv_heads * n_split;
+    *max_split = std::max(*max_split, n_split);
+    ++*n_dreq;
+  }
+  if (fill && s->dtype == DUET_BF16) {
+    ditems->reserve(*n_items);
+    for (int pass = 0; pass < 2; ++pass)
+      for (size_t i = 0; i < dreq->size(); ++i) {
+        const int4 d = (*dreq)[i];
+        const bool full_last = d.w % pps == 0;
+        for (int j = 0; j < s->num_kv_heads; ++j)
+          for (int sp = 0; sp < d.z; ++sp) {
+            const bool is_full = sp + 1 < d.z || full_last;
+            if (is_full == (pass == 0)) ditems->push_back((int32_t)i | (j << 16) | (sp << 22));
+          }
+      }
+  }
+}
+
+// Work lists of a call over `layers` layers and `steps` decode steps (steps > 1: look-ahead),
+// and their offsets in the workspace.
+void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps, Plan* p, bool fill) {
   const int g = s->num_q_heads / s->num_kv_heads;
   const int pps = pages_per_split_for(s);
   p->group = g;
@@ -75,10 +129,8 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, b
   p->prefill_id_cap = 0;
   p->meta.clear();
   p->pitems.clear();
-  p->dreq.clear();
-  p->ditems.clear();
-  int64_t n_pitems = 0, n_dreq = 0, n_items = 0;
-  int max_split = 0;
+  p->steps = steps;
+  int64_t n_pitems = 0;
   struct Tile {
     int64_t keys;
     int4 item;
@@ -109,38 +161,19 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, b
           }
         }
       }
-    } else {
-      const int n_pages = (int)((L + 15) / 16);
-      const int n_split = (n_pages + pps - 1) / pps;
-      if (fill) p->dreq.push_back(make_int4(r, (int)n_items, n_split, n_pages));
-      n_items += (int64_t)s->num_kv_heads * n_split;
-      max_split = std::max(max_split, n_split);
-      ++n_dreq;
     }
   }
   if (fill) {
     std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& x, const Tile& y) { return x.keys > y.keys; });
     p->pitems.reserve(tiles.size());
     for (const Tile& t : tiles) p->pitems.push_back(t.item);
-    // bf16 decode items in execution order: every full split first, then the shorter last
-    // splits (longest first), packed as i | j << 16 | s << 22.
-    if (s->dtype == DUET_BF16) {
-      p->ditems.reserve(n_items);
-      for (int pass = 0; pass < 2; ++pass)
-        for (size_t i = 0; i < p->dreq.size(); ++i) {
-          const int4 d = p->dreq[i];
-          const bool full_last = d.w % pps == 0;
-          for (int j = 0; j < s->num_kv_heads; ++j)
-            for (int sp = 0; sp < d.z; ++sp) {
-              const bool is_full = sp + 1 < d.z || full_last;
-              if (is_full == (pass == 0)) p->ditems.push_back((int32_t)i | (j << 16) | (sp << 22));
-            }
-        }
-    }
   }
+  int64_t n_dreq = 0, n_items = 0;
+  int max_split = 0;
+  decode_lists(s, b, 0, fill, &p->dreq, &p->ditems, &n_dreq, &n_items, &max_split);
   p->n_items_decode = (int)n_items;
   p->max_split = max_split;
-  size_t off = align_up(kCounterOffset + (size_t)layers * sizeof(int32_t));
+  size_t off = align_up(kCounterOffset + (size_t)layers * steps * sizeof(int32_t));
   p->off_meta = off;
   off = align_up(off + (size_t)b->num_reqs * sizeof(int4));
   p->off_pitems = off;
@@ -149,16 +182,100 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, Plan* p, b
   off = align_up(off + (size_t)n_dreq * sizeof(int4));
   p->off_ditems = off;
   off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)n_items * sizeof(int32_t) : 0));
+  // Look-ahead steps: each has its own metadata and decode lists; the split-K partials are
+  // shared, since the steps run one after another on one stream.
+  int64_t max_items = n_items;
+  p->ahead.resize(steps - 1);
+  for (int st = 1; st < steps; ++st) {
+    StepPlan& sp = p->ahead[st - 1];
+    sp.meta.clear();
+    if (fill) {
+      int i = 0;
+      for (int r = 0; r < b->num_reqs; ++r) {
+        const duet_seq_meta& q = b->reqs[r];
+        if (q.kind == DUET_KIND_DECODE) sp.meta.push_back(make_int4(q.kind, i++, 1, q.cached_len + st));
+        else sp.meta.push_back(make_int4(q.kind, q.q_start, q.q_len, q.cached_len));
+      }
+    }
+    int64_t nd = 0, ni = 0;
+    decode_lists(s, b, st, fill, &sp.dreq, &sp.ditems, &nd, &ni, &sp.max_split);
+    sp.n_items = (int)ni;
+    max_items = std::max(max_items, ni);
+    sp.off_meta = off;
+    off = align_up(off + (size_t)b->num_reqs * sizeof(int4));
+    sp.off_dreq = off;
+    off = align_up(off + (size_t)nd * sizeof(int4));
+    sp.off_ditems = off;
+    off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)ni * sizeof(int32_t) : 0));
+  }
   p->upload_bytes = off;
   p->off_pacc = off;
-  off = align_up(off + (size_t)n_items * g * s->head_dim * sizeof(float));
+  off = align_up(off + (size_t)max_items * g * s->head_dim * sizeof(float));
   p->off_pml = off;
-  off = align_up(off + (size_t)n_items * g * 2 * sizeof(float));
+  off = align_up(off + (size_t)max_items * g * 2 * sizeof(float));
   p->total = off;
 }
 
 // Fork and join of a profiled call on the caller's stream; A and B bracket probe kernels.
 enum ProfEv { kEvFork, kEvJoin, kEvA, kEvB, kNumProfEv };
+
+// One kernel launch of a decode step; a step's launches are what its graph captures.
+struct DecodeLaunch {
+  enum Kind { kAppend, kPartial, kReduce } kind;
+  AttnArgs a;
+  WorkArgs w;
+  AppendArgs ap;
+};
+
+hipError_t run_launch(const DecodeLaunch& l, hipStream_t st) {
+  switch (l.kind) {
+    case DecodeLaunch::kAppend: return launch_kv_append(l.ap, l.w, st);
+    case DecodeLaunch::kPartial: return launch_decode_partial(l.a, l.w, st);
+    default: return launch_decode_reduce(l.a, l.w, st);
+  }
+}
+
+template <typename T>
+inline uint64_t bits(T x) {
+  static_assert(sizeof(T) <= 8, "field wider than a key word");
+  uint64_t u = 0;
+  std::memcpy(&u, &x, sizeof x);
+  return u;
+}
+
+// Every argument that reaches a kernel (and so fixes a launch's grid), field by field: two
+// steps with equal keys launch identical kernels, so a graph captured for one replays the other.
+void append_key(std::vector<uint64_t>* k, const DecodeLaunch& l) {
+  const AttnArgs& a = l.a;
+  const WorkArgs& w = l.w;
+  const AppendArgs& p = l.ap;
+  const uint64_t f[] = {(uint64_t)l.kind, bits(a.q), bits(a.k_cache), bits(a.v_cache), bits(a.page_table),
+                        bits(a.out), bits(a.num_phys_pages), bits(a.max_pages), bits(a.h_q), bits(a.h_kv),
+                        bits(a.group), bits(a.head_dim), bits(a.dtype), bits(a.scale_log2), bits(w.meta),
+                        bits(w.pitems), bits(w.dreq), bits(w.pacc), bits(w.pml), bits(w.ditems), bits(w.err),
+                        bits(w.work_counter), bits(w.n_pitems), bits(w.n_dreq), bits(w.max_split),
+                        bits(w.n_ditems), bits(w.pages_per_split), bits(w.decode_cus), bits(w.prefill_id_cap),
+                        bits(p.k_cache), bits(p.v_cache), bits(p.k_new), bits(p.v_new), bits(p.page_table),
+                        bits(p.num_phys_pages), bits(p.max_pages), bits(p.h_kv), bits(p.head_dim), bits(p.dtype)};
+  k->insert(k->end(), std::begin(f), std::end(f));
+}
+
+uint64_t hash_key(const std::vector<uint64_t>& k) {
+  uint64_t h = 1469598103934665603ull;  // FNV-1a over the key words
+  for (uint64_t x : k) {
+    for (int b = 0; b < 8; ++b) {
+      h ^= (x >> (8 * b)) & 0xff;
+      h *= 1099511628211ull;
+    }
+  }
+  return h;
+}
+
+struct GraphEntry {
+  std::vector<uint64_t> key;
+  hipGraphExec_t exec = nullptr;
+  uint64_t last_use = 0;
+};
 
 }  // namespace
 
@@ -185,6 +302,15 @@ struct duet_ctx {
   int32_t* dev_flag = nullptr;  // gather error word
   unsigned* dev_sink = nullptr;  // probe sink
   Plan plan;                     // reused host vectors
+  // Look-ahead decode: each step's kernels are captured once into a graph (on a private
+  // capture stream) and replayed on the decode stream while its launch arguments recur.
+  bool decode_graphs = true;
+  hipStream_t capture = nullptr;
+  std::unordered_map<uint64_t, GraphEntry> graphs;
+  uint64_t graph_clock = 0;
+  uint64_t graphs_captured = 0, graphs_replayed = 0;
+  std::vector<hipEvent_t> ev_step;  // decode stream: before step 0, after each step
+  int prof_steps = 0;               // decode steps of the last profiled call (0: not look-ahead)
 };
 
 namespace {
@@ -260,6 +386,11 @@ int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
   std::memcpy(h + p.off_pitems, p.pitems.data(), p.pitems.size() * sizeof(int4));
   std::memcpy(h + p.off_dreq, p.dreq.data(), p.dreq.size() * sizeof(int4));
   std::memcpy(h + p.off_ditems, p.ditems.data(), p.ditems.size() * sizeof(int32_t));
+  for (const StepPlan& sp : p.ahead) {
+    std::memcpy(h + sp.off_meta, sp.meta.data(), sp.meta.size() * sizeof(int4));
+    std::memcpy(h + sp.off_dreq, sp.dreq.data(), sp.dreq.size() * sizeof(int4));
+    std::memcpy(h + sp.off_ditems, sp.ditems.data(), sp.ditems.size() * sizeof(int32_t));
+  }
   HIP_TRY(hipMemcpyAsync(ws, h, p.upload_bytes, hipMemcpyHostToDevice, st));
   HIP_TRY(hipEventRecord(slot.done, st));
   slot.pending = true;
@@ -274,10 +405,12 @@ int check_device_ptr(const void* p, const char* name) {
 // One call over `layers` layers that share the batch, its page table and its work lists.  Each
 // half runs its kernels for every layer back to back on its own stream; one fork and one join
 // per call.
-int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* const* q_l,
-                const void* const* k_l, const void* const* v_l, int64_t num_phys_pages, const int32_t* page_table,
-                int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
-                size_t workspace_bytes, void* const* out_l, void* stream) {
+// Host-side checks of an attention call, before anything is enqueued.  Decode requests must
+// have pages for `extra` tokens past their stated length (look-ahead slots).
+int check_call(duet_ctx* ctx, const duet_shape* shape, int layers, const void* const* q_l, const void* const* k_l,
+               const void* const* v_l, int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
+               const duet_batch* batch, duet_cu_split split, const void* workspace, const void* const* out_l,
+               int extra) {
   if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
   int rc = check_shape(shape);
   if (rc) return rc;
@@ -295,7 +428,8 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   if (num_phys_pages < 1 || num_phys_pages > (int64_t)INT32_MAX)
     return fail(DUET_EINVAL, "num_phys_pages %lld out of range", (long long)num_phys_pages);
   for (int r = 0; r < batch->num_reqs; ++r) {
-    const int64_t L = (int64_t)batch->reqs[r].cached_len + batch->reqs[r].q_len;
+    const duet_seq_meta& q = batch->reqs[r];
+    const int64_t L = (int64_t)q.cached_len + q.q_len + (q.kind == DUET_KIND_DECODE ? extra : 0);
     if ((L + 15) / 16 > max_pages_per_req)
       return fail(DUET_EINVAL, "request %d needs %lld pages, page_table rows hold %d", r, (long long)((L + 15) / 16),
                   max_pages_per_req);
@@ -304,7 +438,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
     int n_dec = 0;
     for (int r = 0; r < batch->num_reqs; ++r) {
       const duet_seq_meta& q = batch->reqs[r];
-      const int64_t L = (int64_t)q.cached_len + q.q_len;
+      const int64_t L = (int64_t)q.cached_len + q.q_len + (q.kind == DUET_KIND_DECODE ? extra : 0);
       if (q.kind == DUET_KIND_DECODE) ++n_dec;
       if (q.kind == DUET_KIND_PREFILL && L > kMaxPrefillKeys)
         return fail(DUET_EUNSUPPORTED, "request %d: prefill attends %lld keys, at most %d supported", r,
@@ -324,9 +458,51 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
     return fail(DUET_EINVAL, "split mode %d", split.mode);
   }
 
+  return DUET_OK;
+}
+
+// Arguments common to every kernel of a call (step 0's work lists; no per-layer pointers).
+void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char* ws, duet_cu_split split,
+               const int32_t* page_table, int64_t num_phys_pages, int32_t max_pages_per_req, AttnArgs* a,
+               WorkArgs* w) {
+  *a = AttnArgs{};
+  a->page_table = page_table;
+  a->num_phys_pages = num_phys_pages;
+  a->max_pages = max_pages_per_req;
+  a->h_q = shape->num_q_heads;
+  a->h_kv = shape->num_kv_heads;
+  a->group = p.group;
+  a->head_dim = shape->head_dim;
+  a->dtype = shape->dtype;
+  a->scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
+  *w = WorkArgs{};
+  w->meta = reinterpret_cast<const int4*>(ws + p.off_meta);
+  w->pitems = reinterpret_cast<const int4*>(ws + p.off_pitems);
+  w->dreq = reinterpret_cast<const int4*>(ws + p.off_dreq);
+  w->pacc = reinterpret_cast<float*>(ws + p.off_pacc);
+  w->pml = reinterpret_cast<float*>(ws + p.off_pml);
+  w->ditems = reinterpret_cast<const int32_t*>(ws + p.off_ditems);
+  w->err = reinterpret_cast<int32_t*>(ws);
+  w->n_ditems = (int)p.ditems.size();
+  w->decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
+  w->n_pitems = (int)p.pitems.size();
+  w->n_dreq = (int)p.dreq.size();
+  w->max_split = p.max_split;
+  w->pages_per_split = p.pages_per_split;
+  w->prefill_id_cap = p.prefill_id_cap;
+}
+
+int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* const* q_l,
+                const void* const* k_l, const void* const* v_l, int64_t num_phys_pages, const int32_t* page_table,
+                int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                size_t workspace_bytes, void* const* out_l, void* stream) {
+  int rc = check_call(ctx, shape, layers, q_l, k_l, v_l, num_phys_pages, page_table, max_pages_per_req, batch, split,
+                      workspace, out_l, 0);
+  if (rc) return rc;
+
   std::lock_guard<std::mutex> lock(ctx->mu);
   Plan& p = ctx->plan;
-  plan_batch(shape, batch, layers, &p, true);
+  plan_batch(shape, batch, layers, 1, &p, true);
   if (workspace_bytes < p.total)
     return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, p.total);
 
@@ -345,30 +521,8 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
 
   char* ws = static_cast<char*>(workspace);
   AttnArgs a;
-  a.page_table = page_table;
-  a.num_phys_pages = num_phys_pages;
-  a.max_pages = max_pages_per_req;
-  a.h_q = shape->num_q_heads;
-  a.h_kv = shape->num_kv_heads;
-  a.group = p.group;
-  a.head_dim = shape->head_dim;
-  a.dtype = shape->dtype;
-  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
   WorkArgs w;
-  w.meta = reinterpret_cast<const int4*>(ws + p.off_meta);
-  w.pitems = reinterpret_cast<const int4*>(ws + p.off_pitems);
-  w.dreq = reinterpret_cast<const int4*>(ws + p.off_dreq);
-  w.pacc = reinterpret_cast<float*>(ws + p.off_pacc);
-  w.pml = reinterpret_cast<float*>(ws + p.off_pml);
-  w.ditems = reinterpret_cast<const int32_t*>(ws + p.off_ditems);
-  w.err = reinterpret_cast<int32_t*>(ws);
-  w.n_ditems = (int)p.ditems.size();
-  w.decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
-  w.n_pitems = (int)p.pitems.size();
-  w.n_dreq = (int)p.dreq.size();
-  w.max_split = p.max_split;
-  w.pages_per_split = p.pages_per_split;
-  w.prefill_id_cap = p.prefill_id_cap;
+  base_args(ctx, shape, p, ws, split, page_table, num_phys_pages, max_pages_per_req, &a, &w);
   const bool prof_iter = ctx->profiling >= 1;
   const bool prof = ctx->profiling >= 2;
   const bool has_decode = w.n_dreq > 0, has_prefill = w.n_pitems > 0;
@@ -422,8 +576,240 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   ctx->prof_decode = has_decode;
   ctx->prof_prefill = has_prefill;
   ctx->prof_layers = layers;
+  ctx->prof_steps = 0;
   return DUET_OK;
 }
+
+int ensure_step_events(duet_ctx* ctx, int steps) {
+  while (ctx->ev_step.size() < (size_t)(steps + 1)) {
+    hipEvent_t e = nullptr;
+    HIP_TRY(hipEventCreate(&e));
+    ctx->ev_step.push_back(e);
+  }
+  return DUET_OK;
+}
+
+void clear_graphs(duet_ctx* ctx) {
+  for (auto& kv : ctx->graphs) (void)hipGraphExecDestroy(kv.second.exec);
+  ctx->graphs.clear();
+}
+
+// Enqueues one decode step on `st`: from its cached graph when one with the same launch
+// arguments exists, else captured now (on the private capture stream, so `st` keeps its
+// pending work and its CU mask governs the replay), or launched directly when graphs are off.
+int run_decode_step(duet_ctx* ctx, const std::vector<DecodeLaunch>& launches, hipStream_t st) {
+  if (!ctx->decode_graphs) {
+    for (const DecodeLaunch& l : launches) HIP_TRY(run_launch(l, st));
+    return DUET_OK;
+  }
+  std::vector<uint64_t> key;
+  key.reserve(launches.size() * 40);
+  for (const DecodeLaunch& l : launches) append_key(&key, l);
+  const uint64_t h = hash_key(key);
+  auto it = ctx->graphs.find(h);
+  if (it == ctx->graphs.end() || it->second.key != key) {
+    if (!ctx->capture) HIP_TRY(hipStreamCreateWithFlags(&ctx->capture, hipStreamNonBlocking));
+    HIP_TRY(hipStreamBeginCapture(ctx->capture, hipStreamCaptureModeThreadLocal));
+    hipError_t e = hipSuccess;
+    for (const DecodeLaunch& l : launches)
+      if ((e = run_launch(l, ctx->capture)) != hipSuccess) break;
+    hipGraph_t g = nullptr;
+    const hipError_t e_end = hipStreamEndCapture(ctx->capture, &g);
+    if (e != hipSuccess || e_end != hipSuccess) {
+      if (g) (void)hipGraphDestroy(g);
+      return fail(DUET_EHIP, "capturing a decode step: %s",
+                  hipGetErrorString(e != hipSuccess ? e : e_end));
+    }
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) return fail(DUET_EHIP, "instantiating a decode step graph: %s", hipGetErrorString(e));
+    if (it != ctx->graphs.end() || ctx->graphs.size() >= kMaxGraphs) {
+      // A replaced or evicted graph may still be running: wait for the device first.
+      HIP_TRY(hipDeviceSynchronize());
+      auto victim = it;
+      if (victim == ctx->graphs.end()) {  // evict the least recently used graph
+        victim = ctx->graphs.begin();
+        for (auto u = ctx->graphs.begin(); u != ctx->graphs.end(); ++u)
+          if (u->second.last_use < victim->second.last_use) victim = u;
+      }
+      (void)hipGraphExecDestroy(victim->second.exec);
+      ctx->graphs.erase(victim);
+    }
+    GraphEntry& g_new = ctx->graphs[h];
+    g_new.key = std::move(key);
+    g_new.exec = ex;
+    it = ctx->graphs.find(h);
+    ++ctx->graphs_captured;
+  } else {
+    ++ctx->graphs_replayed;
+  }
+  it->second.last_use = ++ctx->graph_clock;
+  HIP_TRY(hipGraphLaunch(it->second.exec, st));
+  return DUET_OK;
+}
+
+// Look-ahead decode (Section 4.3): the prefill half once over all layers and the decode half for
+// k = split.k_decode_steps steps, step s >= 1 writing its token before attending.  SPLIT and
+// CONCURRENT enqueue every decode step first (one graph per step) on the decode stream, then the
+// prefill kernels one by one on the prefill stream; AGG runs decode step 0, the prefill layers
+// and decode steps 1 .. k - 1 in that order on the caller's stream.
+int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_l, const void* const* q_ahead,
+                   const void* const* k_ahead, const void* const* v_ahead, void* const* kc_l, void* const* vc_l,
+                   int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
+                   const duet_batch* batch, duet_cu_split split, void* workspace, size_t workspace_bytes,
+                   void* const* out_l, void* const* out_ahead, void* stream) {
+  if (!shape) return fail(DUET_EINVAL, "shape is NULL");
+  if (!q_l || !kc_l || !vc_l || !out_l) return fail(DUET_EINVAL, "per-layer pointer array is NULL");
+  const int layers = shape->num_layers;
+  const int k = split.k_decode_steps;
+  if (k < 1 || k > kMaxLookahead) return fail(DUET_EINVAL, "k_decode_steps %d not in [1, %d]", k, kMaxLookahead);
+  if (layers < 1 || layers > kMaxLayers) return fail(DUET_EINVAL, "num_layers %d not in [1, %d]", layers, kMaxLayers);
+  const std::vector<const void*> kcc(kc_l, kc_l + layers), vcc(vc_l, vc_l + layers);
+  int rc = check_call(ctx, shape, layers, q_l, kcc.data(), vcc.data(), num_phys_pages, page_table, max_pages_per_req,
+                      batch, split, workspace, out_l, k - 1);
+  if (rc) return rc;
+  if ((int64_t)layers * k > 16384) return fail(DUET_EINVAL, "num_layers x k_decode_steps above 16384");
+  int n_dec = 0;
+  for (int r = 0; r < batch->num_reqs; ++r) n_dec += batch->reqs[r].kind == DUET_KIND_DECODE;
+  if (k > 1 && n_dec > 0) {
+    if (!q_ahead || !k_ahead || !v_ahead || !out_ahead)
+      return fail(DUET_EINVAL, "look-ahead pointer array is NULL");
+    for (int x = 0; x < (k - 1) * layers; ++x) {
+      if ((rc = check_device_ptr(q_ahead[x], "q_ahead")) || (rc = check_device_ptr(k_ahead[x], "k_ahead")) ||
+          (rc = check_device_ptr(v_ahead[x], "v_ahead")) || (rc = check_device_ptr(out_ahead[x], "out_ahead")))
+        return rc;
+      const int l = x % layers;
+      if (out_ahead[x] == q_ahead[x] || out_ahead[x] == k_ahead[x] || out_ahead[x] == v_ahead[x] ||
+          out_ahead[x] == kc_l[l] || out_ahead[x] == vc_l[l])
+        return fail(DUET_EINVAL, "look-ahead output %d aliases an input", x);
+    }
+  }
+
+  std::lock_guard<std::mutex> lock(ctx->mu);
+  Plan& p = ctx->plan;
+  plan_batch(shape, batch, layers, k, &p, true);
+  if (workspace_bytes < p.total)
+    return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, p.total);
+
+  hipStream_t order = static_cast<hipStream_t>(stream);
+  hipStream_t sd = order, sp = order;
+  HIP_TRY(hipSetDevice(ctx->device));
+  if (split.mode == DUET_SPLIT) {
+    if ((rc = get_stream(ctx, split.cus_decode, 0, &sd))) return rc;
+    if ((rc = get_stream(ctx, split.cus_prefill, 1, &sp))) return rc;
+  } else if (split.mode == DUET_CONCURRENT) {
+    if ((rc = get_stream(ctx, ctx->num_cus, 0, &sd))) return rc;
+    if ((rc = get_stream(ctx, ctx->num_cus, 1, &sp))) return rc;
+  }
+  const bool forked = split.mode != DUET_AGG;
+  char* ws = static_cast<char*>(workspace);
+  AttnArgs a;
+  WorkArgs w;
+  base_args(ctx, shape, p, ws, split, page_table, num_phys_pages, max_pages_per_req, &a, &w);
+  const bool prof_iter = ctx->profiling >= 1;
+  const bool prof = ctx->profiling >= 2;
+  const bool has_decode = n_dec > 0, has_prefill = w.n_pitems > 0;
+  if (prof_iter && ((rc = ensure_step_events(ctx, k)) || (rc = ensure_layer_events(ctx, layers)))) return rc;
+
+  if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
+  if ((rc = stage_upload(ctx, p, ws, order))) return rc;
+  if (forked) {
+    HIP_TRY(hipEventRecord(ctx->ev_fork, order));
+    if (has_decode) HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
+    if (has_prefill) HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
+  }
+  int32_t* counters = reinterpret_cast<int32_t*>(ws + kCounterOffset);
+  std::vector<DecodeLaunch> launches;
+  auto decode_step = [&](int st) -> int {
+    launches.clear();
+    WorkArgs ws_w = w;
+    if (st > 0) {
+      const StepPlan& spl = p.ahead[st - 1];
+      ws_w.meta = reinterpret_cast<const int4*>(ws + spl.off_meta);
+      ws_w.dreq = reinterpret_cast<const int4*>(ws + spl.off_dreq);
+      ws_w.ditems = reinterpret_cast<const int32_t*>(ws + spl.off_ditems);
+      ws_w.n_dreq = (int)spl.dreq.size();
+      ws_w.n_ditems = (int)spl.ditems.size();
+      ws_w.max_split = spl.max_split;
+    }
+    for (int l = 0; l < layers; ++l) {
+      const int x = (st - 1) * layers + l;
+      DecodeLaunch dl;
+      dl.a = a;
+      dl.a.q = st == 0 ? q_l[l] : q_ahead[x];
+      dl.a.k_cache = kc_l[l];
+      dl.a.v_cache = vc_l[l];
+      dl.a.out = st == 0 ? out_l[l] : out_ahead[x];
+      dl.w = ws_w;
+      dl.w.work_counter = counters + (size_t)st * layers + l;
+      dl.ap = AppendArgs{};
+      if (st > 0) {
+        dl.ap.k_cache = kc_l[l];
+        dl.ap.v_cache = vc_l[l];
+        dl.ap.k_new = k_ahead[x];
+        dl.ap.v_new = v_ahead[x];
+        dl.ap.page_table = page_table;
+        dl.ap.num_phys_pages = num_phys_pages;
+        dl.ap.max_pages = max_pages_per_req;
+        dl.ap.h_kv = shape->num_kv_heads;
+        dl.ap.head_dim = shape->head_dim;
+        dl.ap.dtype = shape->dtype;
+        dl.kind = DecodeLaunch::kAppend;
+        launches.push_back(dl);
+      }
+      dl.kind = DecodeLaunch::kPartial;
+      launches.push_back(dl);
+      dl.kind = DecodeLaunch::kReduce;
+      launches.push_back(dl);
+    }
+    hipStream_t ds = forked ? sd : order;
+    int r2 = run_decode_step(ctx, launches, ds);
+    if (r2) return r2;
+    if (prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[st + 1], ds));
+    return DUET_OK;
+  };
+  auto prefill_layers = [&]() -> int {
+    for (int l = 0; l < layers; ++l) {
+      AttnArgs al = a;
+      al.q = q_l[l];
+      al.k_cache = kc_l[l];
+      al.v_cache = vc_l[l];
+      al.out = out_l[l];
+      if (prof_iter && (prof || l == 0)) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l], sp));
+      HIP_TRY(launch_prefill(al, w, sp));
+      if (prof_iter && (prof || l == layers - 1)) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l + 1], sp));
+    }
+    return DUET_OK;
+  };
+  if (has_decode && prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[0], forked ? sd : order));
+  if (forked) {
+    // decode first: all k steps are enqueued before any prefill kernel
+    for (int st = 0; has_decode && st < k; ++st)
+      if ((rc = decode_step(st))) return rc;
+    if (has_prefill && (rc = prefill_layers())) return rc;
+  } else {
+    if (has_decode && (rc = decode_step(0))) return rc;
+    if (has_prefill && (rc = prefill_layers())) return rc;
+    for (int st = 1; has_decode && st < k; ++st)
+      if ((rc = decode_step(st))) return rc;
+  }
+  if (forked) {
+    HIP_TRY(hipEventRecord(ctx->ev_djoin, sd));
+    HIP_TRY(hipEventRecord(ctx->ev_pjoin, sp));
+    HIP_TRY(hipStreamWaitEvent(order, ctx->ev_djoin, 0));
+    HIP_TRY(hipStreamWaitEvent(order, ctx->ev_pjoin, 0));
+  }
+  if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
+  ctx->prof_valid = prof_iter;
+  ctx->prof_kernels = prof;
+  ctx->prof_decode = has_decode;
+  ctx->prof_prefill = has_prefill;
+  ctx->prof_layers = layers;
+  ctx->prof_steps = k;
+  return DUET_OK;
+}
+
 
 }  // namespace
 
@@ -488,6 +874,10 @@ int duet_destroy(duet_ctx* ctx) {
     if (e) (void)hipEventDestroy(e);
   for (auto& e : ctx->ev_dec) (void)hipEventDestroy(e);
   for (auto& e : ctx->ev_pre) (void)hipEventDestroy(e);
+  for (auto& e : ctx->ev_step) (void)hipEventDestroy(e);
+  if (!ctx->graphs.empty()) (void)hipDeviceSynchronize();
+  clear_graphs(ctx);
+  if (ctx->capture) (void)hipStreamDestroy(ctx->capture);
   if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
   if (ctx->ev_djoin) (void)hipEventDestroy(ctx->ev_djoin);
   if (ctx->ev_pjoin) (void)hipEventDestroy(ctx->ev_pjoin);
@@ -505,7 +895,7 @@ int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_
   if ((rc = check_batch(shape, batch, false))) return rc;
   if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
   Plan p;
-  plan_batch(shape, batch, shape->num_layers, &p, false);
+  plan_batch(shape, batch, shape->num_layers, 1, &p, false);
   *bytes = p.total;
   return DUET_OK;
 }
@@ -528,6 +918,49 @@ int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* cons
   if (!q || !k_cache || !v_cache || !out) return fail(DUET_EINVAL, "per-layer pointer array is NULL");
   return attn_layers(ctx, shape, shape->num_layers, q, k_cache, v_cache, num_phys_pages, page_table,
                      max_pages_per_req, batch, split, workspace, workspace_bytes, out, stream);
+}
+
+int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* batch, int32_t k_decode_steps,
+                                   size_t* bytes) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
+  if (k_decode_steps < 1 || k_decode_steps > kMaxLookahead)
+    return fail(DUET_EINVAL, "k_decode_steps %d not in [1, %d]", k_decode_steps, kMaxLookahead);
+  Plan p;
+  plan_batch(shape, batch, shape->num_layers, k_decode_steps, &p, false);
+  *bytes = p.total;
+  return DUET_OK;
+}
+
+int duet_attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q, const void* const* q_ahead,
+                        const void* const* k_ahead, const void* const* v_ahead, void* const* k_cache,
+                        void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                        size_t workspace_bytes, void* const* out, void* const* out_ahead, void* stream) {
+  clear_error();
+  return attn_lookahead(ctx, shape, q, q_ahead, k_ahead, v_ahead, k_cache, v_cache, num_phys_pages, page_table,
+                        max_pages_per_req, batch, split, workspace, workspace_bytes, out, out_ahead, stream);
+}
+
+int duet_set_decode_graphs(duet_ctx* ctx, int32_t enable) {
+  clear_error();
+  if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
+  std::lock_guard<std::mutex> lock(ctx->mu);
+  ctx->decode_graphs = enable != 0;
+  return DUET_OK;
+}
+
+int duet_decode_graph_stats(duet_ctx* ctx, int64_t* cached, int64_t* captured, int64_t* replayed) {
+  clear_error();
+  if (!ctx || !cached || !captured || !replayed) return fail(DUET_EINVAL, "NULL argument");
+  std::lock_guard<std::mutex> lock(ctx->mu);
+  *cached = (int64_t)ctx->graphs.size();
+  *captured = (int64_t)ctx->graphs_captured;
+  *replayed = (int64_t)ctx->graphs_replayed;
+  return DUET_OK;
 }
 
 int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream) {
@@ -594,6 +1027,31 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
   const int L = ctx->prof_layers;
   out->layers = L;
   int rc;
+  if (ctx->prof_steps > 0) {
+    // look-ahead call: decode steps are graphs, timed step by step on the decode stream
+    const int k = ctx->prof_steps;
+    out->decode_steps = k;
+    if (ctx->prof_decode) {
+      const std::vector<hipEvent_t>& e = ctx->ev_step;
+      if ((rc = span_us(e[0], e[k], &out->decode_total_us)) ||
+          (rc = span_us(ctx->prof[kEvFork], e[0], &out->decode_start_us)) ||
+          (rc = span_us(e[0], e[1], &out->decode_first_step_us)))
+        return rc;
+      out->decode_step_us = out->decode_total_us / k;
+    }
+    if (ctx->prof_prefill) {
+      const std::vector<hipEvent_t>& e = ctx->ev_pre;
+      if ((rc = span_us(e[0], e[2 * L - 1], &out->prefill_total_us)) ||
+          (rc = span_us(ctx->prof[kEvFork], e[0], &out->prefill_start_us)))
+        return rc;
+      for (int l = 0; ctx->prof_kernels && l < L; ++l) {
+        double t = 0.0;
+        if ((rc = span_us(e[2 * l], e[2 * l + 1], &t))) return rc;
+        out->prefill_us += t / L;
+      }
+    }
+    return span_us(ctx->prof[kEvFork], ctx->prof[kEvJoin], &out->iteration_us);
+  }
   if (ctx->prof_kernels && ctx->prof_decode) {
     const std::vector<hipEvent_t>& e = ctx->ev_dec;
     for (int l = 0; l < L; ++l) {

@@ -107,20 +107,26 @@ def _assign_pages(n_pages_per_req, num_phys_pages, rng) -> np.ndarray:
 
 
 def make_batch(shape: AttnShape, reqs, *, page_seed: int, num_phys_pages: int | None = None,
-               pool_slack: float = 0.10, name: str = "") -> Batch:
-    """reqs: list of (kind, q_len, cached_len).  Pages are placed by a seeded permutation."""
+               pool_slack: float = 0.10, name: str = "", reserve_tokens: int = 0) -> Batch:
+    """reqs: list of (kind, q_len, cached_len).  Pages are placed by a seeded permutation.
+    reserve_tokens: decode requests also get pages for that many future tokens (the KV slots of
+    look-ahead decode steps); those slots start out NaN."""
     kinds = np.array([k for k, _, _ in reqs], dtype=np.int32)
     q_lens = np.array([q for _, q, _ in reqs], dtype=np.int32)
     cached = np.array([c for _, _, c in reqs], dtype=np.int32)
     if np.any(q_lens < 1) or np.any(cached < 0):
         raise ValueError("q_len >= 1 and cached_len >= 0 required")
     ps = shape.page_size
-    n_pages = [-(-int(c + q) // ps) for q, c in zip(q_lens, cached)]
+    if reserve_tokens < 0:
+        raise ValueError("reserve_tokens >= 0 required")
+    n_pages = [-(-int(c + q + (reserve_tokens if k == KIND_DECODE else 0)) // ps)
+               for k, q, c in zip(kinds, q_lens, cached)]
     if num_phys_pages is None:
         num_phys_pages = int(math.ceil(sum(n_pages) * (1.0 + pool_slack))) + 1
     rng = np.random.Generator(np.random.PCG64(page_seed))
     table = _assign_pages(n_pages, num_phys_pages, rng)
-    return Batch(shape, kinds, q_lens, cached, table, int(num_phys_pages), name=name)
+    return Batch(shape, kinds, q_lens, cached, table, int(num_phys_pages), name=name,
+                 meta={"reserve_tokens": int(reserve_tokens)} if reserve_tokens else {})
 
 
 # ----------------------------------------------------------------------------------------------
@@ -220,6 +226,27 @@ def make_tensors(batch: Batch, seed: int, *, device="cpu", scale: float | None =
                 vals = vals.transpose(2, 3).contiguous()
             cache[used[lo:hi]] = vals
     return q, k_cache, v_cache
+
+
+def make_lookahead_tensors(batch: Batch, k: int, seed: int, *, device="cpu", scale: float | None = None):
+    """Inputs of look-ahead decode steps 1 .. k - 1 for one layer: lists (one tensor per step) of
+    queries [R_d, h_q, d] and new key / value rows [R_d, h_kv, d], decode requests in batch order,
+    drawn in that order (per step: q, then k, then v) with a torch generator on `device`."""
+    import torch
+
+    sh = batch.shape
+    tdt = torch.bfloat16 if sh.dtype == "bf16" else torch.float32
+    scale = value_scale(sh) if scale is None else scale
+    dev = torch.device(device)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(int(seed))
+    n_dec = int((batch.kinds == KIND_DECODE).sum())
+    qa, ka, va = [], [], []
+    for _ in range(k - 1):
+        qa.append((torch.randn(n_dec, sh.num_q_heads, sh.head_dim, generator=gen, device=dev) * scale).to(tdt))
+        ka.append((torch.randn(n_dec, sh.num_kv_heads, sh.head_dim, generator=gen, device=dev) * scale).to(tdt))
+        va.append((torch.randn(n_dec, sh.num_kv_heads, sh.head_dim, generator=gen, device=dev) * scale).to(tdt))
+    return qa, ka, va
 
 
 # ----------------------------------------------------------------------------------------------

@@ -106,3 +106,30 @@ def test_model_rejects_concurrent_control_mode(native):
     us = ctypes.c_double()
     assert native.duet_predict_iter_latency(None, ctypes.byref(_shape()), ctypes.byref(b), N.CuSplit(N.CONCURRENT, 256, 256, 1),
                                             ctypes.byref(us)) == -1
+
+
+def test_lookahead_workspace_and_step_validation(native):
+    arr, b = _batch([(0, 0, 100, 20), (1, 100, 1, 500), (1, 101, 1, 31)])
+    one, four = ctypes.c_size_t(), ctypes.c_size_t()
+    plain = ctypes.c_size_t()
+    sh = ctypes.byref(_shape(num_layers=3))
+    assert native.duet_workspace_bytes(sh, ctypes.byref(b), ctypes.byref(plain)) == 0
+    assert native.duet_lookahead_workspace_bytes(sh, ctypes.byref(b), 1, ctypes.byref(one)) == 0
+    assert native.duet_lookahead_workspace_bytes(sh, ctypes.byref(b), 4, ctypes.byref(four)) == 0
+    assert one.value == plain.value
+    # three more steps: 3 x 3 more counters, three more copies of the metadata and work lists
+    assert four.value >= one.value + 3 * 3 * 16
+    for k in (0, 65):
+        assert native.duet_lookahead_workspace_bytes(sh, ctypes.byref(b), k, ctypes.byref(four)) == -1
+
+
+def test_lookahead_rejects_null_context_and_bad_steps(native):
+    arr, b = _batch([(1, 0, 1, 10)])
+    ptrs = (ctypes.c_void_p * 1)(1)
+    rc = native.duet_attn_lookahead(None, ctypes.byref(_shape()), ptrs, ptrs, ptrs, ptrs, ptrs, ptrs, 10, 1, 4,
+                                    ctypes.byref(b), N.CuSplit(0, 256, 0, 2), 1, 1 << 20, ptrs, ptrs, None)
+    assert rc == -1 and b"ctx" in native.duet_last_error()
+    rc = native.duet_attn_lookahead(None, ctypes.byref(_shape()), ptrs, ptrs, ptrs, ptrs, ptrs, ptrs, 10, 1, 4,
+                                    ctypes.byref(b), N.CuSplit(0, 256, 0, 0), 1, 1 << 20, ptrs, ptrs, None)
+    assert rc == -1
+    assert native.duet_set_decode_graphs(None, 1) == -1
