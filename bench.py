@@ -255,6 +255,127 @@ def trace_main(args):
     ctx.close()
 
 
+
+def lookahead_main(args):
+    """Look-ahead decode (Section 4.3) on the prefill-heavy Llama-3-70B batch: Algorithm 1, capped at
+    --max-k decode steps, picks (S_p, S_d, k) under the TBT bound (default: a fifth of the model's
+    aggregated iteration); one step is then one duet_attn_lookahead call -- the prefill chunk once
+    and k decode steps of the 32 decodes, each decode step writing its token into a preallocated
+    KV slot and replayed from a graph on the decode CUs.  Compared with the same work on one
+    stream (AGG with k decode steps: decode step 0, the prefill, decode steps 1 .. k - 1) and with
+    the plain aggregated iteration (one prefill step and one decode step)."""
+    import dataclasses
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from paper_2511_04791_amd.calibration import calibrate_model
+
+    L = args.layers if args.layers is not None else 1
+    cap = args.max_k
+    batch = wl.prefill_heavy_70b(reserve_tokens=cap)
+    ctx = duet.Context(0)
+    calib_s = None
+    if not args.no_calibrate:
+        t0 = time.perf_counter()
+        calibrate_model(ctx, shape=batch.shape)
+        calib_s = round(time.perf_counter() - t0, 1)
+    shape = dataclasses.replace(batch.shape, num_layers=L)
+    rows3 = [(int(k), int(q), int(c)) for k, q, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
+    agg_pred = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), shape, ctx.model)
+    tau = args.tbt_slo_us if args.tbt_slo_us is not None else 0.2 * agg_pred
+    sp, pred, rho, flags = duet.choose_cu_split(rows3, tau, shape, ctx.model, max_decode_steps=cap)
+    if sp.mode != duet.SPLIT:
+        print(json.dumps({"error": "Algorithm 1 kept aggregated execution", "tau_us": tau, "flags": flags}))
+        sys.exit(1)
+    k = sp.k_decode_steps
+    n_dec = int((batch.kinds == 1).sum())
+    q_pre = int(batch.q_lens[batch.kinds == 0].sum())
+
+    layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
+    qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
+    la = [wl.make_lookahead_tensors(batch, cap, seed=3003 + l, device="cuda") for l in range(L)]
+    pt = torch.as_tensor(batch.page_table, device="cuda")
+    meta = batch.seq_meta
+    outs = [torch.empty_like(q) for q in qs]
+
+    def arrays(kk):
+        qa = [la[l][0][s - 1] for s in range(1, kk) for l in range(L)]
+        ka = [la[l][1][s - 1] for s in range(1, kk) for l in range(L)]
+        va = [la[l][2][s - 1] for s in range(1, kk) for l in range(L)]
+        return qa, ka, va, [torch.empty_like(x) for x in qa]
+
+    def measure(split):
+        kk = split.k_decode_steps
+        qa, ka, va, oa = arrays(kk)
+        ws = ctx.workspace(duet.lookahead_workspace_bytes(shape, meta, kk))
+
+        def call():
+            ctx.attn_lookahead(qs, qa, ka, va, kcs, vcs, pt, meta, split, outs=outs, outs_ahead=oa, workspace=ws)
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            call()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) / args.steps * 1e6
+        ctx.set_profiling(1)
+        rec = []
+        for i in range(6):
+            call()
+            kt = ctx.last_kernel_times()
+            if i:
+                rec.append(kt)
+        ctx.set_profiling(0)
+        host = {}
+        for graphs in (True, False):
+            ctx.set_decode_graphs(graphs)
+            call()
+            ts = []
+            for _ in range(5):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                call()
+                ts.append((time.perf_counter() - t0) * 1e6)
+            host["graphs" if graphs else "direct"] = round(statistics.median(ts), 1)
+        ctx.set_decode_graphs(True)
+        torch.cuda.synchronize()
+        m = {key: statistics.fmean(r[key] for r in rec) for key in rec[0]}
+        it = m["iteration_us"]
+        res = {"split": str(split), "k": kk, "wall_us_per_call": round(wall, 1), "iteration_us": round(it, 1),
+               "decode_step_us": round(m["decode_step_us"], 1),
+               "decode_first_step_us": round(m["decode_first_step_us"], 1),
+               "decode_ready_first_us": round(m["decode_start_us"] + m["decode_first_step_us"], 1),
+               "prefill_total_us": round(m["prefill_total_us"], 1),
+               "decode_tokens_per_s": round(n_dec * kk / (wall * 1e-6), 1),
+               "prefill_tokens_per_s": round(q_pre / (wall * 1e-6), 1),
+               "host_submit_us": host}
+        if split.mode == duet.AGG:
+            # decode step 1 waits for the whole prefill: its interval is the prefill plus one step
+            res["decode_interval_max_us"] = round(m["prefill_total_us"] + m["decode_first_step_us"], 1) \
+                if kk > 1 else round(it, 1)
+        else:
+            res["decode_interval_max_us"] = round(m["decode_step_us"], 1)
+        return res
+
+    split_res = measure(sp)
+    agg_k = measure(duet.CuSplit.agg(k))
+    agg_1 = measure(duet.CuSplit.agg(1))
+    line = {"metric": "look-ahead decode: decode tokens/s at one prefill step per k decode steps",
+            "value": split_res["decode_tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True,
+            "steps": args.steps, "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": WORKLOADS["prefill-heavy-70b"].format(L=L) + "; look-ahead slots for "
+                                   f"{cap} tokens per decode", "tau_us": round(tau, 1), "max_k": cap},
+            "chosen": {"S_p": sp.cus_prefill, "S_d": sp.cus_decode, "k": k, "predicted_us": round(pred, 1),
+                       "rho": rho, "agg_predicted_us": round(agg_pred, 1)},
+            "lookahead_split": split_res, "agg_same_work": agg_k, "agg_one_step": agg_1,
+            "decode_tokens_per_s_vs_agg_one_step": round(split_res["decode_tokens_per_s"] /
+                                                         agg_1["decode_tokens_per_s"], 3),
+            "wall_vs_agg_same_work": round(agg_k["wall_us_per_call"] / split_res["wall_us_per_call"], 3),
+            "graphs": ctx.decode_graph_stats(), "calibration_seconds": calib_s}
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +401,10 @@ def main():
     ap.add_argument("--trace", action="store_true",
                     help="run the serving-trace configuration instead (adaptive vs always-aggregated)")
     ap.add_argument("--trace-iters", type=int, default=200)
+    ap.add_argument("--lookahead", action="store_true",
+                    help="run look-ahead decode (k decode steps per prefill step) on the prefill-heavy Llama-3-70B "
+                         "batch instead")
+    ap.add_argument("--max-k", type=int, default=64, help="cap on Algorithm 1's k for --lookahead")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path; "
@@ -297,6 +422,9 @@ def main():
         sys.exit(1)
     if args.trace:
         trace_main(args)
+        return
+    if args.lookahead:
+        lookahead_main(args)
         return
     L = args.layers if args.layers is not None else (32 if args.workload == "llama8b-mixed" else 1)
     if args.workload == "decode-heavy" and L != 1:

@@ -275,7 +275,9 @@ int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* ba
  * SPLIT / CONCURRENT: every decode step is enqueued (decode first) on the decode stream, then the
  * prefill layers on the prefill stream; one fork and one join on `stream`.  AGG: decode step 0,
  * then the prefill layers, then decode steps 1 .. k - 1, on `stream`.
- * Decode steps run from graphs by default: a step's kernels are captured on first use and the
+ * Decode steps run from graphs by default: the kernels of the steps that run back to back (all k
+ * steps with SPLIT / CONCURRENT; step 0, then steps 1 .. k - 1, with AGG; one step per graph
+ * while profiling is on, so events can mark each step's end) are captured on first use, and the
  * graph is replayed on later calls whose launch arguments (pointers, work-list sizes, CU share)
  * are the same; at most 128 graphs are kept per context (least recently used evicted, after a
  * device synchronisation).  Outputs and cache writes are bit-identical with graphs on or off,
@@ -291,7 +293,7 @@ int duet_attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* cons
  * kernel at a time (enable == 0). */
 int duet_set_decode_graphs(duet_ctx* ctx, int32_t enable);
 
-/* Graphs held by the context, and how many decode steps were captured / replayed so far. */
+/* Graphs held by the context, and how many decode-step graphs were captured / replayed so far. */
 int duet_decode_graph_stats(duet_ctx* ctx, int64_t* cached, int64_t* captured, int64_t* replayed);
 
 /* Synchronises `stream`, reads the workspace's error word and clears it: DUET_OK or DUET_EPAGE. */

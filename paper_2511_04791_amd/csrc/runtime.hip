@@ -260,15 +260,14 @@ void append_key(std::vector<uint64_t>* k, const DecodeLaunch& l) {
   k->insert(k->end(), std::begin(f), std::end(f));
 }
 
+// Word-wise multiply-xor hash (a lookup index only: a hit is confirmed by comparing the keys).
 uint64_t hash_key(const std::vector<uint64_t>& k) {
-  uint64_t h = 1469598103934665603ull;  // FNV-1a over the key words
+  uint64_t h = 0x9e3779b97f4a7c15ull ^ k.size();
   for (uint64_t x : k) {
-    for (int b = 0; b < 8; ++b) {
-      h ^= (x >> (8 * b)) & 0xff;
-      h *= 1099511628211ull;
-    }
+    h ^= x + 0x9e3779b97f4a7c15ull + (h << 6) + (h >> 2);
+    h *= 0xff51afd7ed558ccdull;
   }
-  return h;
+  return h ^ (h >> 33);
 }
 
 struct GraphEntry {
@@ -594,7 +593,7 @@ void clear_graphs(duet_ctx* ctx) {
   ctx->graphs.clear();
 }
 
-// Enqueues one decode step on `st`: from its cached graph when one with the same launch
+// Enqueues a run of decode launches on `st`: from its cached graph when one with the same launch
 // arguments exists, else captured now (on the private capture stream, so `st` keeps its
 // pending work and its CU mask governs the replay), or launched directly when graphs are off.
 int run_decode_step(duet_ctx* ctx, const std::vector<DecodeLaunch>& launches, hipStream_t st) {
@@ -721,8 +720,8 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
   }
   int32_t* counters = reinterpret_cast<int32_t*>(ws + kCounterOffset);
   std::vector<DecodeLaunch> launches;
-  auto decode_step = [&](int st) -> int {
-    launches.clear();
+  // Appends decode step st's launches (every layer) to `launches`.
+  auto add_step = [&](int st) {
     WorkArgs ws_w = w;
     if (st > 0) {
       const StepPlan& spl = p.ahead[st - 1];
@@ -763,10 +762,21 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
       dl.kind = DecodeLaunch::kReduce;
       launches.push_back(dl);
     }
+  };
+  // Enqueues decode steps first .. last - 1 on the decode stream.  Unprofiled, they form one
+  // graph (one launch for the whole run of steps); profiled, each step is its own graph, so an
+  // event can mark its end.
+  auto decode_steps = [&](int first, int last) -> int {
     hipStream_t ds = forked ? sd : order;
-    int r2 = run_decode_step(ctx, launches, ds);
-    if (r2) return r2;
-    if (prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[st + 1], ds));
+    for (int st = first; st < last;) {
+      const int end = prof_iter ? st + 1 : last;
+      launches.clear();
+      for (int x = st; x < end; ++x) add_step(x);
+      int r2 = run_decode_step(ctx, launches, ds);
+      if (r2) return r2;
+      if (prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[end], ds));
+      st = end;
+    }
     return DUET_OK;
   };
   auto prefill_layers = [&]() -> int {
@@ -785,14 +795,12 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
   if (has_decode && prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[0], forked ? sd : order));
   if (forked) {
     // decode first: all k steps are enqueued before any prefill kernel
-    for (int st = 0; has_decode && st < k; ++st)
-      if ((rc = decode_step(st))) return rc;
+    if (has_decode && (rc = decode_steps(0, k))) return rc;
     if (has_prefill && (rc = prefill_layers())) return rc;
   } else {
-    if (has_decode && (rc = decode_step(0))) return rc;
+    if (has_decode && (rc = decode_steps(0, 1))) return rc;
     if (has_prefill && (rc = prefill_layers())) return rc;
-    for (int st = 1; has_decode && st < k; ++st)
-      if ((rc = decode_step(st))) return rc;
+    if (has_decode && k > 1 && (rc = decode_steps(1, k))) return rc;
   }
   if (forked) {
     HIP_TRY(hipEventRecord(ctx->ev_djoin, sd));

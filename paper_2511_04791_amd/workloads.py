@@ -142,13 +142,13 @@ def tiny_mixed(seed: int = 1001, page_seed: int | None = None) -> Batch:
 
 
 def llama8b_mixed(seed: int = 1002, page_seed: int | None = None, num_decodes: int = 64,
-                  prefill_len: int = 2048) -> Batch:
+                  prefill_len: int = 2048, reserve_tokens: int = 0) -> Batch:
     """Llama-3-8B shapes: a 2048-token prefill at prefix 0 plus 64 decodes, context U{512..4096}."""
     rng = np.random.Generator(np.random.PCG64(seed))
     ctx = rng.integers(512, 4096, size=num_decodes, endpoint=True)
     reqs = [(KIND_PREFILL, prefill_len, 0)] + [(KIND_DECODE, 1, int(c) - 1) for c in ctx]
     return make_batch(LLAMA3_8B, reqs, page_seed=seed + 7 if page_seed is None else page_seed,
-                      name="llama3-8b-mixed-2048p-64d")
+                      name="llama3-8b-mixed-2048p-64d", reserve_tokens=reserve_tokens)
 
 
 def decode_heavy(seed: int = 1003, page_seed: int | None = None, num_decodes: int = 256,
@@ -165,11 +165,12 @@ def decode_heavy(seed: int = 1003, page_seed: int | None = None, num_decodes: in
                       num_phys_pages=pool, name="llama3-8b-decode-heavy-256d")
 
 
-def prefill_heavy_70b(seed: int = 1004, page_seed: int | None = None) -> Batch:
-    """Llama-3-70B shapes: an 8192-token chunk after a 24576-token prefix plus 32 decodes at 2048."""
+def prefill_heavy_70b(seed: int = 1004, page_seed: int | None = None, reserve_tokens: int = 0) -> Batch:
+    """Llama-3-70B shapes: an 8192-token chunk after a 24576-token prefix plus 32 decodes at 2048.
+    reserve_tokens: KV slots of that many future decode tokens per decode request (look-ahead)."""
     reqs = [(KIND_PREFILL, 8192, 24576)] + [(KIND_DECODE, 1, 2047)] * 32
     return make_batch(LLAMA3_70B, reqs, page_seed=seed + 7 if page_seed is None else page_seed,
-                      name="llama3-70b-prefill-heavy")
+                      name="llama3-70b-prefill-heavy", reserve_tokens=reserve_tokens)
 
 
 WORKLOADS = {1: tiny_mixed, 2: llama8b_mixed, 3: decode_heavy, 4: prefill_heavy_70b}
