@@ -12,8 +12,8 @@
 //   O^T [16 dims x 16 heads]  += V^T   [16 x 16] . P^T [16 x 16]  (16x16x16, one per 16 dims)
 // Heads beyond the group size are zero columns.  K is read token-major (16 B per lane, the
 // MFMA A layout); V pages are stored dim-major, so a lane's 4 consecutive tokens of one dim
-// are 8 contiguous bytes and P^T never leaves registers.  Pages cycle through three register
-// buffers (the loop is unrolled by three), so two pages are in flight while one is computed.
+// are 8 contiguous bytes and P^T never leaves registers.  Pages cycle through four register
+// buffers, so three pages are in flight while one is computed, across item boundaries too.
 // Online softmax keeps a reference max per head that only moves when a score exceeds it by
 // more than 2^8 (base-2 units), so the output rescale is rare.  Partials (unnormalised output,
 // reference max, denominator) go to the workspace and the reduce kernel merges the splits.
@@ -21,6 +21,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <cmath>
 
 #include "kernels.h"
@@ -32,10 +33,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
 #ifndef DUET_DECODE_RING
-#define DUET_DECODE_RING 3
+#define DUET_DECODE_RING 4
 #endif
 constexpr int kRing = DUET_DECODE_RING;  // page buffers per wave: kRing - 1 pages in flight
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -87,162 +89,225 @@ __device__ __forceinline__ void load_page(Page<D>& pg, const char* kbase, const 
 
 __device__ __forceinline__ bool page_ok(int id, long long num_phys) { return id >= 0 && (long long)id < num_phys; }
 
-// One work item: decode request i (an index into dreq), kv head j, split s.
-template <int D, int PPS>
-__device__ __forceinline__ void decode_item(const AttnArgs& a, const WorkArgs& w, int i, int j, int s, int lane) {
-  const int4 dr = w.dreq[i];    // (req, item_base, n_split, n_pages)
-  const int4 m = w.meta[dr.x];  // (kind, q_start, q_len, cached_len)
-  const int L = m.w + m.z;
-  const int g = a.group;
-  const int col = lane & 15, quad = lane >> 4;
-  const int pb = s * w.pages_per_split;
-  const int pe = min(pb + w.pages_per_split, dr.w);
+// Uniform loads of the read-only work list through the scalar cache: they are counted by
+// lgkmcnt, so waiting for them never waits for the page stream in flight.
+__device__ __forceinline__ i32x4 sload4(const void* p) { return *(const __attribute__((address_space(4))) i32x4*)(p); }
 
-  // Q^T as the B operand: column = head of the group, k = dims 32 ks + 8 quad .. +8.
-  bf16x8 qf[D / 32];
-  {
-    const __bf16* qrow = reinterpret_cast<const __bf16*>(a.q) + ((size_t)m.y * a.h_q + j * g + col) * D + quad * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) {
-      uint4 u = col < g ? *reinterpret_cast<const uint4*>(qrow + ks * 32) : make_uint4(0, 0, 0, 0);
-      qf[ks] = __builtin_bit_cast(bf16x8, u);
-    }
-  }
-
-  const char* kbase = reinterpret_cast<const char*>(a.k_cache) + (size_t)j * 16 * D * 2;
-  const char* vbase = reinterpret_cast<const char*>(a.v_cache) + (size_t)j * 16 * D * 2;
-  // Both caches are [P, h_kv, 16 * d] in bytes per (page, head) slab; fold h_kv into the page stride.
-  const long long slab_stride_pages = a.h_kv;
-  const int* prow = a.page_table + (size_t)dr.x * a.max_pages;
-
-  f32x4 acc[D / 16];
-#pragma unroll
-  for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float l_run = 0.f;
-  int bad = 0;
-
-  // The split's page ids (at most 64) are fetched once, one per lane, and broadcast per page.
-  // An out-of-range id is replaced by page 0 for the load and its tokens are masked.  Loads of
-  // page slots past the split re-read its last page (an L2 hit), so every load is unconditional
-  // and the compiler never has to merge a loaded buffer with a stale one.
-  const int my_id = lane < pe - pb ? prow[pb + lane] : 0;
-  struct Ids {
-    size_t slab;
-    bool ok;
-  };
-  auto page_id = [&](int p) {
-    Ids r;
-    const int id = __builtin_amdgcn_readlane(my_id, min(p, pe - 1) - pb);
-    r.ok = page_ok(id, a.num_phys_pages);
-    bad |= !r.ok;
-    r.slab = (size_t)(r.ok ? id : 0) * slab_stride_pages;
-    return r;
-  };
-
-  float m_ref = -INFINITY;  // reference max (base-2 units) the probabilities are taken against
-  auto compute = [&](const Page<D>& pg, int p, const Ids& ids) {
-    // Scores S^T: lane holds head `col`, tokens 4 quad + i of the page.
-    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pg.k[ks]), qf[ks], sc, 0, 0, 0);
-    const int t0 = 16 * p + 4 * quad;
-    // Tokens past the end (NaN-poisoned slots) and tokens of a bad page are masked; only the
-    // last page of a request or a bad page needs it.
-    const bool tail = 16 * (p + 1) > L || !ids.ok;
-    if (tail) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (!ids.ok || t0 + i >= L) sc[i] = -INFINITY;
-    }
-    float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    mx *= a.scale_log2;  // the scale is positive: max of scaled = scaled max
-    // The reference max moves only when a score exceeds it by more than the slack, so the
-    // output rescale is rare; numerator and denominator share the reference.
-#ifndef DUET_DECODE_EAGER_RESCALE
-    if (__any(mx > m_ref + kRescaleSlack)) {
-#endif
-      const float m_new = fmaxf(m_ref, mx);
-      const float alpha = fast_exp2(m_ref - m_new);
-      m_ref = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int n = 0; n < D / 16; ++n) acc[n] *= alpha;
-#ifndef DUET_DECODE_EAGER_RESCALE
-    }
-#endif
-    bf16x4 pb4;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pb4[i] = static_cast<__bf16>(fast_exp2(__builtin_fmaf(sc[i], a.scale_log2, -m_ref)));
-    // The denominator sums the bf16 probabilities the PV product consumes.
-    const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-    l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[0], pb4[1]}, ones, l_run, false);
-    l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[2], pb4[3]}, ones, l_run, false);
-    const s16x4 pbs = __builtin_bit_cast(s16x4, pb4);
-    // Their values must not reach the MFMA either (0 x NaN is NaN).
-    const uint64_t mk = !ids.ok ? 0ull : (tail ? low_elems_mask(L - t0) : ~0ull);
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) {
-      const uint64_t v = ((uint64_t)pg.v[n].y << 32 | pg.v[n].x) & mk;
-      acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, v), pbs, acc[n], 0, 0, 0);
-    }
-  };
-
-  // kRing page buffers used in turn: the next kRing - 1 pages are in flight while one page is
-  // computed.  The split has at most PPS pages and the loop is fully unrolled, so no buffer is
-  // ever copied and every wait counts exactly the loads still needed.
-  constexpr int R = kRing;
-  Page<D> buf[R];
-  Ids ids[R];
-#pragma unroll
-  for (int k = 0; k < R - 1 && k < PPS; ++k) {
-    ids[k] = page_id(pb + k);
-    load_page<D>(buf[k], kbase, vbase, ids[k].slab, lane);
-  }
-#pragma unroll
-  for (int k = 0; k < PPS; ++k) {
-    if (k + R - 1 < PPS) {
-      ids[(k + R - 1) % R] = page_id(pb + k + R - 1);
-      load_page<D>(buf[(k + R - 1) % R], kbase, vbase, ids[(k + R - 1) % R].slab, lane);
-    }
-    compute(buf[k % R], pb + k, ids[k % R]);
-    if (pb + k + 1 >= pe) break;
-  }
-
-  float l_tot = l_run + __shfl_xor(l_run, 16);
-  l_tot += __shfl_xor(l_tot, 32);
-  if (bad && lane == 0) atomicOr(w.err, 1);
-  const int item = dr.y + j * dr.z + s;
-  if (col < g) {
-    float* pa = w.pacc + ((size_t)item * g + col) * D + 4 * quad;
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) *reinterpret_cast<f32x4*>(pa + 16 * n) = acc[n];
-    if (quad == 0) {
-      w.pml[((size_t)item * g + col) * 2 + 0] = m_ref;
-      w.pml[((size_t)item * g + col) * 2 + 1] = l_tot;
-    }
-  }
+// A decode work item as the host lists it: (q_start, req | kv head << 24, split | kv_len << 10,
+// row of its split-K partial).  pages_in_split, and the item's tokens, are relative to the
+// split's first page.
+struct DItem {
+  int q_start, req, j, split, L, slot;
+  bool valid;
+};
+__device__ __forceinline__ DItem unpack_item(i32x4 v, bool valid) {
+  DItem d;
+  d.q_start = v.x;
+  d.req = v.y & 0xffffff;
+  d.j = (int)((unsigned)v.y >> 24);
+  d.split = v.z & 1023;
+  d.L = (int)((unsigned)v.z >> 10);
+  d.slot = v.w;
+  d.valid = valid;
+  return d;
 }
 
-// Persistent: the grid holds as many waves as fit on the CUs the stream may use, and each wave
-// takes the next item from a counter until the list is exhausted (every wave reaches the exit).
-// Items are listed longest first.  Which wave computes an item never changes its arithmetic.
+// Persistent: the grid holds as many waves as fit on the CUs the stream may use; each wave takes
+// one item by its index, then the next ones from a counter until the list is exhausted (every
+// wave reaches the exit).  Items are listed longest first.  Which wave computes an item never changes its arithmetic.
+//
+// A wave streams pages through a ring of kRing register buffers without a break at item
+// boundaries: while it works on one item it takes the next one from the counter, reads the
+// item's descriptor, then its page ids and query; the next item's first pages are loaded while
+// the current item's last pages are computed.  Each item is processed in groups of kRing pages
+// (the last group padded with masked pages that re-read the item's last page), so a page's
+// buffer is known at compile time and a load is never separated from its use by an early exit.
 #ifndef DUET_DECODE_MIN_BLOCKS_PER_CU
 #define DUET_DECODE_MIN_BLOCKS_PER_CU 1
 #endif
 template <int D, int PPS>
 __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
+  constexpr int R = kRing;
+  static_assert(PPS % R == 0, "a split must hold whole groups of ring pages");
+  constexpr size_t kSlabBytes = 16 * D * 2;  // one (page, kv head) slab of K or V
   const int lane = threadIdx.x & 63;
-  for (;;) {
+  const int col = lane & 15, quad = lane >> 4;
+  const int g = a.group;
+  const int n_items = w.n_ditems;
+  const char* kcache = reinterpret_cast<const char*>(a.k_cache);
+  const char* vcache = reinterpret_cast<const char*>(a.v_cache);
+  // Both caches are [P, h_kv, 16 * d] in bytes per (page, head) slab; fold h_kv into the page stride.
+  const long long slab_stride_pages = a.h_kv;
+
+  // Wave v of the grid starts with item v; later items come from the counter, past the first
+  // ones, so the whole grid does not start with one contended atomic per wave.
+  const int n_waves = gridDim.x * (blockDim.x >> 6);
+  auto grab = [&]() {
     int next = 0;
-    if (lane == 0) next = atomicAdd(w.work_counter, 1);
-    const int item = __builtin_amdgcn_readfirstlane(next);
-    if (item >= w.n_ditems) break;
-    const int code = w.ditems[item];
-    decode_item<D, PPS>(a, w, code & 0xffff, (code >> 16) & 63, (code >> 22) & 1023, lane);
+    if (lane == 0) next = n_waves + atomicAdd(w.work_counter, 1);
+    return next;
+  };
+  auto pages_of = [&](const DItem& it) { return min(PPS, (it.L - 16 * PPS * it.split + 15) >> 4); };
+  // The item's page ids, one per lane (at most PPS <= 64), and Q^T as the MFMA B operand:
+  // column = head of the group, k = dims 32 ks + 8 quad .. +8.
+  auto fetch_lane_data = [&](const DItem& it, int& ids, bf16x8 (&qf)[D / 32]) {
+    const int* prow = a.page_table + (size_t)it.req * a.max_pages + (size_t)it.split * PPS;
+    ids = lane < pages_of(it) ? prow[lane] : 0;
+    const __bf16* qrow = reinterpret_cast<const __bf16*>(a.q) + ((size_t)it.q_start * a.h_q + it.j * g + col) * D + quad * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const uint4 u = col < g ? *reinterpret_cast<const uint4*>(qrow + ks * 32) : make_uint4(0, 0, 0, 0);
+      qf[ks] = __builtin_bit_cast(bf16x8, u);
+    }
+  };
+  struct Ids {
+    size_t slab;
+    bool ok;
+  };
+  int bad = 0;
+  // Page p (clamped to the item's last page) of an item whose ids a lane-distributed register holds.
+  auto page_id = [&](int id_reg, int p, int n_pages, int j) {
+    Ids r;
+    const int id = __builtin_amdgcn_readlane(id_reg, min(p, n_pages - 1));
+    r.ok = page_ok(id, a.num_phys_pages);
+    bad |= !r.ok;
+    r.slab = (size_t)(r.ok ? id : 0) * slab_stride_pages + j;
+    return r;
+  };
+
+  const int first = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (first >= n_items) return;
+  DItem cur = unpack_item(sload4(w.ditems + first), true);
+  int cur_ids;
+  bf16x8 qf[D / 32];
+  fetch_lane_data(cur, cur_ids, qf);
+
+  Page<D> buf[R];
+  Ids ids[R];
+  {
+    const int np = pages_of(cur);
+#pragma unroll
+    for (int k = 0; k < R - 1; ++k) {
+      ids[k] = page_id(cur_ids, k, np, cur.j);
+      load_page<D>(buf[k], kcache, vcache, ids[k].slab, lane);
+    }
   }
+
+  for (;;) {
+    const int n_pages = pages_of(cur);
+    // At least two groups, so the next item's descriptor and ids (fetched in the first group)
+    // are in before the last group loads its first pages.
+    const int n_groups = max(2, (n_pages + R - 1) / R);
+    const int n_tok = cur.L - 16 * PPS * cur.split;  // the item's tokens, from its first page on
+
+    int nxt_raw = 0, nxt_ids = 0;
+    DItem nxt;
+    bf16x8 qn[D / 32];
+
+    f32x4 acc[D / 16];
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float l_run = 0.f;
+    float m_ref = -INFINITY;  // reference max (base-2 units) the probabilities are taken against
+
+    auto compute = [&](const Page<D>& pg, int p, const Ids& pid) {
+      // Scores S^T: lane holds head `col`, tokens 4 quad + i of the page.
+      f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pg.k[ks]), qf[ks], sc, 0, 0, 0);
+      const int t0 = 16 * p + 4 * quad;
+      // Tokens past the end (NaN-poisoned slots, and the padding pages of the last group) and
+      // tokens of a bad page are masked; only the last pages of an item or a bad page need it.
+      const bool tail = 16 * (p + 1) > n_tok || !pid.ok;
+      if (tail) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (!pid.ok || t0 + i >= n_tok) sc[i] = -INFINITY;
+      }
+      float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx *= a.scale_log2;  // the scale is positive: max of scaled = scaled max
+      // The reference max moves only when a score exceeds it by more than the slack, so the
+      // output rescale is rare; numerator and denominator share the reference.
+      if (__any(mx > m_ref + kRescaleSlack)) {
+        const float m_new = fmaxf(m_ref, mx);
+        const float alpha = fast_exp2(m_ref - m_new);
+        m_ref = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int n = 0; n < D / 16; ++n) acc[n] *= alpha;
+      }
+      bf16x4 pb4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pb4[i] = static_cast<__bf16>(fast_exp2(__builtin_fmaf(sc[i], a.scale_log2, -m_ref)));
+      // The denominator sums the bf16 probabilities the PV product consumes.
+      const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[0], pb4[1]}, ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb4[2], pb4[3]}, ones, l_run, false);
+      const s16x4 pbs = __builtin_bit_cast(s16x4, pb4);
+      // Their values must not reach the MFMA either (0 x NaN is NaN).
+      const uint64_t mk = !pid.ok ? 0ull : (tail ? low_elems_mask(n_tok - t0) : ~0ull);
+#pragma unroll
+      for (int n = 0; n < D / 16; ++n) {
+        const uint64_t v = ((uint64_t)pg.v[n].y << 32 | pg.v[n].x) & mk;
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, v), pbs, acc[n], 0, 0, 0);
+      }
+    };
+
+    // One group of R pages.  Every group issues the same loads in the same order (sources are
+    // selected, never branched on), so the wait counts stay exact across the loop.  The first
+    // group also fetches the next item: counter, descriptor (scalar), then ids and query.  The
+    // last group loads the next item's first R - 1 pages (or, with no next item, re-reads).
+    auto group = [&](int grp, auto first_tag, auto last_tag) {
+      constexpr bool kFirst = decltype(first_tag)::value;
+      constexpr bool kLast = decltype(last_tag)::value;
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        if constexpr (kFirst) {
+          if (u == 0) nxt_raw = grab();
+          if (u == 1) {
+            const int idx = __builtin_amdgcn_readfirstlane(nxt_raw);
+            nxt = unpack_item(sload4(w.ditems + min(idx, n_items - 1)), idx < n_items);
+          }
+          if (u == 2) fetch_lane_data(nxt, nxt_ids, qn);  // a valid address even without a next item
+        }
+        const int p = grp * R + u;
+        const bool from_nxt = kLast && u > 0 && nxt.valid;
+        const int src_ids = from_nxt ? nxt_ids : cur_ids;
+        const int src_page = from_nxt ? u - 1 : p + R - 1;
+        const int src_pages = from_nxt ? pages_of(nxt) : n_pages;
+        const int src_j = from_nxt ? nxt.j : cur.j;
+        ids[(u + R - 1) % R] = page_id(src_ids, src_page, src_pages, src_j);
+        load_page<D>(buf[(u + R - 1) % R], kcache, vcache, ids[(u + R - 1) % R].slab, lane);
+        compute(buf[u], p, ids[u]);
+      }
+    };
+    using T = std::true_type;
+    using F = std::false_type;
+    group(0, T{}, F{});
+    for (int grp = 1; grp < n_groups - 1; ++grp) group(grp, F{}, F{});
+    group(n_groups - 1, F{}, T{});
+
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (col < g) {
+      float* pa = w.pacc + ((size_t)cur.slot * g + col) * D + 4 * quad;
+#pragma unroll
+      for (int n = 0; n < D / 16; ++n) *reinterpret_cast<f32x4*>(pa + 16 * n) = acc[n];
+      if (quad == 0) {
+        w.pml[((size_t)cur.slot * g + col) * 2 + 0] = m_ref;
+        w.pml[((size_t)cur.slot * g + col) * 2 + 1] = l_tot;
+      }
+    }
+    if (!nxt.valid) break;
+    cur = nxt;
+    cur_ids = nxt_ids;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) qf[ks] = qn[ks];
+  }
+  if (bad && lane == 0) atomicOr(w.err, 1);
 }
 
 // fp32 path (small shapes): one wave per item, lane = dim, scores reduced across the wave.

@@ -27,7 +27,8 @@ struct WorkArgs {
   const int4* dreq;     // [RD] decode requests (req, item_base, n_split, n_pages)
   float* pacc;          // [ND, group, d]  unnormalised split-K partial outputs
   float* pml;           // [ND, group, 2]  (running max in base-2 units, softmax denominator)
-  const int32_t* ditems;  // [ND] bf16 decode items in execution order: i | j << 16 | s << 22
+  const int4* ditems;   // [ND] bf16 decode items in execution order: (q_start, req | kv head << 24,
+                        //      split | kv_len << 10, row of the split's partial)
   int32_t* err;         // error word: bit 0 = page id out of range
   int32_t* work_counter;  // next decode item to take (zeroed by the per-call upload)
   int32_t n_pitems, n_dreq, max_split, n_ditems;

@@ -60,7 +60,7 @@ struct StagingSlot {
 // (decode, i, 1, cached_len + s), i = its index among the decode requests).
 struct StepPlan {
   std::vector<int4> meta, dreq;
-  std::vector<int32_t> ditems;
+  std::vector<int4> ditems;
   int n_items = 0, max_split = 0;
   size_t off_meta = 0, off_dreq = 0, off_ditems = 0;
 };
@@ -68,7 +68,7 @@ struct StepPlan {
 // Work lists of one iteration and where they live in the caller's workspace.
 struct Plan {
   std::vector<int4> meta, pitems, dreq;
-  std::vector<int32_t> ditems;
+  std::vector<int4> ditems;
   std::vector<StepPlan> ahead;  // look-ahead decode steps 1 .. steps - 1
   int steps = 1;
   int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0, prefill_id_cap = 0;
@@ -83,10 +83,12 @@ int pages_per_split_for(const duet_shape* s) {
 
 // Decode work of the batch's decode requests when each holds `extra` more tokens than seq_meta
 // states: per request (req, item_base, n_split, n_pages), and for bf16 the work items in
-// execution order -- every full split first, then the shorter last splits (longest first),
-// packed as i | j << 16 | s << 22.
-void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool fill, std::vector<int4>* dreq,
-                  std::vector<int32_t>* ditems, int64_t* n_dreq, int64_t* n_items, int* max_split) {
+// execution order -- every full split first, then the shorter last splits, longest first -- as
+// descriptors (q_start, req | kv head << 24, split | kv_len << 10, row of the split's partial).
+// With step_rows (look-ahead steps), decode request i reads its query from row i.
+void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step_rows, bool fill,
+                  std::vector<int4>* dreq, std::vector<int4>* ditems, int64_t* n_dreq, int64_t* n_items,
+                  int* max_split) {
   const int pps = pages_per_split_for(s);
   dreq->clear();
   ditems->clear();
@@ -106,16 +108,26 @@ void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool fill
   }
   if (fill && s->dtype == DUET_BF16) {
     ditems->reserve(*n_items);
-    for (int pass = 0; pass < 2; ++pass)
-      for (size_t i = 0; i < dreq->size(); ++i) {
-        const int4 d = (*dreq)[i];
-        const bool full_last = d.w % pps == 0;
-        for (int j = 0; j < s->num_kv_heads; ++j)
-          for (int sp = 0; sp < d.z; ++sp) {
-            const bool is_full = sp + 1 < d.z || full_last;
-            if (is_full == (pass == 0)) ditems->push_back((int32_t)i | (j << 16) | (sp << 22));
-          }
-      }
+    struct Part {
+      int pages;
+      int4 item;
+    };
+    std::vector<Part> parts;
+    for (size_t i = 0; i < dreq->size(); ++i) {
+      const int4 d = (*dreq)[i];
+      const duet_seq_meta& q = b->reqs[d.x];
+      const int L = q.cached_len + q.q_len + extra;
+      const int q_start = step_rows ? (int)i : q.q_start;
+      for (int j = 0; j < s->num_kv_heads; ++j)
+        for (int sp = 0; sp < d.z; ++sp) {
+          const int pages = std::min(pps, d.w - sp * pps);
+          const int4 it = make_int4(q_start, d.x | (j << 24), sp | (L << 10), d.y + j * d.z + sp);
+          if (pages == pps) ditems->push_back(it);
+          else parts.push_back({pages, it});
+        }
+    }
+    std::stable_sort(parts.begin(), parts.end(), [](const Part& x, const Part& y) { return x.pages > y.pages; });
+    for (const Part& pt : parts) ditems->push_back(pt.item);
   }
 }
 
@@ -170,7 +182,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   }
   int64_t n_dreq = 0, n_items = 0;
   int max_split = 0;
-  decode_lists(s, b, 0, fill, &p->dreq, &p->ditems, &n_dreq, &n_items, &max_split);
+  decode_lists(s, b, 0, false, fill, &p->dreq, &p->ditems, &n_dreq, &n_items, &max_split);
   p->n_items_decode = (int)n_items;
   p->max_split = max_split;
   size_t off = align_up(kCounterOffset + (size_t)layers * steps * sizeof(int32_t));
@@ -181,7 +193,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   p->off_dreq = off;
   off = align_up(off + (size_t)n_dreq * sizeof(int4));
   p->off_ditems = off;
-  off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)n_items * sizeof(int32_t) : 0));
+  off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)n_items * sizeof(int4) : 0));
   // Look-ahead steps: each has its own metadata and decode lists; the split-K partials are
   // shared, since the steps run one after another on one stream.
   int64_t max_items = n_items;
@@ -198,7 +210,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
       }
     }
     int64_t nd = 0, ni = 0;
-    decode_lists(s, b, st, fill, &sp.dreq, &sp.ditems, &nd, &ni, &sp.max_split);
+    decode_lists(s, b, st, true, fill, &sp.dreq, &sp.ditems, &nd, &ni, &sp.max_split);
     sp.n_items = (int)ni;
     max_items = std::max(max_items, ni);
     sp.off_meta = off;
@@ -206,7 +218,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
     sp.off_dreq = off;
     off = align_up(off + (size_t)nd * sizeof(int4));
     sp.off_ditems = off;
-    off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)ni * sizeof(int32_t) : 0));
+    off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)ni * sizeof(int4) : 0));
   }
   p->upload_bytes = off;
   p->off_pacc = off;
@@ -384,11 +396,11 @@ int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
   std::memcpy(h + p.off_meta, p.meta.data(), p.meta.size() * sizeof(int4));
   std::memcpy(h + p.off_pitems, p.pitems.data(), p.pitems.size() * sizeof(int4));
   std::memcpy(h + p.off_dreq, p.dreq.data(), p.dreq.size() * sizeof(int4));
-  std::memcpy(h + p.off_ditems, p.ditems.data(), p.ditems.size() * sizeof(int32_t));
+  std::memcpy(h + p.off_ditems, p.ditems.data(), p.ditems.size() * sizeof(int4));
   for (const StepPlan& sp : p.ahead) {
     std::memcpy(h + sp.off_meta, sp.meta.data(), sp.meta.size() * sizeof(int4));
     std::memcpy(h + sp.off_dreq, sp.dreq.data(), sp.dreq.size() * sizeof(int4));
-    std::memcpy(h + sp.off_ditems, sp.ditems.data(), sp.ditems.size() * sizeof(int32_t));
+    std::memcpy(h + sp.off_ditems, sp.ditems.data(), sp.ditems.size() * sizeof(int4));
   }
   HIP_TRY(hipMemcpyAsync(ws, h, p.upload_bytes, hipMemcpyHostToDevice, st));
   HIP_TRY(hipEventRecord(slot.done, st));
@@ -446,6 +458,7 @@ int check_call(duet_ctx* ctx, const duet_shape* shape, int layers, const void* c
         return fail(DUET_EUNSUPPORTED, "request %d: decode context %lld too long", r, (long long)L);
     }
     if (n_dec > 65535) return fail(DUET_EUNSUPPORTED, "more than 65535 decode requests");
+    if (batch->num_reqs >= (1 << 24)) return fail(DUET_EUNSUPPORTED, "more than %d requests", (1 << 24) - 1);
     if (shape->num_kv_heads > 63) return fail(DUET_EUNSUPPORTED, "more than 63 kv heads");
   }
   if (split.mode == DUET_SPLIT) {
@@ -480,7 +493,7 @@ void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char
   w->dreq = reinterpret_cast<const int4*>(ws + p.off_dreq);
   w->pacc = reinterpret_cast<float*>(ws + p.off_pacc);
   w->pml = reinterpret_cast<float*>(ws + p.off_pml);
-  w->ditems = reinterpret_cast<const int32_t*>(ws + p.off_ditems);
+  w->ditems = reinterpret_cast<const int4*>(ws + p.off_ditems);
   w->err = reinterpret_cast<int32_t*>(ws);
   w->n_ditems = (int)p.ditems.size();
   w->decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
@@ -727,7 +740,7 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
       const StepPlan& spl = p.ahead[st - 1];
       ws_w.meta = reinterpret_cast<const int4*>(ws + spl.off_meta);
       ws_w.dreq = reinterpret_cast<const int4*>(ws + spl.off_dreq);
-      ws_w.ditems = reinterpret_cast<const int32_t*>(ws + spl.off_ditems);
+      ws_w.ditems = reinterpret_cast<const int4*>(ws + spl.off_ditems);
       ws_w.n_dreq = (int)spl.dreq.size();
       ws_w.n_ditems = (int)spl.ditems.size();
       ws_w.max_split = spl.max_split;
