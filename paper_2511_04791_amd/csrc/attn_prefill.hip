@@ -243,6 +243,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
 
   for (int t = 0; t < kStages - 1 && t < n_tiles; ++t) issue_tile(t);
   publish(0, min(n_tiles - 1, kStages - 2));
+  // The query fragments have landed before the loop (tile 0's wait above covers them in
+  // hardware, but the compiler would otherwise keep them pending at the loop head and make every
+  // step's first MFMA wait for all tile loads in flight, collapsing the ring to one tile).
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 
   // S^T of key tile kt for this wave's 32 rows: K fragments from LDS, Q^T from registers.
   auto scores = [&](int kt, f32x16 (&sacc)[2]) {
