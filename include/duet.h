@@ -202,8 +202,9 @@ int duet_destroy(duet_ctx* ctx);
 duet_model* duet_ctx_model(duet_ctx* ctx);
 
 /* Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
- * (shape->num_layers decode work counters) and batch: metadata, work lists, split-K partials
- * and an error word.  Host only. */
+ * and batch: an error word, the decode work-queue counters, metadata, work lists and split-K
+ * partials.  The layers of a call share all of it, so the size does not depend on
+ * shape->num_layers.  Host only. */
 int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
 
 /* One layer's attention over a mixed batch (Section 4.3: prefill and decode of one iteration
@@ -251,8 +252,8 @@ int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* cons
  * decode steps fit in one prefill step: t = max(k t_d, t_p)). */
 
 /* Workspace for duet_attn_lookahead with k_decode_steps steps (shape->num_layers layers):
- * duet_workspace_bytes' layout plus a decode work counter per (step, layer) and the metadata
- * and work lists of steps 1 .. k - 1.  Host only. */
+ * duet_workspace_bytes' layout plus the metadata and work lists of steps 1 .. k - 1.  Host
+ * only. */
 int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* batch, int32_t k_decode_steps,
                                    size_t* bytes);
 

@@ -21,6 +21,9 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              # MFMA accumulators in VGPRs: the online-softmax rescale works on them in place
              "-mllvm", "-amdgpu-mfma-vgpr-form",
+             # atomics stay as written: the decode kernel's one-lane counter atomic must not get the
+             # wave-aggregation rewrite, which reads its result right after issue
+             "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
              "-I" + INCLUDE, "-I" + CSRC]
 CXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-I" + INCLUDE, "-I" + CSRC,
              "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__"]

@@ -47,6 +47,26 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Combine a value across the four 16-lane rows of a wave (lanes l, l ^ 16, l ^ 32, l ^ 48) with
+// the row-swap permutes, which stay in the vector ALU: an LDS permute would be counted with the
+// scalar loads, so waiting for it would also wait for them.
+__device__ __forceinline__ float max_rows(float x) {
+  const unsigned u = __float_as_uint(x);
+  auto s32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const float m = fmaxf(__uint_as_float(s32[0]), __uint_as_float(s32[1]));
+  const unsigned v = __float_as_uint(m);
+  auto s16 = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(s16[0]), __uint_as_float(s16[1]));
+}
+__device__ __forceinline__ float sum_rows(float x) {
+  const unsigned u = __float_as_uint(x);
+  auto s16 = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = __uint_as_float(s16[0]) + __uint_as_float(s16[1]);  // rows (0+1, 0+1, 2+3, 2+3)
+  const unsigned v = __float_as_uint(m);
+  auto s32 = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
+}
+
 // K/V pages are read exactly once per iteration.
 #ifdef DUET_DECODE_NT_LOADS
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -89,15 +109,15 @@ __device__ __forceinline__ void load_page(Page<D>& pg, const char* kbase, const 
 
 __device__ __forceinline__ bool page_ok(int id, long long num_phys) { return id >= 0 && (long long)id < num_phys; }
 
-// Uniform loads of the read-only work list through the scalar cache: they are counted by
-// lgkmcnt, so waiting for them never waits for the page stream in flight.
+// Uniform loads of the read-only work list through the scalar cache (used before the page stream
+// starts; inside it a scalar load would be waited for together with every LDS operation).
 __device__ __forceinline__ i32x4 sload4(const void* p) { return *(const __attribute__((address_space(4))) i32x4*)(p); }
 
-// A decode work item as the host lists it: (q_start, req | kv head << 24, split | kv_len << 10,
-// row of its split-K partial).  pages_in_split, and the item's tokens, are relative to the
-// split's first page.
+// A decode work item as the host lists it: (q_start, req | kv head << 24, first page |
+// (tokens - 1) << 22, row of its split-K partial).  The item covers `tokens` keys (at most 16 PPS)
+// from its first logical page on.
 struct DItem {
-  int q_start, req, j, split, L, slot;
+  int q_start, req, j, first_page, n_tok, slot;
   bool valid;
 };
 __device__ __forceinline__ DItem unpack_item(i32x4 v, bool valid) {
@@ -105,8 +125,8 @@ __device__ __forceinline__ DItem unpack_item(i32x4 v, bool valid) {
   d.q_start = v.x;
   d.req = v.y & 0xffffff;
   d.j = (int)((unsigned)v.y >> 24);
-  d.split = v.z & 1023;
-  d.L = (int)((unsigned)v.z >> 10);
+  d.first_page = v.z & 0x3fffff;
+  d.n_tok = (int)((unsigned)v.z >> 22) + 1;
   d.slot = v.w;
   d.valid = valid;
   return d;
@@ -125,6 +145,12 @@ __device__ __forceinline__ DItem unpack_item(i32x4 v, bool valid) {
 #ifndef DUET_DECODE_MIN_BLOCKS_PER_CU
 #define DUET_DECODE_MIN_BLOCKS_PER_CU 1
 #endif
+// Per-wave LDS staging of finished items' partials (floats): up to kStageFloats / (g d + 2 g)
+// items (7 for g = 4, d = 128) are written out together, when the buffer is full or the wave's
+// work is done.  A store's completion comes back late while the memory system streams reads, and
+// vector memory operations complete in order, so every store burst stalls the page loads issued
+// after it until it completes: one burst per buffer instead of one per item.
+constexpr int kStageFloats = 4096;
 template <int D, int PPS>
 __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
   constexpr int R = kRing;
@@ -139,19 +165,63 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
   // Both caches are [P, h_kv, 16 * d] in bytes per (page, head) slab; fold h_kv into the page stride.
   const long long slab_stride_pages = a.h_kv;
 
-  // Wave v of the grid starts with item v; later items come from the counter, past the first
-  // ones, so the whole grid does not start with one contended atomic per wave.
-  const int n_waves = gridDim.x * (blockDim.x >> 6);
-  auto grab = [&]() {
-    int next = 0;
-    if (lane == 0) next = n_waves + atomicAdd(w.work_counter, 1);
-    return next;
+  __shared__ __align__(16) float stage_lds[4 * kStageFloats];
+  float* const stage = stage_lds + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) * kStageFloats;
+  const int ml_floats = (2 * g + 3) & ~3;
+  const int item_floats = g * D + ml_floats;  // [g][d] output, then (m, l) per head
+  const int n_slots = kStageFloats / item_floats;
+  int n_staged = 0;     // items in the buffer
+  int staged_rows = 0;  // lane k: partial row of buffered item k
+  // Writes the buffered items to their partial rows, coalesced (LDS operations of one wave complete
+  // in order, so the reads see the staging writes).
+  auto flush = [&]() {
+    for (int k = 0; k < n_staged; ++k) {
+      const int row = __builtin_amdgcn_readlane(staged_rows, k);
+      const float* src = stage + k * item_floats;
+      float* dst = w.pacc + (size_t)row * g * D;
+      for (int i = 4 * lane; i < g * D; i += 256)
+        *reinterpret_cast<f32x4*>(dst + i) = *reinterpret_cast<const f32x4*>(src + i);
+      if (lane < 2 * g) w.pml[(size_t)row * 2 * g + lane] = src[g * D + lane];
+    }
+    n_staged = 0;
   };
-  auto pages_of = [&](const DItem& it) { return min(PPS, (it.L - 16 * PPS * it.split + 15) >> 4); };
+
+  // Wave v of the grid starts with items v and n_waves + v; the items past those are dealt
+  // round-robin to n_queues counters (one atomic per item on a single counter would saturate it),
+  // and wave v takes them from counter v % n_queues: ticket t is item 2 n_waves + t n_queues + c.
+  // Every queue has a wave (n_waves >= n_queues), and a wave's tickets rise, as do their items,
+  // all of them above the static ones: when a wave stops at an item past the end, every ticket it
+  // still holds is past the end too.
+  const int n_waves = gridDim.x * (blockDim.x >> 6);
+  const int n_queues = n_waves >= kDecodeQueues ? kDecodeQueues : 1;
+  const int first = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int queue = first % n_queues;
+  int* const counter = w.work_counter + queue * kDecodeQueueStride;
+  // The counter's old value, in lane 0; nothing touches it in the branch, so the load is waited
+  // for only where it is read.
+  auto grab = [&]() {
+    int ticket = 0;
+    if (lane == 0) ticket = atomicAdd(counter, 1);
+    return ticket;
+  };
+  // An item's descriptor through the vector memory path, one word per lane: it completes in order
+  // with the page loads issued before it, so waiting for it never drains the page stream.
+  auto load_desc = [&](int idx) {
+    return reinterpret_cast<const int*>(w.ditems)[(size_t)min(idx, n_items - 1) * 4 + (lane & 3)];
+  };
+  auto desc_item = [&](int words, int idx) {
+    i32x4 v;
+    v.x = __builtin_amdgcn_readlane(words, 0);
+    v.y = __builtin_amdgcn_readlane(words, 1);
+    v.z = __builtin_amdgcn_readlane(words, 2);
+    v.w = __builtin_amdgcn_readlane(words, 3);
+    return unpack_item(v, idx < n_items);
+  };
+  auto pages_of = [&](const DItem& it) { return min(PPS, (it.n_tok + 15) >> 4); };
   // The item's page ids, one per lane (at most PPS <= 64), and Q^T as the MFMA B operand:
   // column = head of the group, k = dims 32 ks + 8 quad .. +8.
   auto fetch_lane_data = [&](const DItem& it, int& ids, bf16x8 (&qf)[D / 32]) {
-    const int* prow = a.page_table + (size_t)it.req * a.max_pages + (size_t)it.split * PPS;
+    const int* prow = a.page_table + (size_t)it.req * a.max_pages + it.first_page;
     ids = lane < pages_of(it) ? prow[lane] : 0;
     const __bf16* qrow = reinterpret_cast<const __bf16*>(a.q) + ((size_t)it.q_start * a.h_q + it.j * g + col) * D + quad * 8;
 #pragma unroll
@@ -175,9 +245,9 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     return r;
   };
 
-  const int first = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (first >= n_items) return;
   DItem cur = unpack_item(sload4(w.ditems + first), true);
+  DItem nxt = unpack_item(sload4(w.ditems + min(first + n_waves, n_items - 1)), first + n_waves < n_items);
   int cur_ids;
   bf16x8 qf[D / 32];
   fetch_lane_data(cur, cur_ids, qf);
@@ -198,10 +268,9 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     // At least two groups, so the next item's descriptor and ids (fetched in the first group)
     // are in before the last group loads its first pages.
     const int n_groups = max(2, (n_pages + R - 1) / R);
-    const int n_tok = cur.L - 16 * PPS * cur.split;  // the item's tokens, from its first page on
+    const int n_tok = cur.n_tok;  // the item's tokens, from its first page on
 
-    int nxt_raw = 0, nxt_ids = 0;
-    DItem nxt;
+    int ticket = 0, nn_words = 0, nn_idx = n_items, nxt_ids = 0;
     bf16x8 qn[D / 32];
 
     f32x4 acc[D / 16];
@@ -226,8 +295,7 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
           if (!pid.ok || t0 + i >= n_tok) sc[i] = -INFINITY;
       }
       float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = max_rows(mx);
       mx *= a.scale_log2;  // the scale is positive: max of scaled = scaled max
       // The reference max moves only when a score exceeds it by more than the slack, so the
       // output rescale is rare; numerator and denominator share the reference.
@@ -257,21 +325,26 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     };
 
     // One group of R pages.  Every group issues the same loads in the same order (sources are
-    // selected, never branched on), so the wait counts stay exact across the loop.  The first
-    // group also fetches the next item: counter, descriptor (scalar), then ids and query.  The
-    // last group loads the next item's first R - 1 pages (or, with no next item, re-reads).
+    // selected, never branched on), so the wait counts stay exact across the loop.  Items move
+    // through a pipeline two deep: the first group takes a ticket for the item after next and
+    // fetches the next item's ids and query; the last group reads the ticket (its atomic has
+    // returned while the pages loaded after it did), loads that item's descriptor, then the next
+    // item's first R - 1 pages (or, with no next item, re-reads).  No result is used right after
+    // its load.
     auto group = [&](int grp, auto first_tag, auto last_tag) {
       constexpr bool kFirst = decltype(first_tag)::value;
       constexpr bool kLast = decltype(last_tag)::value;
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         if constexpr (kFirst) {
-          if (u == 0) nxt_raw = grab();
-          if (u == 1) {
-            const int idx = __builtin_amdgcn_readfirstlane(nxt_raw);
-            nxt = unpack_item(sload4(w.ditems + min(idx, n_items - 1)), idx < n_items);
-          }
+          if (u == 0) ticket = grab();
           if (u == 2) fetch_lane_data(nxt, nxt_ids, qn);  // a valid address even without a next item
+        }
+        if constexpr (kLast) {
+          if (u == 0) {
+            nn_idx = 2 * n_waves + __builtin_amdgcn_readfirstlane(ticket) * n_queues + queue;
+            nn_words = load_desc(nn_idx);
+          }
         }
         const int p = grp * R + u;
         const bool from_nxt = kLast && u > 0 && nxt.valid;
@@ -290,19 +363,24 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     for (int grp = 1; grp < n_groups - 1; ++grp) group(grp, F{}, F{});
     group(n_groups - 1, F{}, T{});
 
-    float l_tot = l_run + __shfl_xor(l_run, 16);
-    l_tot += __shfl_xor(l_tot, 32);
-    if (col < g) {
-      float* pa = w.pacc + ((size_t)cur.slot * g + col) * D + 4 * quad;
+    const float l_tot = sum_rows(l_run);
+    {
+      float* st = stage + n_staged * item_floats;
+      if (col < g) {
 #pragma unroll
-      for (int n = 0; n < D / 16; ++n) *reinterpret_cast<f32x4*>(pa + 16 * n) = acc[n];
-      if (quad == 0) {
-        w.pml[((size_t)cur.slot * g + col) * 2 + 0] = m_ref;
-        w.pml[((size_t)cur.slot * g + col) * 2 + 1] = l_tot;
+        for (int n = 0; n < D / 16; ++n) *reinterpret_cast<f32x4*>(st + col * D + 16 * n + 4 * quad) = acc[n];
+        if (quad == 0) {
+          st[g * D + 2 * col + 0] = m_ref;
+          st[g * D + 2 * col + 1] = l_tot;
+        }
       }
+      staged_rows = lane == n_staged ? cur.slot : staged_rows;
+      ++n_staged;
     }
+    if (n_staged == n_slots || !nxt.valid) flush();
     if (!nxt.valid) break;
     cur = nxt;
+    nxt = desc_item(nn_words, nn_idx);
     cur_ids = nxt_ids;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) qf[ks] = qn[ks];
@@ -379,6 +457,9 @@ __global__ __launch_bounds__(256) void decode_partial_f32(AttnArgs a, WorkArgs w
 template <int D, typename OutT>
 __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
   constexpr int E = D / 64;
+  // The partial kernel before this one on the stream has finished with the queue counters: clear
+  // them for the next one.
+  if (blockIdx.x == 0 && threadIdx.x < kDecodeQueues) w.work_counter[threadIdx.x * kDecodeQueueStride] = 0;
   const int lane = threadIdx.x & 63;
   const int pair = blockIdx.x * 4 + uniform(threadIdx.x >> 6);
   const int i = pair / a.h_q;

@@ -28,9 +28,9 @@ struct WorkArgs {
   float* pacc;          // [ND, group, d]  unnormalised split-K partial outputs
   float* pml;           // [ND, group, 2]  (running max in base-2 units, softmax denominator)
   const int4* ditems;   // [ND] bf16 decode items in execution order: (q_start, req | kv head << 24,
-                        //      split | kv_len << 10, row of the split's partial)
+                        //      first page | (tokens - 1) << 22, row of the item's partial)
   int32_t* err;         // error word: bit 0 = page id out of range
-  int32_t* work_counter;  // next decode item to take (zeroed by the per-call upload)
+  int32_t* work_counter;  // kDecodeCounterInts ints: the decode queues' next tickets (see kDecodeQueues)
   int32_t n_pitems, n_dreq, max_split, n_ditems;
   int32_t pages_per_split;
   int32_t decode_cus;   // CUs the decode stream may use (sizes the persistent grid)
@@ -55,6 +55,38 @@ struct AppendArgs {
 // Decode split length in pages (bf16); fixed, so results do not depend on the CU split.
 constexpr int kDecodePagesPerSplit = DUET_DECODE_PAGES_PER_SPLIT;
 constexpr int kDecodePagesPerSplitF32 = 2;
+#ifndef DUET_DECODE_TAIL_SPLITS
+#define DUET_DECODE_TAIL_SPLITS 0
+#endif
+#ifndef DUET_DECODE_TAIL_PAGES
+#define DUET_DECODE_TAIL_PAGES 8
+#endif
+// bf16 decode items: a (request, kv head) page range is cut into splits of kDecodePagesPerSplit
+// pages from its first page on; with kDecodeTailSplits > 0 the pages of its last kDecodeTailSplits
+// splits are cut into pieces of kDecodeTailPages instead, which run last, so the kernel ends with
+// short items (near its end a wave streams alone, at the rate its few pages in flight allow).  The
+// cut depends on the request's length only.  Off by default: measured, it shortens the tail on all
+// 256 CUs but costs more than it saves on smaller shares.
+constexpr int kDecodeTailSplits = DUET_DECODE_TAIL_SPLITS;
+constexpr int kDecodeTailPages = DUET_DECODE_TAIL_PAGES;
+static_assert(kDecodeTailPages <= kDecodePagesPerSplit, "tail pieces are shorter than splits");
+// Most logical pages of a bf16 decode request (an item's first page is a 22-bit field).
+constexpr long long kMaxDecodePages = (1LL << 22) - 1;
+
+#ifndef DUET_DECODE_QUEUES
+#define DUET_DECODE_QUEUES 8
+#endif
+#ifndef DUET_DECODE_QUEUE_STRIDE
+#define DUET_DECODE_QUEUE_STRIDE 32
+#endif
+// The persistent decode kernel's work queue is split into kDecodeQueues counters (items are dealt
+// round-robin to them), each on its own 128-byte line: atomics on one line are serialised, at a
+// few tens per microsecond.  Every decode launch of a call uses the same counters: the upload
+// zeroes them and each reduce kernel clears them once its partial kernel is done, before the
+// next partial kernel on the stream starts.
+constexpr int kDecodeQueues = DUET_DECODE_QUEUES;
+constexpr int kDecodeQueueStride = DUET_DECODE_QUEUE_STRIDE;
+constexpr int kDecodeCounterInts = kDecodeQueues * kDecodeQueueStride;
 
 // Keys a prefill request may attend (its page ids are staged in LDS: 8192 ids, 32 KB).
 constexpr int kMaxPrefillKeys = 131072;

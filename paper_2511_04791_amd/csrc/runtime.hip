@@ -34,9 +34,9 @@ using namespace duet;
 constexpr int kStagingSlots = 4;
 constexpr size_t kMaxMaskedStreams = 6;  // each CU-masked stream owns a hardware queue
 constexpr size_t kAlign = 256;
-// Workspace head: the device error word at offset 0, one decode work counter per layer from
+// Workspace head: the device error word at offset 0 and the decode queue counters from
 // kCounterOffset on; the head is zeroed by every call's upload.
-constexpr size_t kCounterOffset = 64;
+constexpr size_t kCounterOffset = 128;
 constexpr int kMaxLayers = 1024;
 constexpr int kMaxLookahead = 64;     // decode steps per look-ahead call
 constexpr size_t kMaxGraphs = 128;    // cached decode-step graphs per context
@@ -86,6 +86,20 @@ int pages_per_split_for(const duet_shape* s) {
 // execution order -- every full split first, then the shorter last splits, longest first -- as
 // descriptors (q_start, req | kv head << 24, split | kv_len << 10, row of the split's partial).
 // With step_rows (look-ahead steps), decode request i reads its query from row i.
+// How a (request, kv head) range of n_pages pages is cut: n_long splits of pps pages from page 0
+// (the last one short when nothing follows it), then n_short tail pieces of kDecodeTailPages
+// pages (the last one short).  fp32 keeps uniform splits.
+struct SplitShape {
+  int n_long, n_short;
+};
+SplitShape split_shape(int n_pages, int pps, bool graded) {
+  const int n = (n_pages + pps - 1) / pps;
+  if (!graded || kDecodeTailSplits == 0) return {n, 0};
+  const int n_long = std::max(0, n - kDecodeTailSplits);
+  const int rest = n_pages - n_long * pps;
+  return {n_long, (rest + kDecodeTailPages - 1) / kDecodeTailPages};
+}
+
 void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step_rows, bool fill,
                   std::vector<int4>* dreq, std::vector<int4>* ditems, int64_t* n_dreq, int64_t* n_items,
                   int* max_split) {
@@ -100,7 +114,8 @@ void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step
     if (q.kind != DUET_KIND_DECODE) continue;
     const int64_t L = (int64_t)q.cached_len + q.q_len + extra;
     const int n_pages = (int)((L + 15) / 16);
-    const int n_split = (n_pages + pps - 1) / pps;
+    const SplitShape ss = split_shape(n_pages, pps, s->dtype == DUET_BF16);
+    const int n_split = ss.n_long + ss.n_short;
     if (fill) dreq->push_back(make_int4(r, (int)*n_items, n_split, n_pages));
     *n_items += (int64_t)s->num_kv_heads * n_split;
     *max_split = std::max(*max_split, n_split);
@@ -118,10 +133,14 @@ void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step
       const duet_seq_meta& q = b->reqs[d.x];
       const int L = q.cached_len + q.q_len + extra;
       const int q_start = step_rows ? (int)i : q.q_start;
+      const SplitShape ss = split_shape(d.w, pps, true);
       for (int j = 0; j < s->num_kv_heads; ++j)
         for (int sp = 0; sp < d.z; ++sp) {
-          const int pages = std::min(pps, d.w - sp * pps);
-          const int4 it = make_int4(q_start, d.x | (j << 24), sp | (L << 10), d.y + j * d.z + sp);
+          const bool tail = sp >= ss.n_long;
+          const int first = tail ? ss.n_long * pps + (sp - ss.n_long) * kDecodeTailPages : sp * pps;
+          const int tokens = std::min(16 * (tail ? kDecodeTailPages : pps), L - 16 * first);
+          const int pages = (tokens + 15) / 16;
+          const int4 it = make_int4(q_start, d.x | (j << 24), first | ((tokens - 1) << 22), d.y + j * d.z + sp);
           if (pages == pps) ditems->push_back(it);
           else parts.push_back({pages, it});
         }
@@ -185,7 +204,7 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   decode_lists(s, b, 0, false, fill, &p->dreq, &p->ditems, &n_dreq, &n_items, &max_split);
   p->n_items_decode = (int)n_items;
   p->max_split = max_split;
-  size_t off = align_up(kCounterOffset + (size_t)layers * steps * sizeof(int32_t));
+  size_t off = align_up(kCounterOffset + (size_t)kDecodeCounterInts * sizeof(int32_t));
   p->off_meta = off;
   off = align_up(off + (size_t)b->num_reqs * sizeof(int4));
   p->off_pitems = off;
@@ -454,7 +473,7 @@ int check_call(duet_ctx* ctx, const duet_shape* shape, int layers, const void* c
       if (q.kind == DUET_KIND_PREFILL && L > kMaxPrefillKeys)
         return fail(DUET_EUNSUPPORTED, "request %d: prefill attends %lld keys, at most %d supported", r,
                     (long long)L, kMaxPrefillKeys);
-      if (q.kind == DUET_KIND_DECODE && (L + 15) / 16 > 1023LL * kDecodePagesPerSplit)
+      if (q.kind == DUET_KIND_DECODE && (L + 15) / 16 > kMaxDecodePages)
         return fail(DUET_EUNSUPPORTED, "request %d: decode context %lld too long", r, (long long)L);
     }
     if (n_dec > 65535) return fail(DUET_EUNSUPPORTED, "more than 65535 decode requests");
@@ -495,6 +514,7 @@ void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char
   w->pml = reinterpret_cast<float*>(ws + p.off_pml);
   w->ditems = reinterpret_cast<const int4*>(ws + p.off_ditems);
   w->err = reinterpret_cast<int32_t*>(ws);
+  w->work_counter = reinterpret_cast<int32_t*>(ws + kCounterOffset);
   w->n_ditems = (int)p.ditems.size();
   w->decode_cus = split.mode == DUET_SPLIT ? split.cus_decode : ctx->num_cus;
   w->n_pitems = (int)p.pitems.size();
@@ -563,7 +583,6 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
     const AttnArgs al = layer_args(l);
     if (has_decode) {
       WorkArgs wl = w;
-      wl.work_counter = reinterpret_cast<int32_t*>(ws + kCounterOffset) + l;
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l], sd));
       HIP_TRY(launch_decode_partial(al, wl, sd));
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 1], sd));
@@ -731,7 +750,6 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
     if (has_decode) HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
     if (has_prefill) HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
   }
-  int32_t* counters = reinterpret_cast<int32_t*>(ws + kCounterOffset);
   std::vector<DecodeLaunch> launches;
   // Appends decode step st's launches (every layer) to `launches`.
   auto add_step = [&](int st) {
@@ -754,7 +772,6 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
       dl.a.v_cache = vc_l[l];
       dl.a.out = st == 0 ? out_l[l] : out_ahead[x];
       dl.w = ws_w;
-      dl.w.work_counter = counters + (size_t)st * layers + l;
       dl.ap = AppendArgs{};
       if (st > 0) {
         dl.ap.k_cache = kc_l[l];
