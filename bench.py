@@ -380,7 +380,10 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The first time a run of split calls is queued several deep, the runtime settles for a few
+    # dozen steps (measured: the first 20-step back-to-back loop at 4480-4830 us per step, every
+    # later one at 4355), so the default warm-up queues 30 steps before the timed region.
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--layers", type=int, default=None,
                     help="attention layers per iteration (default 32 for the Llama-3-8B mixed batch, 1 otherwise)")
     ap.add_argument("--workload", choices=list(WORKLOADS), default="llama8b-mixed",
@@ -420,6 +423,10 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    # Every call runs on a created stream, as a serving loop's would: on the legacy default stream
+    # HIP ties each launch on the CU-masked streams to the work pending there (the next call's
+    # fork, the previous call's join), which costs a back-to-back split iteration about 10%.
+    torch.cuda.set_stream(torch.cuda.Stream())
     if args.trace:
         trace_main(args)
         return

@@ -22,6 +22,11 @@
  *     its streams, events, pinned staging buffers and latency-model tables.
  *   - GPU work is asynchronous to the host: it starts after the work already queued on the
  *     caller's `stream` and completes before work queued there later.
+ *   - Give spatially shared calls a created stream, not the legacy default stream (NULL): HIP
+ *     synchronises every launch on a blocking stream, the CU-masked ones included, with work
+ *     pending on the default stream, and back-to-back calls always leave some there (the next
+ *     call's fork and the previous call's join).  Measured on a 32-layer iteration: 4878 vs
+ *     4385 us per step.  Results do not depend on the stream.
  *
  * Tensor layouts (one layer)
  *   q, out    [T, h_q, d]                 tokens of all requests, packed in seq_meta order
