@@ -14,6 +14,15 @@ Paper, Section 4.2 and Algorithm 1:
   S_p = S - S_d, k in (floor(t_p / t_d), floor(t_p / t_d) + 1) and
   rho = (k T_decode + T_prefill) / max(k t_d, t_p); keep the first strictly larger rho.
 
+Full-model estimate (Section 4.1, "Token-Level Operators", "Overall Estimation"):
+  F_lin = 2 n d_i d_o,  B_lin = n d_i b + d_i d_o b + n d_o b  for n tokens through a d_i x d_o weight;
+  QKV and output projections d -> d, gate-up d -> m, down m -> d (as the paper states them);
+  t_tok = max(F_tok / Pi, B_tok / B_HBM) per operator, summed; t_block = t_tok + t_attn (one GPU:
+  no all-reduce); t_total = L t_block + t_cls with t_cls a linear operator d -> vocab_size.
+  Readings: RMSNorm F = 4 n d, B = 2 n d b + d b; SwiGLU activation F = 5 n m, B = 3 n m b;
+  residual add F = n d, B = 3 n d b; the classifier runs on one row per request; options give the
+  true GQA QKV width (h_q + 2 h_kv) d_h and a fused gate-up of width 2 m.
+
 Readings where the paper is silent (each also listed in the design notes):
   * CU shares are multiples of 8 (one CU per XCD), S_d runs 8, 16, ..., S - 8.
   * k = 0 is dropped: decode must make progress; k may be capped by the look-ahead depth.
@@ -116,6 +125,115 @@ def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, st
         base = math.floor(t_p / t_d) if t_d > 0 else 1
         # rho(k) rises up to k = base and falls from k = base + 1 on, so under a cap on the
         # decode steps the best allowed candidates are base and base + 1 clamped to the cap
+        cands = (base, base + 1) if kmax is None else tuple(sorted({min(base, kmax), min(base + 1, kmax)}))
+        for k in cands:
+            if k < 1:
+                continue
+            t = max(k * t_d, t_p)
+            rho = (k * t_decode_tokens + t_prefill_tokens) / t
+            if rho > best_rho:
+                best_rho, best = rho, dict(mode=SPLIT, s_p=s_p, s_d=s_d, k=k, rho=rho, t=t, flags=0)
+    if best is None:
+        return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=SLO_INFEASIBLE)
+    return best
+
+
+# ---- full-model estimate (token-level operators, Section 4.1) ---------------------------------
+
+@dataclass
+class Block:
+    """Dense dimensions of a transformer block: FFN width m and the classifier's vocabulary."""
+    ffn_dim: int
+    vocab_size: int = 0
+    gqa_qkv: bool = False      # QKV output width (h_q + 2 h_kv) d_h instead of the paper's d
+    fused_gate_up: bool = False  # gate-up output width 2 m instead of m
+
+
+def linear_cost(n, d_i, d_o, b):
+    """(F_lin, B_lin) of n tokens through a d_i x d_o linear operator."""
+    return 2.0 * n * d_i * d_o, n * d_i * b + d_i * d_o * b + n * d_o * b
+
+
+def rmsnorm_cost(n, d, b):
+    """Reading: square, sum, scale and weight per element; read x, write y, read the weight."""
+    return 4.0 * n * d, 2.0 * n * d * b + d * b
+
+
+def swiglu_cost(n, m, b):
+    """Reading: silu(gate) * up, about five operations per element; read gate and up, write."""
+    return 5.0 * n * m, 3.0 * n * m * b
+
+
+def add_cost(n, d, b):
+    """Residual add: one operation per element; read two tensors, write one."""
+    return 1.0 * n * d, 3.0 * n * d * b
+
+
+def token_ops(n, block, *, h_q, h_kv, d_h, b):
+    """(F, B) of each token-level operator of one layer for n tokens, in block order."""
+    d = h_q * d_h
+    m = block.ffn_dim
+    d_qkv = (h_q + 2 * h_kv) * d_h if block.gqa_qkv else d
+    m_gu = 2 * m if block.fused_gate_up else m
+    return [rmsnorm_cost(n, d, b), linear_cost(n, d, d_qkv, b), linear_cost(n, d, d, b), add_cost(n, d, b),
+            rmsnorm_cost(n, d, b), linear_cost(n, d, m_gu, b), swiglu_cost(n, m, b), linear_cost(n, m, d, b),
+            add_cost(n, d, b)]
+
+
+def t_tok(n, s, tables, block, *, h_q, h_kv, d_h, b):
+    """Seconds for one layer's token-level operators on n tokens and s CUs (none for n = 0)."""
+    if n == 0:
+        return 0.0
+    pi, bw = tables.pi(s), tables.b(s)
+    return sum(max(f / pi, by / bw) for f, by in token_ops(n, block, h_q=h_q, h_kv=h_kv, d_h=d_h, b=b))
+
+
+def t_cls(n_rows, s, tables, block, *, h_q, d_h, b):
+    """Seconds for the classifier (d -> vocab_size) on n_rows rows."""
+    if n_rows == 0 or block.vocab_size == 0:
+        return 0.0
+    f, by = linear_cost(n_rows, h_q * d_h, block.vocab_size, b)
+    return max(f / tables.pi(s), by / tables.b(s))
+
+
+def f_model(reqs, s, tables, block, *, h_q, h_kv, d_h, b, layers) -> float:
+    """t_total = L (t_tok + t_attn) + t_cls for the requests [(q, c), ...] on s CUs."""
+    n = sum(q for q, _ in reqs)
+    per_layer = t_tok(n, s, tables, block, h_q=h_q, h_kv=h_kv, d_h=d_h, b=b) + \
+        t_attn(reqs, s, tables, h_q, h_kv, d_h, b)
+    return layers * per_layer + t_cls(len(reqs), s, tables, block, h_q=h_q, d_h=d_h, b=b)
+
+
+def predict_model(batch, mode, s_p, s_d, k, tables, block, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS) -> float:
+    """Full-model iteration latency in seconds: aggregated, or max(k t_d(S_d), t_p(S_p)) where each
+    partition runs all layers for its own tokens."""
+    kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
+    if mode == AGG:
+        return f_model([(q, c) for _, q, c in batch], total, tables, block, **kw)
+    pre, dec = split_requests(batch)
+    t_d = f_model(dec, s_d, tables, block, **kw)
+    t_p = f_model(pre, s_p, tables, block, **kw)
+    return max(k * t_d, t_p)
+
+
+def choose_model(batch, tau, tables, block, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP,
+                 kmax=None):
+    """Algorithm 1 on the full-model estimate (same steps as choose)."""
+    kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
+    t_mixed = f_model([(q, c) for _, q, c in batch], total, tables, block, **kw)
+    if t_mixed <= tau:
+        return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=0)
+    pre, dec = split_requests(batch)
+    t_decode_tokens = len(dec)
+    t_prefill_tokens = sum(q for q, _ in pre)
+    best_rho, best = 0.0, None
+    for s_d in range(step, total, step):
+        t_d = f_model(dec, s_d, tables, block, **kw)
+        if t_d > tau:
+            continue
+        s_p = total - s_d
+        t_p = f_model(pre, s_p, tables, block, **kw)
+        base = math.floor(t_p / t_d) if t_d > 0 else 1
         cands = (base, base + 1) if kmax is None else tuple(sorted({min(base, kmax), min(base + 1, kmax)}))
         for k in cands:
             if k < 1:

@@ -1,0 +1,125 @@
+"""Pins of the oracle's full-model estimate (Section 4.1: token-level operators, overall
+estimation) against facts that do not come from its own formulas: operation and byte counts of
+an explicit matrix product, the published parameter counts of Llama-3-8B and -70B, the
+token-level property, and Algorithm 1 by brute force."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+from oracle import roofline as R
+
+LLAMA8B = dict(h_q=32, h_kv=8, d_h=128, layers=32, ffn=14336, vocab=128256)
+LLAMA70B = dict(h_q=64, h_kv=8, d_h=128, layers=80, ffn=28672, vocab=128256)
+
+
+@pytest.mark.parametrize("n,d_i,d_o,b,dt", [(3, 4, 5, 2, np.float16), (1, 7, 2, 4, np.float32), (5, 1, 3, 2, np.float16)])
+def test_linear_cost_counts_an_explicit_matmul(n, d_i, d_o, b, dt):
+    # operations: one multiply and one add per (token, input, output) triple, counted by looping
+    ops = 0
+    for _t, _o in itertools.product(range(n), range(d_o)):
+        for _i in range(d_i):
+            ops += 2
+    x, w, y = np.zeros((n, d_i), dt), np.zeros((d_i, d_o), dt), np.zeros((n, d_o), dt)
+    f, by = R.linear_cost(n, d_i, d_o, b)
+    assert f == ops
+    assert by == x.nbytes + w.nbytes + y.nbytes
+
+
+def _weights(shape, blk):
+    """Weight elements of one layer and of the classifier, read off the operators' byte terms at n = 0."""
+    b = 2
+    layer = sum(by for _f, by in R.token_ops(0, blk, h_q=shape["h_q"], h_kv=shape["h_kv"], d_h=shape["d_h"], b=b)) / b
+    d = shape["h_q"] * shape["d_h"]
+    cls = R.linear_cost(0, d, blk.vocab_size, b)[1] / b
+    return layer, cls, d
+
+
+@pytest.mark.parametrize("shape,published", [(LLAMA8B, 8_030_261_248), (LLAMA70B, 70_553_706_496)])
+def test_weight_terms_reproduce_published_parameter_counts(shape, published):
+    # with the real GQA QKV width and the fused gate-up, the operators' weight bytes are the
+    # model's parameters: L layers (four projections, two norm weights) + classifier; adding the
+    # embedding table (vocab x d) and the final norm (d) gives the published count exactly
+    blk = R.Block(ffn_dim=shape["ffn"], vocab_size=shape["vocab"], gqa_qkv=True, fused_gate_up=True)
+    layer, cls, d = _weights(shape, blk)
+    total = shape["layers"] * layer + cls + shape["vocab"] * d + d
+    assert total == published
+
+
+def test_paper_widths_undercount_qkv_and_gate_up_as_stated():
+    # as the paper states the widths (QKV d -> d, gate-up d -> m), a Llama-3-8B layer's
+    # projections hold d^2 + d^2 + d m + m d weights
+    s = LLAMA8B
+    layer, _cls, d = _weights(s, R.Block(ffn_dim=s["ffn"]))
+    assert layer == 2 * d * d + 2 * d * s["ffn"] + 2 * d
+
+
+def test_token_level_time_depends_on_total_tokens_only():
+    t = R.nominal_tables()
+    blk = R.Block(ffn_dim=14336, vocab_size=128256)
+    kw = dict(h_q=32, h_kv=8, d_h=128, b=2)
+    for n in (1, 64, 2048, 8192):
+        a = R.t_tok(n, 96, t, blk, **kw)
+        # the same n split any way among requests gives the same token-level time
+        reqs1 = [(n, 0)]
+        reqs2 = [(1, 5000)] * n if n <= 64 else [(n // 2, 0), (n - n // 2, 100)]
+        assert R.t_tok(sum(q for q, _ in reqs1), 96, t, blk, **kw) == a
+        assert R.t_tok(sum(q for q, _ in reqs2), 96, t, blk, **kw) == a
+    assert R.t_tok(0, 96, t, blk, **kw) == 0.0
+
+
+def test_total_is_linear_in_layers_plus_classifier():
+    t = R.nominal_tables()
+    blk = R.Block(ffn_dim=14336, vocab_size=128256)
+    reqs = [(2048, 0)] + [(1, 1000 + 37 * i) for i in range(64)]
+    kw = dict(h_q=32, h_kv=8, d_h=128, b=2)
+    one = R.f_model(reqs, 256, t, blk, layers=1, **kw)
+    two = R.f_model(reqs, 256, t, blk, layers=2, **kw)
+    cls = R.t_cls(len(reqs), 256, t, blk, h_q=32, d_h=128, b=2)
+    assert cls > 0
+    assert math.isclose(two - one, one - cls, rel_tol=1e-12)
+    # the attention-only estimate is the full one without token-level and classifier terms
+    att = R.f_roofline(reqs, 256, t, h_q=32, h_kv=8, d_h=128, b=2, layers=1)
+    assert math.isclose(one - cls - R.t_tok(sum(q for q, _ in reqs), 256, t, blk, **kw), att, rel_tol=1e-12)
+
+
+def test_decode_linear_layers_are_weight_bound_and_long_prefill_compute_bound():
+    # roofline regimes: 64 decode tokens read each weight once for little work (bytes dominate);
+    # 8192 prefill tokens reuse it thousands of times (FLOPs dominate)
+    t = R.nominal_tables()
+    for n, compute_bound in ((64, False), (8192, True)):
+        f, by = R.linear_cost(n, 4096, 4096, 2)
+        assert (f / t.pi(256) > by / t.b(256)) == compute_bound
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_choose_model_matches_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    t = R.nominal_tables()
+    blk = R.Block(ffn_dim=14336, vocab_size=128256)
+    kw = dict(h_q=32, h_kv=8, d_h=128, b=2, layers=32)
+    batch = [(0, int(rng.integers(256, 8192)), int(rng.integers(0, 20000)))] + \
+            [(1, 1, int(rng.integers(100, 30000))) for _ in range(int(rng.integers(8, 200)))]
+    t_agg = R.predict_model(batch, R.AGG, 256, 0, 1, t, blk, **kw)
+    for tau in (0.3 * t_agg, 0.6 * t_agg, 2 * t_agg):
+        got = R.choose_model(batch, tau, t, blk, **kw)
+        if t_agg <= tau:
+            assert got["mode"] == R.AGG
+            continue
+        pre, dec = R.split_requests(batch)
+        best = None
+        for s_d in range(8, 256, 8):
+            t_d = R.f_model(dec, s_d, t, blk, **kw)
+            if t_d > tau:
+                continue
+            t_p = R.f_model(pre, 256 - s_d, t, blk, **kw)
+            for k in range(1, 400):
+                rho = (k * len(dec) + sum(q for q, _ in pre)) / max(k * t_d, t_p)
+                if best is None or rho > best[0] * (1 + 1e-12):
+                    best = (rho, s_d, k)
+        if best is None:
+            assert got["mode"] == R.AGG and got["flags"] == R.SLO_INFEASIBLE
+        else:
+            assert got["mode"] == R.SPLIT
+            assert math.isclose(got["rho"], best[0], rel_tol=1e-9)
