@@ -196,6 +196,39 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
                          double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,
                          double* predicted_us, double* rho, int32_t* status_flags);
 
+/* ---- full-model estimate (Section 4.1: token-level operators, overall estimation) --------- */
+
+/* Dense dimensions of the transformer block around the attention layers. */
+typedef struct {
+  int32_t ffn_dim;     /* m: width of the gate-up output and of the down projection's input, >= 1 */
+  int32_t vocab_size;  /* classifier output width, >= 0 (0 leaves the classifier out) */
+  int32_t flags;       /* DUET_BLOCK_* bits */
+} duet_block_shape;
+#define DUET_BLOCK_GQA_QKV 1        /* QKV projection d -> (h_q + 2 h_kv) head_dim; the paper states d -> d */
+#define DUET_BLOCK_FUSED_GATE_UP 2  /* gate-up projection d -> 2 m; the paper states d -> m */
+
+/* Full-model iteration latency (Section 4.1, "Token-Level Operators" and "Overall Estimation"):
+ * t = num_layers (t_tok + t_attn) + t_cls.  t_attn is duet_predict_iter_latency's per-layer term.
+ * t_tok sums, over the token-level operators of one layer on the n tokens the requests process
+ * (n = sum of q_len), max(F / Pi(S), B / B(S)):
+ *   RMSNorm, QKV (d -> d), output (d -> d), residual add, RMSNorm, gate-up (d -> m), SwiGLU,
+ *   down (m -> d), residual add; d = num_q_heads * head_dim, b = element bytes;
+ *   linear d_i -> d_o: F = 2 n d_i d_o, B = (n d_i + d_i d_o + n d_o) b (Section 4.1);
+ *   the paper leaves the others open; read here as RMSNorm F = 4 n d, B = 2 n d b + d b;
+ *   SwiGLU F = 5 n m, B = 3 n m b; residual add F = n d, B = 3 n d b.
+ * t_cls is a linear operator d -> vocab_size on one row per request.  SPLIT: each partition runs
+ * every layer and the classifier for its own requests (reading the weights itself), with the
+ * same tables as duet_predict_iter_latency, and t = max(k t_decode(S_d), t_prefill(S_p)).  One
+ * GPU: no all-reduce term.  Host only; m may be NULL (nominal tables). */
+int duet_predict_model_latency(const duet_model* m, const duet_shape* shape, const duet_block_shape* block,
+                               const duet_batch* batch, duet_cu_split split, double* us);
+
+/* Algorithm 1 on the full-model estimate.  Arguments, results and flags as duet_choose_cu_split;
+ * T_decode and T_prefill, the tokens of rho, are unchanged. */
+int duet_choose_cu_split_model(const duet_model* m, const duet_shape* shape, const duet_block_shape* block,
+                               const duet_batch* batch, double tbt_slo_us, int32_t max_decode_steps,
+                               duet_cu_split* out, double* predicted_us, double* rho, int32_t* status_flags);
+
 /* ---- GPU context ----------------------------------------------------------------------------- */
 
 /* Context on HIP device `device`: checks for gfx950 and 256 CUs, creates the CU-masked stream

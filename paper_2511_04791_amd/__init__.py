@@ -165,6 +165,44 @@ def choose_cu_split(batch, tbt_slo_us: float, shape: AttnShape, model: Model | N
     return CuSplit(out.mode, out.cus_prefill, out.cus_decode, out.k_decode_steps), us.value, rho.value, flags.value
 
 
+BLOCK_GQA_QKV = 1
+BLOCK_FUSED_GATE_UP = 2
+
+
+@dataclass(frozen=True)
+class BlockShape:
+    """Dense dimensions of the block around the attention layers (duet_block_shape)."""
+    ffn_dim: int
+    vocab_size: int = 0
+    flags: int = 0
+
+    def to_c(self) -> N.BlockShape:
+        return N.BlockShape(int(self.ffn_dim), int(self.vocab_size), int(self.flags))
+
+
+def predict_model_latency(batch, cu_split: CuSplit, shape: AttnShape, block: BlockShape,
+                          model: Model | None = None) -> float:
+    """Full-model latency (us): token-level operators, attention and classifier (duet_predict_model_latency)."""
+    b = _BatchC(batch)
+    us = ctypes.c_double()
+    N.check(N.lib().duet_predict_model_latency(model.handle if model else None, ctypes.byref(_shape_c(shape)),
+                                               ctypes.byref(block.to_c()), ctypes.byref(b.c), cu_split.to_c(),
+                                               ctypes.byref(us)), "duet_predict_model_latency")
+    return us.value
+
+
+def choose_cu_split_model(batch, tbt_slo_us: float, shape: AttnShape, block: BlockShape, model: Model | None = None,
+                          max_decode_steps: int = 0):
+    """Algorithm 1 on the full-model estimate: (CuSplit, predicted_us, rho, status_flags)."""
+    b = _BatchC(batch)
+    out, us, rho, flags = N.CuSplit(), ctypes.c_double(), ctypes.c_double(), ctypes.c_int32()
+    N.check(N.lib().duet_choose_cu_split_model(model.handle if model else None, ctypes.byref(_shape_c(shape)),
+                                               ctypes.byref(block.to_c()), ctypes.byref(b.c), float(tbt_slo_us),
+                                               int(max_decode_steps), ctypes.byref(out), ctypes.byref(us),
+                                               ctypes.byref(rho), ctypes.byref(flags)), "duet_choose_cu_split_model")
+    return CuSplit(out.mode, out.cus_prefill, out.cus_decode, out.k_decode_steps), us.value, rho.value, flags.value
+
+
 def batch_work(batch, shape: AttnShape, kind: int = -1) -> tuple[float, float]:
     """The model's (FLOPs, bytes) for the requests of `kind` (-1 = all), shape.num_layers layers."""
     b = _BatchC(batch)

@@ -36,6 +36,10 @@ class CuSplit(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("cus_prefill", c_int32), ("cus_decode", c_int32), ("k_decode_steps", c_int32)]
 
 
+class BlockShape(ctypes.Structure):
+    _fields_ = [("ffn_dim", c_int32), ("vocab_size", c_int32), ("flags", c_int32)]
+
+
 class KernelTimes(ctypes.Structure):
     _fields_ = [("decode_partial_us", c_double), ("decode_reduce_us", c_double), ("prefill_us", c_double),
                 ("decode_total_us", c_double), ("iteration_us", c_double),
@@ -60,6 +64,9 @@ _SIGS = {
     "duet_predict_iter_latency": (c_int32, [c_void_p, P(Shape), P(Batch), CuSplit, P(c_double)]),
     "duet_choose_cu_split": (c_int32, [c_void_p, P(Shape), P(Batch), c_double, c_int32, P(CuSplit), P(c_double),
                                        P(c_double), P(c_int32)]),
+    "duet_predict_model_latency": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(Batch), CuSplit, P(c_double)]),
+    "duet_choose_cu_split_model": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(Batch), c_double, c_int32,
+                                             P(CuSplit), P(c_double), P(c_double), P(c_int32)]),
     "duet_init": (c_int32, [c_int32, P(c_void_p)]),
     "duet_destroy": (c_int32, [c_void_p]),
     "duet_ctx_model": (c_void_p, [c_void_p]),

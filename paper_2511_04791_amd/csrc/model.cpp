@@ -44,23 +44,57 @@ inline ReqCost request_cost(const duet_shape* s, const duet_seq_meta& r) {
 
 inline int cu_index(int cus) { return cus / DUET_CU_STEP - 1; }
 
-// Seconds for the attention of `num_layers` layers of the requests whose kind matches `kind`
-// (-1 = all) on `cus` CUs.  `shared`: the half runs while the other half runs on the other CUs,
-// so the spatial-sharing efficiencies apply.
+// Token-level operators of one layer on n tokens (Section 4.1): sum of max(F / pi, B / bw).
+double token_level(double n, const duet_shape* s, const duet_block_shape* blk, double pi, double bw) {
+  const double b = (s->dtype == DUET_BF16) ? 2.0 : 4.0;
+  const double hq = s->num_q_heads, hkv = s->num_kv_heads, dh = s->head_dim;
+  const double d = hq * dh, ffn = blk->ffn_dim;
+  const double d_qkv = (blk->flags & DUET_BLOCK_GQA_QKV) ? (hq + 2.0 * hkv) * dh : d;
+  const double d_gu = (blk->flags & DUET_BLOCK_FUSED_GATE_UP) ? 2.0 * ffn : ffn;
+  auto op = [&](double f, double by) { return std::fmax(f / pi, by / bw); };
+  auto linear = [&](double di, double dout) { return op(2.0 * n * di * dout, n * di * b + di * dout * b + n * dout * b); };
+  const double norm = op(4.0 * n * d, 2.0 * n * d * b + d * b);
+  const double add = op(1.0 * n * d, 3.0 * n * d * b);
+  double t = norm;
+  t += linear(d, d_qkv);
+  t += linear(d, d);
+  t += add;
+  t += norm;
+  t += linear(d, d_gu);
+  t += op(5.0 * n * ffn, 3.0 * n * ffn * b);
+  t += linear(ffn, d);
+  t += add;
+  return t;
+}
+
+// Seconds for `num_layers` layers of the requests whose kind matches `kind` (-1 = all) on `cus`
+// CUs: attention only (blk NULL), or the full model with its token-level operators and classifier.
+// `shared`: the half runs while the other half runs on the other CUs, so the spatial-sharing
+// efficiencies apply.
 double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b, int kind, int cus,
-                  bool shared = false) {
+                  bool shared = false, const duet_block_shape* blk = nullptr) {
   const int i = cu_index(cus);
   const bool tab = shared && m->has_shared;
   const double pi = (tab ? m->flops_shared[i] : m->flops[i]) * (shared ? m->prefill_eff : 1.0);
   const double bw = (tab ? m->bytes_shared[i] : m->bytes[i]) * (shared ? m->decode_eff : 1.0);
-  double t = 0.0;
+  double t = 0.0, n = 0.0;
+  int n_req = 0;
   for (int r = 0; r < b->num_reqs; ++r) {
     const duet_seq_meta& rq = b->reqs[r];
     if (kind >= 0 && rq.kind != kind) continue;
     const ReqCost rc = request_cost(s, rq);
     t += std::fmax(rc.flops / pi, rc.bytes / bw);
+    n += rq.q_len;
+    ++n_req;
   }
-  return s->num_layers * t;
+  if (!blk || n_req == 0) return s->num_layers * t;
+  double total = s->num_layers * (token_level(n, s, blk, pi, bw) + t);
+  if (blk->vocab_size > 0) {
+    const double el = (s->dtype == DUET_BF16) ? 2.0 : 4.0;
+    const double d = (double)s->num_q_heads * s->head_dim, v = blk->vocab_size, rows = n_req;
+    total += std::fmax(2.0 * rows * d * v / pi, (rows * d * el + d * v * el + rows * v * el) / bw);
+  }
+  return total;
 }
 
 bool has_both_kinds(const duet_batch* b) {
@@ -368,8 +402,18 @@ int duet_model_load(duet_model* m, const char* path) {
   return DUET_OK;
 }
 
-int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
-                              duet_cu_split split, double* us) {
+namespace {
+int check_block(const duet_block_shape* blk) {
+  if (!blk) return fail(DUET_EINVAL, "block is NULL");
+  if (blk->ffn_dim < 1) return fail(DUET_EINVAL, "ffn_dim %d must be >= 1", blk->ffn_dim);
+  if (blk->vocab_size < 0) return fail(DUET_EINVAL, "vocab_size %d must be >= 0", blk->vocab_size);
+  if (blk->flags & ~(DUET_BLOCK_GQA_QKV | DUET_BLOCK_FUSED_GATE_UP))
+    return fail(DUET_EINVAL, "unknown block flags 0x%x", (unsigned)blk->flags);
+  return DUET_OK;
+}
+
+int predict_impl(const duet_model* m, const duet_shape* shape, const duet_block_shape* blk, const duet_batch* batch,
+                 duet_cu_split split, double* us) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_batch(shape, batch, false))) return rc;
@@ -379,20 +423,20 @@ int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, cons
   const duet_model* mm = model_or_nominal(m, &nominal);
   double t;
   if (split.mode == DUET_AGG) {
-    t = f_roofline(mm, shape, batch, -1, DUET_TOTAL_CUS);
+    t = f_roofline(mm, shape, batch, -1, DUET_TOTAL_CUS, false, blk);
   } else {
     const bool shared = has_both_kinds(batch);
-    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, split.cus_decode, shared);
-    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, split.cus_prefill, shared);
+    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, split.cus_decode, shared, blk);
+    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, split.cus_prefill, shared, blk);
     t = std::fmax(split.k_decode_steps * td, tp);
   }
   *us = t * 1e6;
   return DUET_OK;
 }
 
-int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
-                         double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,
-                         double* predicted_us, double* rho, int32_t* status_flags) {
+int choose_impl(const duet_model* m, const duet_shape* shape, const duet_block_shape* blk, const duet_batch* batch,
+                double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out, double* predicted_us, double* rho,
+                int32_t* status_flags) {
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_batch(shape, batch, false))) return rc;
@@ -403,7 +447,7 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
   const double tau = tbt_slo_us * 1e-6;
   int32_t flags = mm->calibrated ? 0 : DUET_STATUS_UNCALIBRATED;
 
-  const double t_mixed = f_roofline(mm, shape, batch, -1, DUET_TOTAL_CUS);
+  const double t_mixed = f_roofline(mm, shape, batch, -1, DUET_TOTAL_CUS, false, blk);
   duet_cu_split agg{DUET_AGG, DUET_TOTAL_CUS, 0, 1};
   if (t_mixed <= tau) {
     *out = agg;
@@ -421,10 +465,10 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
   duet_cu_split best{-1, 0, 0, 0};
   const bool shared = has_both_kinds(batch);
   for (int sd = DUET_CU_STEP; sd < DUET_TOTAL_CUS; sd += DUET_CU_STEP) {
-    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, sd, shared);
+    const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, sd, shared, blk);
     if (td > tau) continue;
     const int sp = DUET_TOTAL_CUS - sd;
-    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, sp, shared);
+    const double tp = f_roofline(mm, shape, batch, DUET_KIND_PREFILL, sp, shared, blk);
     const double base = td > 0.0 ? std::floor(tp / td) : 1.0;
     // rho(k) rises up to k = base and falls from base + 1 on: under a cap on the decode steps
     // the candidates are clamped to it (the second is skipped when both clamp to the cap).
@@ -456,6 +500,35 @@ int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const due
   if (rho) *rho = best_rho;
   if (status_flags) *status_flags = flags;
   return DUET_OK;
+}
+
+}  // namespace
+
+int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                              duet_cu_split split, double* us) {
+  return predict_impl(m, shape, nullptr, batch, split, us);
+}
+
+int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                         double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,
+                         double* predicted_us, double* rho, int32_t* status_flags) {
+  return choose_impl(m, shape, nullptr, batch, tbt_slo_us, max_decode_steps, out, predicted_us, rho, status_flags);
+}
+
+int duet_predict_model_latency(const duet_model* m, const duet_shape* shape, const duet_block_shape* block,
+                               const duet_batch* batch, duet_cu_split split, double* us) {
+  clear_error();
+  const int rc = check_block(block);
+  return rc ? rc : predict_impl(m, shape, block, batch, split, us);
+}
+
+int duet_choose_cu_split_model(const duet_model* m, const duet_shape* shape, const duet_block_shape* block,
+                               const duet_batch* batch, double tbt_slo_us, int32_t max_decode_steps,
+                               duet_cu_split* out, double* predicted_us, double* rho, int32_t* status_flags) {
+  clear_error();
+  const int rc = check_block(block);
+  return rc ? rc : choose_impl(m, shape, block, batch, tbt_slo_us, max_decode_steps, out, predicted_us, rho,
+                               status_flags);
 }
 
 }  // extern "C"
