@@ -116,8 +116,10 @@ typedef struct {
   /* Filled by duet_last_kernel_times() when profiling is on, for the last duet_attn_mixed_batch
    * or duet_attn_iteration call, from HIP events on each kernel's own stream.  Per-kernel
    * durations are means over the call's layers. */
-  double decode_partial_us; /* split-K paged decode kernel, per launch */
-  double decode_reduce_us;  /* partial merge kernel, per launch */
+  double decode_partial_us; /* split-K paged decode kernel, per launch (with bf16 it includes the
+                               merge of the layer before, except in the first layer) */
+  double decode_reduce_us;  /* partial merge kernel, per launch (a bf16 call launches one, after
+                               its last layer) */
   double prefill_us;        /* prefill attention kernel, per launch */
   double decode_total_us;   /* decode half: first partial start to last reduce end (with AGG the
                                halves interleave on one stream, so the two spans overlap) */
@@ -240,9 +242,9 @@ int duet_destroy(duet_ctx* ctx);
 duet_model* duet_ctx_model(duet_ctx* ctx);
 
 /* Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
- * and batch: an error word, the decode work-queue counters, metadata, work lists and split-K
- * partials.  The layers of a call share all of it, so the size does not depend on
- * shape->num_layers.  Host only. */
+ * and batch: an error word, the decode work-queue counters, metadata, work lists and two
+ * buffers of split-K partials (consecutive layers alternate between them).  The layers of a call
+ * share all of it, so the size does not depend on shape->num_layers.  Host only. */
 int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
 
 /* One layer's attention over a mixed batch (Section 4.3: prefill and decode of one iteration
@@ -273,8 +275,10 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
  * num_layers device pointers, each laid out as in duet_attn_mixed_batch.  The work lists are
  * built and uploaded once; with SPLIT each half runs its kernels for every layer back to back on
  * its CU-masked stream (the host enqueues the halves layer by layer, alternating), with one fork
- * and one join per call; AGG runs layer by layer, decode then prefill, on `stream`.  Layer l's output is bit-identical
- * to duet_attn_mixed_batch on layer l's pointers. */
+ * and one join per call; AGG runs layer by layer, decode then prefill, on `stream`.  With bf16,
+ * layer l's decode split merge runs inside layer l + 1's decode kernel (one reduce kernel per call,
+ * after the last layer), so no layer's output is complete before the call returns.  Layer l's
+ * output is bit-identical to duet_attn_mixed_batch on layer l's pointers. */
 int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* const* q,
                         const void* const* k_cache, const void* const* v_cache, int64_t num_phys_pages,
                         const int32_t* page_table, int32_t max_pages_per_req, const duet_batch* batch,

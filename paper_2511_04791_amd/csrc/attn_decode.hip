@@ -16,7 +16,9 @@
 // buffers, so three pages are in flight while one is computed, across item boundaries too.
 // Online softmax keeps a reference max per head that only moves when a score exceeds it by
 // more than 2^8 (base-2 units), so the output rescale is rare.  Partials (unnormalised output,
-// reference max, denominator) go to the workspace and the reduce kernel merges the splits.
+// reference max, denominator) go to the workspace, and one wave per (request, query head) merges
+// the splits: the reduce kernel, or, for the layers of a call but the last, the next layer's bf16
+// partial kernel, in the waves whose item queue has run dry.
 // All arithmetic order depends on logical token positions only.
 #include <hip/hip_runtime.h>
 
@@ -132,6 +134,60 @@ __device__ __forceinline__ DItem unpack_item(i32x4 v, bool valid) {
   return d;
 }
 
+// Merges the splits of one (decode request, query head) pair, pair = request * h_q + head, with
+// one wave.  Lanes first take one split each to find the common max and the denominator, then take
+// one dim each to sum the weighted outputs.
+template <int D, typename OutT>
+__device__ __forceinline__ void merge_pair(const AttnArgs& a, const WorkArgs& w, const float* pacc, const float* pml,
+                                           void* out, int pair, int lane) {
+  constexpr int E = D / 64;
+  const int i = pair / a.h_q;
+  const int h = pair - i * a.h_q;
+  const int4 dr = w.dreq[i];
+  const int4 m = w.meta[dr.x];
+  const int g = a.group;
+  const int j = h / g, col = h - j * g;
+  const size_t base = (size_t)(dr.y + j * dr.z) * g + col;  // partial row of split 0
+  const int n = dr.z;
+  float M = -INFINITY;
+  for (int s = lane; s < n; s += 64) M = fmaxf(M, pml[(base + (size_t)s * g) * 2]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  float den = 0.f, num[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) num[e] = 0.f;
+  for (int s0 = 0; s0 < n; s0 += 64) {
+    const int s = s0 + lane;
+    const size_t row = base + (size_t)s * g;
+    const float wgt = s < n ? fast_exp2(pml[row * 2] - M) : 0.f;
+    den += s < n ? wgt * pml[row * 2 + 1] : 0.f;
+    const int cnt = min(64, n - s0);
+    // Eight partial rows are loaded before any is accumulated, so their loads overlap.
+    for (int t0 = 0; t0 < cnt; t0 += 8) {
+      float part[8][E];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = min(t0 + u, cnt - 1);
+        const float* pa = pacc + (base + (size_t)(s0 + t) * g) * D + lane;
+#pragma unroll
+        for (int e = 0; e < E; ++e) part[u][e] = pa[64 * e];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float wt = t0 + u < cnt ? __shfl(wgt, t0 + u) : 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) num[e] += wt * part[u][e];
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) den += __shfl_xor(den, off);
+  const float inv = 1.0f / den;
+  OutT* o = reinterpret_cast<OutT*>(out) + ((size_t)m.y * a.h_q + h) * D;
+#pragma unroll
+  for (int e = 0; e < E; ++e) o[lane + 64 * e] = static_cast<OutT>(num[e] * inv);
+}
+
 // Persistent: the grid holds as many waves as fit on the CUs the stream may use; each wave takes
 // one item by its index, then the next ones from a counter until the list is exhausted (every
 // wave reaches the exit).  Items are listed longest first.  Which wave computes an item never changes its arithmetic.
@@ -245,7 +301,29 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     return r;
   };
 
-  if (first >= n_items) return;
+  // The deferred merge of the layer before: once a wave's item queue is empty (the launch's
+  // tail, where waves would otherwise idle until the last items finish), it takes (request,
+  // query head) pairs from merge queue `queue`: ticket t is pair t n_queues + queue.  Every queue
+  // has a wave and every wave ends here, so every pair is merged.
+  auto merge_tail = [&]() {
+    if (w.n_merge == 0) return;
+    int* const mcounter = w.work_counter + (kDecodeQueues + queue) * kDecodeQueueStride;
+    for (;;) {
+      int t = 0;
+      if (lane == 0) t = atomicAdd(mcounter, 1);
+      const int pair = __builtin_amdgcn_readfirstlane(t) * n_queues + queue;
+      if (pair >= w.n_merge) break;
+      merge_pair<D, __bf16>(a, w, w.merge_pacc, w.merge_pml, w.merge_out, pair, lane);
+    }
+  };
+  // The counter set of the partial kernel before this one on the stream (it has finished).
+  if (w.clear_counter && blockIdx.x == 0 && threadIdx.x < kDecodeSetLines)
+    w.clear_counter[threadIdx.x * kDecodeQueueStride] = 0;
+
+  if (first >= n_items) {
+    merge_tail();
+    return;
+  }
   DItem cur = unpack_item(sload4(w.ditems + first), true);
   DItem nxt = unpack_item(sload4(w.ditems + min(first + n_waves, n_items - 1)), first + n_waves < n_items);
   int cur_ids;
@@ -386,6 +464,7 @@ __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_par
     for (int ks = 0; ks < D / 32; ++ks) qf[ks] = qn[ks];
   }
   if (bad && lane == 0) atomicOr(w.err, 1);
+  merge_tail();
 }
 
 // fp32 path (small shapes): one wave per item, lane = dim, scores reduced across the wave.
@@ -452,62 +531,15 @@ __global__ __launch_bounds__(256) void decode_partial_f32(AttnArgs a, WorkArgs w
   if (bad && lane == 0) atomicOr(w.err, 1);
 }
 
-// Merge the splits of one (decode request, query head): one wave.  Lanes first take one split
-// each to find the common max and the denominator, then take one dim each to sum the outputs.
+// Merges every (decode request, query head) pair of one layer: one wave per pair.
 template <int D, typename OutT>
 __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
-  constexpr int E = D / 64;
-  // The partial kernel before this one on the stream has finished with the queue counters: clear
-  // them for the next one.
-  if (blockIdx.x == 0 && threadIdx.x < kDecodeQueues) w.work_counter[threadIdx.x * kDecodeQueueStride] = 0;
-  const int lane = threadIdx.x & 63;
+  // The partial kernel before this one on the stream has finished with its counter set: clear it
+  // for the next call.
+  if (blockIdx.x == 0 && threadIdx.x < kDecodeSetLines) w.work_counter[threadIdx.x * kDecodeQueueStride] = 0;
   const int pair = blockIdx.x * 4 + uniform(threadIdx.x >> 6);
-  const int i = pair / a.h_q;
-  const int h = pair - i * a.h_q;
-  if (i >= w.n_dreq) return;
-  const int4 dr = w.dreq[i];
-  const int4 m = w.meta[dr.x];
-  const int g = a.group;
-  const int j = h / g, col = h - j * g;
-  const size_t base = (size_t)(dr.y + j * dr.z) * g + col;  // partial row of split 0
-  const int n = dr.z;
-  float M = -INFINITY;
-  for (int s = lane; s < n; s += 64) M = fmaxf(M, w.pml[(base + (size_t)s * g) * 2]);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  float den = 0.f, num[E];
-#pragma unroll
-  for (int e = 0; e < E; ++e) num[e] = 0.f;
-  for (int s0 = 0; s0 < n; s0 += 64) {
-    const int s = s0 + lane;
-    const size_t row = base + (size_t)s * g;
-    const float wgt = s < n ? fast_exp2(w.pml[row * 2] - M) : 0.f;
-    den += s < n ? wgt * w.pml[row * 2 + 1] : 0.f;
-    const int cnt = min(64, n - s0);
-    // Eight partial rows are loaded before any is accumulated, so their loads overlap.
-    for (int t0 = 0; t0 < cnt; t0 += 8) {
-      float part[8][E];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int t = min(t0 + u, cnt - 1);
-        const float* pa = w.pacc + (base + (size_t)(s0 + t) * g) * D + lane;
-#pragma unroll
-        for (int e = 0; e < E; ++e) part[u][e] = pa[64 * e];
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float wt = t0 + u < cnt ? __shfl(wgt, t0 + u) : 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) num[e] += wt * part[u][e];
-      }
-    }
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) den += __shfl_xor(den, off);
-  const float inv = 1.0f / den;
-  OutT* o = reinterpret_cast<OutT*>(a.out) + ((size_t)m.y * a.h_q + h) * D;
-#pragma unroll
-  for (int e = 0; e < E; ++e) o[lane + 64 * e] = static_cast<OutT>(num[e] * inv);
+  if (pair >= w.n_dreq * a.h_q) return;
+  merge_pair<D, OutT>(a, w, w.pacc, w.pml, a.out, pair, threadIdx.x & 63);
 }
 
 }  // namespace

@@ -30,7 +30,14 @@ struct WorkArgs {
   const int4* ditems;   // [ND] bf16 decode items in execution order: (q_start, req | kv head << 24,
                         //      first page | (tokens - 1) << 22, row of the item's partial)
   int32_t* err;         // error word: bit 0 = page id out of range
-  int32_t* work_counter;  // kDecodeCounterInts ints: the decode queues' next tickets (see kDecodeQueues)
+  int32_t* work_counter;  // kDecodeSetInts ints: this launch's counter set (see kDecodeQueues)
+  int32_t* clear_counter; // counter set a bf16 partial kernel clears when it starts, or null
+  // Deferred merge (bf16): the split-K partials of the layer before, merged by this partial
+  // kernel's waves once its item queue is empty.  n_merge = 0: nothing to merge.
+  const float* merge_pacc;
+  const float* merge_pml;
+  void* merge_out;        // that layer's output
+  int32_t n_merge;        // (decode request, query head) pairs
   int32_t n_pitems, n_dreq, max_split, n_ditems;
   int32_t pages_per_split;
   int32_t decode_cus;   // CUs the decode stream may use (sizes the persistent grid)
@@ -81,12 +88,16 @@ constexpr long long kMaxDecodePages = (1LL << 22) - 1;
 #endif
 // The persistent decode kernel's work queue is split into kDecodeQueues counters (items are dealt
 // round-robin to them), each on its own 128-byte line: atomics on one line are serialised, at a
-// few tens per microsecond.  Every decode launch of a call uses the same counters: the upload
-// zeroes them and each reduce kernel clears them once its partial kernel is done, before the
-// next partial kernel on the stream starts.
+// few tens per microsecond.  A counter set is kDecodeQueues item queues followed by kDecodeQueues
+// merge queues (the deferred merge of the layer before).  A call has two sets, which consecutive
+// layers alternate: the upload zeroes both, a partial kernel clears the set the kernel before it
+// on the stream used (that kernel has finished), and a reduce kernel clears the set of the
+// partial kernel it follows.
 constexpr int kDecodeQueues = DUET_DECODE_QUEUES;
 constexpr int kDecodeQueueStride = DUET_DECODE_QUEUE_STRIDE;
-constexpr int kDecodeCounterInts = kDecodeQueues * kDecodeQueueStride;
+constexpr int kDecodeSetLines = 2 * kDecodeQueues;
+constexpr int kDecodeSetInts = kDecodeSetLines * kDecodeQueueStride;
+constexpr int kDecodeCounterInts = 2 * kDecodeSetInts;
 
 // Keys a prefill request may attend (its page ids are staged in LDS: 8192 ids, 32 KB).
 constexpr int kMaxPrefillKeys = 131072;

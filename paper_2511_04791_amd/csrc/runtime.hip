@@ -72,8 +72,10 @@ struct Plan {
   std::vector<StepPlan> ahead;  // look-ahead decode steps 1 .. steps - 1
   int steps = 1;
   int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0, prefill_id_cap = 0;
-  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, off_pacc = 0, off_pml = 0, upload_bytes = 0,
-         total = 0;
+  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, upload_bytes = 0, total = 0;
+  // Two buffers of split-K partials: consecutive layers of a call alternate between them, so a
+  // layer's partials survive until the next layer's decode kernel has merged them.
+  size_t off_pacc[2] = {0, 0}, off_pml[2] = {0, 0};
 };
 
 // Fixed per dtype, never per split or placement, so results are identical for every CU split.
@@ -240,10 +242,12 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
     off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)ni * sizeof(int4) : 0));
   }
   p->upload_bytes = off;
-  p->off_pacc = off;
-  off = align_up(off + (size_t)max_items * g * s->head_dim * sizeof(float));
-  p->off_pml = off;
-  off = align_up(off + (size_t)max_items * g * 2 * sizeof(float));
+  for (int b = 0; b < 2; ++b) {
+    p->off_pacc[b] = off;
+    off = align_up(off + (size_t)max_items * g * s->head_dim * sizeof(float));
+    p->off_pml[b] = off;
+    off = align_up(off + (size_t)max_items * g * 2 * sizeof(float));
+  }
   p->total = off;
 }
 
@@ -284,7 +288,8 @@ void append_key(std::vector<uint64_t>* k, const DecodeLaunch& l) {
                         bits(a.out), bits(a.num_phys_pages), bits(a.max_pages), bits(a.h_q), bits(a.h_kv),
                         bits(a.group), bits(a.head_dim), bits(a.dtype), bits(a.scale_log2), bits(w.meta),
                         bits(w.pitems), bits(w.dreq), bits(w.pacc), bits(w.pml), bits(w.ditems), bits(w.err),
-                        bits(w.work_counter), bits(w.n_pitems), bits(w.n_dreq), bits(w.max_split),
+                        bits(w.work_counter), bits(w.clear_counter), bits(w.merge_pacc), bits(w.merge_pml),
+                        bits(w.merge_out), bits(w.n_merge), bits(w.n_pitems), bits(w.n_dreq), bits(w.max_split),
                         bits(w.n_ditems), bits(w.pages_per_split), bits(w.decode_cus), bits(w.prefill_id_cap),
                         bits(p.k_cache), bits(p.v_cache), bits(p.k_new), bits(p.v_new), bits(p.page_table),
                         bits(p.num_phys_pages), bits(p.max_pages), bits(p.h_kv), bits(p.head_dim), bits(p.dtype)};
@@ -322,6 +327,7 @@ struct duet_ctx {
   int profiling = 0;  // 0 off, 1 iteration events only, 2 also per-kernel events
   bool prof_valid = false;
   bool prof_decode = false, prof_prefill = false, prof_kernels = false;
+  bool prof_deferred = false;  // only the last layer of the profiled call launched a reduce kernel
   int prof_layers = 0;
   // Per-layer kernel brackets of a profiled call: decode layer l uses events 3l (before the
   // partial kernel), 3l+1 (between partial and reduce) and 3l+2 (after the reduce); prefill
@@ -510,8 +516,8 @@ void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char
   w->meta = reinterpret_cast<const int4*>(ws + p.off_meta);
   w->pitems = reinterpret_cast<const int4*>(ws + p.off_pitems);
   w->dreq = reinterpret_cast<const int4*>(ws + p.off_dreq);
-  w->pacc = reinterpret_cast<float*>(ws + p.off_pacc);
-  w->pml = reinterpret_cast<float*>(ws + p.off_pml);
+  w->pacc = reinterpret_cast<float*>(ws + p.off_pacc[0]);
+  w->pml = reinterpret_cast<float*>(ws + p.off_pml[0]);
   w->ditems = reinterpret_cast<const int4*>(ws + p.off_ditems);
   w->err = reinterpret_cast<int32_t*>(ws);
   w->work_counter = reinterpret_cast<int32_t*>(ws + kCounterOffset);
@@ -579,15 +585,35 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
     if (has_decode) HIP_TRY(hipStreamWaitEvent(sd, ctx->ev_fork, 0));
     if (has_prefill) HIP_TRY(hipStreamWaitEvent(sp, ctx->ev_fork, 0));
   }
+  // bf16 decode defers each layer's split merge into the next layer's partial kernel, whose waves
+  // merge once their item queue is empty; partial buffers and counter sets alternate by layer,
+  // and one reduce kernel merges the last layer.  The fp32 path merges every layer in its own
+  // reduce kernel.
+  const bool defer = has_decode && shape->dtype == DUET_BF16;
   for (int l = 0; l < layers; ++l) {
     const AttnArgs al = layer_args(l);
     if (has_decode) {
       WorkArgs wl = w;
+      if (defer) {
+        const int cur = l & 1, prev = cur ^ 1;
+        wl.pacc = reinterpret_cast<float*>(ws + p.off_pacc[cur]);
+        wl.pml = reinterpret_cast<float*>(ws + p.off_pml[cur]);
+        wl.work_counter = w.work_counter + cur * kDecodeSetInts;
+        wl.clear_counter = w.work_counter + prev * kDecodeSetInts;
+        if (l > 0) {
+          wl.merge_pacc = reinterpret_cast<const float*>(ws + p.off_pacc[prev]);
+          wl.merge_pml = reinterpret_cast<const float*>(ws + p.off_pml[prev]);
+          wl.merge_out = out_l[l - 1];
+          wl.n_merge = w.n_dreq * a.h_q;
+        }
+      }
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l], sd));
       HIP_TRY(launch_decode_partial(al, wl, sd));
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 1], sd));
-      HIP_TRY(launch_decode_reduce(al, wl, sd));
-      if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 2], sd));
+      if (!defer || l == layers - 1) {
+        HIP_TRY(launch_decode_reduce(al, wl, sd));
+        if (prof) HIP_TRY(hipEventRecord(ctx->ev_dec[3 * l + 2], sd));
+      }
     }
     if (has_prefill) {
       if (prof) HIP_TRY(hipEventRecord(ctx->ev_pre[2 * l], sp));
@@ -604,6 +630,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
   ctx->prof_valid = prof_iter;
   ctx->prof_kernels = prof;
+  ctx->prof_deferred = defer;
   ctx->prof_decode = has_decode;
   ctx->prof_prefill = has_prefill;
   ctx->prof_layers = layers;
@@ -841,6 +868,7 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
   if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
   ctx->prof_valid = prof_iter;
   ctx->prof_kernels = prof;
+  ctx->prof_deferred = false;
   ctx->prof_decode = has_decode;
   ctx->prof_prefill = has_prefill;
   ctx->prof_layers = layers;
@@ -1092,11 +1120,15 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
   }
   if (ctx->prof_kernels && ctx->prof_decode) {
     const std::vector<hipEvent_t>& e = ctx->ev_dec;
+    // Layers whose merge was deferred into the next layer's partial kernel launched no reduce.
+    const int first_red = ctx->prof_deferred ? L - 1 : 0;
     for (int l = 0; l < L; ++l) {
       double part = 0.0, red = 0.0;
-      if ((rc = span_us(e[3 * l], e[3 * l + 1], &part)) || (rc = span_us(e[3 * l + 1], e[3 * l + 2], &red))) return rc;
+      if ((rc = span_us(e[3 * l], e[3 * l + 1], &part))) return rc;
       out->decode_partial_us += part / L;
-      out->decode_reduce_us += red / L;
+      if (l < first_red) continue;
+      if ((rc = span_us(e[3 * l + 1], e[3 * l + 2], &red))) return rc;
+      out->decode_reduce_us += red / (L - first_red);
     }
     if ((rc = span_us(e[0], e[3 * L - 1], &out->decode_total_us)) ||
         (rc = span_us(ctx->prof[kEvFork], e[0], &out->decode_start_us)))

@@ -213,6 +213,32 @@ def test_iteration_layers_match_single_layer_calls(ctx, dtype):
         assert mx <= BF16_MAX_ABS and mean <= BF16_MEAN_ABS
 
 
+def test_iteration_deferred_merge_many_decodes(ctx):
+    """bf16 layers of a call merge the layer before inside their own decode kernel.  With many
+    decode requests (merge tickets on every queue), four layers, three decode shares and each call
+    made twice in a row (the counter sets must be left cleared), every layer equals its
+    single-layer call bit for bit."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    rng = np.random.default_rng(79)
+    reqs = [(0, 130, 0)] + [(1, 1, int(c)) for c in rng.integers(16, 3000, 48)]
+    b = wl.make_batch(wl.LLAMA3_8B, reqs, page_seed=78)
+    L = 4
+    layers = [_case(b, seed=3400 + l, gen_device="cpu") for l in range(L)]
+    qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
+    pt = layers[0][3]
+    singles = [_run(ctx, b, *layers[l]) for l in range(L)]
+    for sp in (duet.CuSplit.agg(), duet.CuSplit.split(96, 160), duet.CuSplit.split(232, 24)):
+        for rep in range(2):
+            outs = ctx.attn_iteration(qs, kcs, vcs, pt, b.seq_meta, sp, check_errors=True)
+            torch.cuda.synchronize()
+            for l in range(L):
+                assert torch.equal(outs[l], singles[l]), f"layer {l} {sp} call {rep}"
+    mx, mean = errors(singles[L - 1], oracle_out(b, qs[L - 1], kcs[L - 1], vcs[L - 1]))
+    _report("deferred merge, last layer", mx, mean)
+    assert mx <= BF16_MAX_ABS and mean <= BF16_MEAN_ABS
+
+
 def test_concurrent_control_mode_matches_aggregated(ctx):
     """The unpartitioned two-stream control computes the same bits as aggregated execution."""
     import paper_2511_04791_amd as duet
