@@ -376,6 +376,92 @@ def lookahead_main(args):
     print(json.dumps(line), flush=True)
     ctx.close()
 
+def block_main(args):
+    """Whole transformer blocks (Section 4.1: the token-level operators around attention) on the
+    Llama-3-8B mixed batch: --layers (default 32) blocks of random-init bf16 weights (d 4096,
+    32/8 heads, FFN 14336); one step is one duet_block_forward call over the 2048-token chunk
+    and the 64 decodes.  Aggregated execution, the full-model estimate's choice of Algorithm 1,
+    and spatial splits in steps of 32 CUs, each with the full-model estimate beside it."""
+    import dataclasses
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from paper_2511_04791_amd.calibration import calibrate_model
+
+    L = args.layers if args.layers is not None else 32
+    ffn = 14336
+    batch = wl.llama8b_mixed()
+    ctx = duet.Context(0)
+    if not args.no_calibrate:
+        calibrate_model(ctx, shape=batch.shape, batch=batch)
+    x, weights, caches = wl.make_block_tensors(batch, ffn, L, seed=5005, device="cuda")
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    del caches
+    pt = torch.as_tensor(batch.page_table, device="cuda")
+    meta = batch.seq_meta
+    rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
+    shape = dataclasses.replace(batch.shape, num_layers=L)
+    block = duet.BlockShape(ffn, 0, duet.BLOCK_GQA_QKV | duet.BLOCK_FUSED_GATE_UP)
+    ws = ctx.workspace(duet.block_workspace_bytes(shape, block, meta))
+    st = torch.cuda.current_stream()
+
+    def run(sp, steps):
+        for _ in range(steps):
+            ctx.block_forward(x, weights, kcs, vcs, pt, meta, ffn, sp, workspace=ws)
+
+    def timed(sp):
+        run(sp, args.warmup)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        run(sp, args.steps)
+        e1.record(st)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        # one synchronous profiled call: when the decode tokens are ready (fork to the decode
+        # partition's end; the whole call under AGG)
+        ctx.set_profiling(1)
+        run(sp, 1)
+        t = ctx.last_kernel_times()
+        ctx.set_profiling(0)
+        ready = t["decode_start_us"] + t["decode_total_us"] if sp.mode == duet.SPLIT else t["iteration_us"]
+        return us, ready
+
+    ctx.block_forward(x, weights, kcs, vcs, pt, meta, ffn, duet.CuSplit.agg(), workspace=ws, check_errors=True)
+    d = shape.num_q_heads * shape.head_dim
+    n_params = d * (shape.num_q_heads + 2 * shape.num_kv_heads) * shape.head_dim + d * d + 3 * d * ffn
+    flops = L * (2.0 * batch.num_tokens * n_params + prefill_causal_flops(batch))
+    agg_pred = duet.predict_model_latency(rows3, duet.CuSplit.agg(), shape, block, ctx.model)
+    tau = args.tbt_slo_us if args.tbt_slo_us is not None else 0.99 * agg_pred
+    chosen, pred, rho, flags = duet.choose_cu_split_model(rows3, tau, shape, block, ctx.model, max_decode_steps=1)
+    rows = []
+    agg_us, agg_ready = timed(duet.CuSplit.agg())
+    rows.append({"mode": "AGG", "us": round(agg_us, 1), "decode_ready_us": round(agg_ready, 1),
+                 "predicted_us": round(agg_pred, 1)})
+    splits = [(sp_, 256 - sp_) for sp_ in range(32, 256, 32)]
+    if chosen.mode == duet.SPLIT and (chosen.cus_prefill, chosen.cus_decode) not in splits:
+        splits.append((chosen.cus_prefill, chosen.cus_decode))
+    for s_p, s_d in splits:
+        sp = duet.CuSplit.split(s_p, s_d)
+        us, ready = timed(sp)
+        rows.append({"mode": f"SPLIT({s_p},{s_d})", "us": round(us, 1), "decode_ready_us": round(ready, 1),
+                     "predicted_us": round(duet.predict_model_latency(rows3, sp, shape, block, ctx.model), 1)})
+    chosen_row = next((r for r in rows if chosen.mode == duet.SPLIT and
+                       r["mode"] == f"SPLIT({chosen.cus_prefill},{chosen.cus_decode})"), rows[0])
+    best = min(rows, key=lambda r: r["us"])
+    print(json.dumps({
+        "metric": "transformer-block iteration latency (us)", "value": chosen_row["us"], "unit": "us", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"llama3-8b, {L} transformer blocks (random-init weights, FFN {ffn}): 1 prefill chunk "
+                               "of 2048 tokens at prefix 0 + 64 decodes (context U[512,4096]), page 16",
+                   "layers": L},
+        "chosen": chosen_row["mode"], "tbt_slo_us": round(tau, 1), "agg_us": round(agg_us, 1),
+        "speedup_vs_agg": round(agg_us / chosen_row["us"], 4), "best": best["mode"],
+        "decode_ready_us": chosen_row["decode_ready_us"], "agg_decode_ready_us": round(agg_ready, 1),
+        "decode_ready_speedup": round(agg_ready / chosen_row["decode_ready_us"], 3),
+        "agg_tflops": round(flops / agg_us / 1e6, 1), "rows": rows}))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -408,6 +494,9 @@ def main():
                     help="run look-ahead decode (k decode steps per prefill step) on the prefill-heavy Llama-3-70B "
                          "batch instead")
     ap.add_argument("--max-k", type=int, default=64, help="cap on Algorithm 1's k for --lookahead")
+    ap.add_argument("--block", action="store_true",
+                    help="run whole transformer blocks (token-level operators around attention) on the Llama-3-8B "
+                         "mixed batch instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path; "
@@ -432,6 +521,9 @@ def main():
         return
     if args.lookahead:
         lookahead_main(args)
+        return
+    if args.block:
+        block_main(args)
         return
     L = args.layers if args.layers is not None else (32 if args.workload == "llama8b-mixed" else 1)
     if args.workload == "decode-heavy" and L != 1:

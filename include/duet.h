@@ -285,6 +285,50 @@ int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* cons
                         duet_cu_split split, void* workspace, size_t workspace_bytes, void* const* out,
                         void* stream);
 
+/* ---- the whole block (Section 4.1, token-level operators) --------------------------------------
+ *
+ * L transformer blocks over a mixed batch, each partition running its own tokens through every
+ * operator on its CUs (Section 4.3: the decode and prefill partitions each run the model for
+ * their requests).  Per layer: h = RMSNorm(x) g_attn; qkv = h W_qkv; the query columns go to
+ * attention and the new tokens' key and value columns are written into the paged cache (token t
+ * of a request with c cached tokens at position c + t); a = attention (the kernels above);
+ * x += a W_o; h = RMSNorm(x) g_ffn; [g | u] = h W_gate_up; x += (silu(g) * u) W_down.  RMSNorm
+ * is x / sqrt(mean(x^2) + eps); silu(g) = g / (1 + exp(-g)).  bf16 tensors, fp32 arithmetic
+ * inside each operator, bf16 between operators; the projections run on hipBLASLt. */
+typedef struct {
+  const void* attn_norm; /* [d] (d = h_q * head_dim) */
+  const void* w_qkv;     /* [d, (h_q + 2 h_kv) head_dim] row-major: query, key, value columns */
+  const void* w_o;       /* [d, d] */
+  const void* ffn_norm;  /* [d] */
+  const void* w_gate_up; /* [d, 2 ffn_dim]: gate columns 0 .. ffn_dim - 1, then up */
+  const void* w_down;    /* [ffn_dim, d] */
+} duet_block_weights;
+
+/* Workspace of duet_block_forward: duet_workspace_bytes' layout, the activations of every
+ * scheduled token ([T, d] x4, [T, (h_q + 2 h_kv) head_dim], [T, 2 ffn_dim], [T, ffn_dim], bf16)
+ * and two hipBLASLt workspaces.  Host only. */
+int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
+                               size_t* bytes);
+
+/* Runs shape->num_layers blocks in place on the residual stream x [T, d] (bf16, rows packed per
+ * request in batch order).  weights, k_cache and v_cache are host arrays of num_layers entries
+ * (device pointers; caches laid out as in duet_attn_mixed_batch); every scheduled token's key and
+ * value rows are written to its layer's cache.  block->flags must be DUET_BLOCK_GQA_QKV |
+ * DUET_BLOCK_FUSED_GATE_UP (the layout above); ffn_dim and d are multiples of 8; bf16 only;
+ * norm_eps > 0.  AGG runs everything on `stream`; SPLIT runs the decode requests' rows on the
+ * decode CUs and the prefill requests' rows on the prefill CUs, each partition all layers back
+ * to back, and needs each kind's rows to be one contiguous range (DUET_EUNSUPPORTED otherwise).
+ * Requests must not share cache pages.  A page id outside [0, num_phys_pages) met while writing
+ * or reading the cache is not dereferenced and sets the error word.  Stream, ownership and
+ * validation rules as for duet_attn_iteration.  With profiling on, duet_last_kernel_times()
+ * reports iteration_us (fork to join) and, under a split, decode_total_us / decode_start_us (the
+ * decode partition: its tokens are ready at its end) and prefill_total_us / prefill_start_us. */
+int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* block,
+                       const duet_block_weights* weights, float norm_eps, void* x, void* const* k_cache,
+                       void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                       int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 /* ---- look-ahead decode (Section 4.3, interruption-free dispatch) -------------------------------
  *
  * Decode requests get KV slots for k future steps ahead of time, and the k decode steps run back

@@ -220,6 +220,18 @@ def workspace_bytes(shape: AttnShape, seq_meta) -> int:
     return n.value
 
 
+def block_workspace_bytes(shape: AttnShape, block: BlockShape, seq_meta) -> int:
+    """Device workspace of duet_block_forward for this batch."""
+    b = _BatchC(seq_meta)
+    n = ctypes.c_size_t()
+    N.check(N.lib().duet_block_workspace_bytes(ctypes.byref(_shape_c(shape)), ctypes.byref(block.to_c()),
+                                               ctypes.byref(b.c), ctypes.byref(n)), "duet_block_workspace_bytes")
+    return n.value
+
+
+BLOCK_WEIGHT_NAMES = ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")
+
+
 def lookahead_workspace_bytes(shape: AttnShape, seq_meta, k_decode_steps: int) -> int:
     b = _BatchC(seq_meta)
     n = ctypes.c_size_t()
@@ -312,6 +324,51 @@ class Context:
             N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
                     "duet_check_device_error")
         return out
+
+    def block_forward(self, x, weights, k_caches, v_caches, page_table, seq_meta, ffn_dim: int,
+                      cu_split: CuSplit = CuSplit.agg(), *, norm_eps: float = 1e-5, workspace=None, stream=None,
+                      check_errors: bool = False):
+        """len(weights) transformer blocks in place on the residual stream x [T, h_q d] (duet_block_forward).
+        weights: per-layer dicts of contiguous bf16 device tensors named as BLOCK_WEIGHT_NAMES; the caches
+        receive every scheduled token's keys and values.  Returns x."""
+        import torch
+        L = len(weights)
+        if L < 1 or len(k_caches) != L or len(v_caches) != L:
+            raise ValueError("weights, k_caches and v_caches must be non-empty lists of equal length")
+        b = _BatchC(seq_meta)
+        n_tok = int(b.rows[:, 2].sum()) if len(b.rows) else 0
+        kc0 = k_caches[0]
+        shape = AttnShape(int(x.shape[1]) // int(kc0.shape[3]), int(kc0.shape[1]), int(kc0.shape[3]), "bf16",
+                          int(kc0.shape[2]), L)
+        if x.dtype != torch.bfloat16 or not x.is_cuda or not x.is_contiguous() or x.dim() != 2 or x.shape[0] != n_tok:
+            raise ValueError(f"x must be a contiguous bf16 device tensor [{n_tok}, d]")
+        if page_table.dtype != torch.int32 or not page_table.is_cuda or not page_table.is_contiguous():
+            raise ValueError("page_table must be a contiguous int32 device tensor")
+        d, dh = int(x.shape[1]), shape.head_dim
+        d_qkv = (shape.num_q_heads + 2 * shape.num_kv_heads) * dh
+        want = {"attn_norm": (d,), "w_qkv": (d, d_qkv), "w_o": (d, d), "ffn_norm": (d,), "w_gate_up": (d, 2 * ffn_dim),
+                "w_down": (ffn_dim, d)}
+        for l, w in enumerate(weights):
+            for name in BLOCK_WEIGHT_NAMES:
+                t = w[name]
+                if tuple(t.shape) != want[name] or t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+                    raise ValueError(f"layer {l}: {name} must be a contiguous bf16 device tensor {want[name]}")
+            self._check_layer(x.view(n_tok, shape.num_q_heads, dh), k_caches[l], v_caches[l], page_table, b)
+        block = BlockShape(int(ffn_dim), 0, BLOCK_GQA_QKV | BLOCK_FUSED_GATE_UP)
+        need = block_workspace_bytes(shape, block, b.rows)
+        ws = self.workspace(need) if workspace is None else workspace
+        wts = (N.BlockWeights * L)(*[N.BlockWeights(*[w[n].data_ptr() for n in BLOCK_WEIGHT_NAMES]) for w in weights])
+        arr = lambda ts: (ctypes.c_void_p * L)(*[t.data_ptr() for t in ts])
+        st = torch.cuda.current_stream(x.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_block_forward(self.handle, ctypes.byref(_shape_c(shape)), ctypes.byref(block.to_c()), wts,
+                                           float(norm_eps), x.data_ptr(), arr(k_caches), arr(v_caches),
+                                           int(kc0.shape[0]), page_table.data_ptr(), int(page_table.shape[1]),
+                                           ctypes.byref(b.c), cu_split.to_c(), ws.data_ptr(), ws.numel(),
+                                           ctypes.c_void_p(st)), "duet_block_forward")
+        if check_errors:
+            N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
+                    "duet_check_device_error")
+        return x
 
     def attn_iteration(self, qs, k_caches, v_caches, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
                        outs=None, workspace=None, stream=None, check_errors: bool = False):

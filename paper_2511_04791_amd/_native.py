@@ -40,6 +40,11 @@ class BlockShape(ctypes.Structure):
     _fields_ = [("ffn_dim", c_int32), ("vocab_size", c_int32), ("flags", c_int32)]
 
 
+class BlockWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", c_void_p), ("w_qkv", c_void_p), ("w_o", c_void_p), ("ffn_norm", c_void_p),
+                ("w_gate_up", c_void_p), ("w_down", c_void_p)]
+
+
 class KernelTimes(ctypes.Structure):
     _fields_ = [("decode_partial_us", c_double), ("decode_reduce_us", c_double), ("prefill_us", c_double),
                 ("decode_total_us", c_double), ("iteration_us", c_double),
@@ -71,6 +76,10 @@ _SIGS = {
     "duet_destroy": (c_int32, [c_void_p]),
     "duet_ctx_model": (c_void_p, [c_void_p]),
     "duet_workspace_bytes": (c_int32, [P(Shape), P(Batch), P(c_size_t)]),
+    "duet_block_workspace_bytes": (c_int32, [P(Shape), P(BlockShape), P(Batch), P(c_size_t)]),
+    "duet_block_forward": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(BlockWeights), ctypes.c_float, c_void_p,
+                                     P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,
+                                     c_void_p, c_size_t, c_void_p]),
     "duet_attn_mixed_batch": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),
     "duet_attn_iteration": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p,

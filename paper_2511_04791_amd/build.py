@@ -15,6 +15,7 @@ OBJDIR = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libduet.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ROCM_LIB = "/opt/rocm/lib"
 ARCH = "gfx950"
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall",
              # no packed-fp32 instructions anywhere in the device code
@@ -53,7 +54,8 @@ def build(verbose: bool = False) -> str:
                 print(r.stderr)
     objs = [j[-1] for j in jobs]
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *objs])
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *objs, "-L" + ROCM_LIB, "-lhipblaslt",
+          "-Wl,-rpath," + ROCM_LIB])
     os.replace(tmp, LIB)
     return LIB
 

@@ -211,7 +211,6 @@ template <int D, int PPS>
 __global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
   constexpr int R = kRing;
   static_assert(PPS % R == 0, "a split must hold whole groups of ring pages");
-  constexpr size_t kSlabBytes = 16 * D * 2;  // one (page, kv head) slab of K or V
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, quad = lane >> 4;
   const int g = a.group;

@@ -110,6 +110,24 @@ constexpr int kPrefillKeys = 64;   // keys per LDS stage (4 pages)
 int prefill_heads_per_unit(int group);
 int prefill_rows_per_unit(int group, int dtype);
 
+// The QKV-split step of a block (bf16): query rows out, new keys and values into the cache.
+struct QkvSplitArgs {
+  const __bf16* qkv;       // [T, (h_q + 2 h_kv) d] projection output
+  __bf16* q;               // [T, h_q, d]
+  __bf16* k_cache;         // [P, h_kv, 16, d]
+  __bf16* v_cache;         // [P, h_kv, d, 16]
+  const int4* meta;        // [R] (kind, q_start, q_len, cached_len), q_start rising
+  const int32_t* page_table;
+  long long num_phys_pages;
+  int32_t* err;
+  int32_t num_reqs, max_pages, h_q, h_kv, head_dim;
+  int32_t row0;            // first row of the launch
+};
+
+hipError_t launch_rmsnorm(const __bf16* x, const __bf16* w, __bf16* y, int rows, int d, float eps, hipStream_t s);
+hipError_t launch_swiglu(const __bf16* gu, __bf16* a, int rows, int m, hipStream_t s);
+hipError_t launch_qkv_split(const QkvSplitArgs& a, int rows, hipStream_t s);
+
 hipError_t launch_decode_partial(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
 hipError_t launch_decode_reduce(const AttnArgs& a, const WorkArgs& w, hipStream_t s);
 hipError_t launch_prefill(const AttnArgs& a, const WorkArgs& w, hipStream_t s);

@@ -25,6 +25,7 @@
 #include <vector>
 
 #include "duet_internal.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace {
@@ -347,6 +348,7 @@ struct duet_ctx {
   uint64_t graphs_captured = 0, graphs_replayed = 0;
   std::vector<hipEvent_t> ev_step;  // decode stream: before step 0, after each step
   int prof_steps = 0;               // decode steps of the last profiled call (0: not look-ahead)
+  duet::GemmCache* gemm = nullptr;  // hipBLASLt handle and planned GEMMs of the block forward
 };
 
 namespace {
@@ -876,6 +878,221 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
   return DUET_OK;
 }
 
+// ---- the whole block: token-level operators around the attention kernels --------------------
+
+// Byte offsets of the block forward's buffers after the attention workspace.
+struct BlockLayout {
+  size_t h = 0, qkv = 0, q = 0, attn = 0, gu = 0, act = 0, gemm_ws[2] = {0, 0}, total = 0;
+};
+
+BlockLayout block_layout(const duet_shape* s, const duet_block_shape* blk, int64_t T, size_t attn_total) {
+  const size_t d = (size_t)s->num_q_heads * s->head_dim;
+  const size_t d_qkv = (size_t)(s->num_q_heads + 2 * s->num_kv_heads) * s->head_dim;
+  const size_t m = (size_t)blk->ffn_dim, b = 2;
+  BlockLayout L;
+  size_t off = align_up(attn_total);
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.h = take(T * d * b);
+  L.qkv = take(T * d_qkv * b);
+  L.q = take(T * d * b);
+  L.attn = take(T * d * b);
+  L.gu = take(T * 2 * m * b);
+  L.act = take(T * m * b);
+  L.gemm_ws[0] = take(kGemmWorkspaceBytes);
+  L.gemm_ws[1] = take(kGemmWorkspaceBytes);
+  L.total = off;
+  return L;
+}
+
+int check_block_exec(const duet_shape* s, const duet_block_shape* blk) {
+  if (!blk) return fail(DUET_EINVAL, "block is NULL");
+  if (s->dtype != DUET_BF16) return fail(DUET_EUNSUPPORTED, "the block forward runs bf16 only");
+  if (blk->flags != (DUET_BLOCK_GQA_QKV | DUET_BLOCK_FUSED_GATE_UP))
+    return fail(DUET_EUNSUPPORTED, "the block forward needs flags DUET_BLOCK_GQA_QKV | DUET_BLOCK_FUSED_GATE_UP");
+  if (blk->ffn_dim < 8 || blk->ffn_dim % 8) return fail(DUET_EINVAL, "ffn_dim %d must be a positive multiple of 8", blk->ffn_dim);
+  if (blk->ffn_dim > (1 << 20)) return fail(DUET_EINVAL, "ffn_dim %d too large", blk->ffn_dim);
+  return DUET_OK;
+}
+
+// Rows [row0, row0 + rows) of the requests of one kind, or rows = -1 when they are not one
+// contiguous range (rows = 0: none of that kind).
+void kind_rows(const duet_batch* b, int kind, int* row0, int* rows) {
+  int64_t lo = INT64_MAX, hi = -1, n = 0;
+  for (int r = 0; r < b->num_reqs; ++r) {
+    const duet_seq_meta& q = b->reqs[r];
+    if (q.kind != kind) continue;
+    lo = std::min<int64_t>(lo, q.q_start);
+    hi = std::max<int64_t>(hi, (int64_t)q.q_start + q.q_len);
+    n += q.q_len;
+  }
+  *row0 = n ? (int)lo : 0;
+  *rows = n == 0 ? 0 : (hi - lo == n ? (int)n : -1);
+}
+
+int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* blk, const duet_block_weights* wts,
+                  float eps, void* x, void* const* k_l, void* const* v_l, int64_t num_phys_pages,
+                  const int32_t* page_table, int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+  if (!shape) return fail(DUET_EINVAL, "shape is NULL");
+  const int layers = shape->num_layers;
+  if (layers < 1 || layers > kMaxLayers) return fail(DUET_EINVAL, "num_layers %d not in [1, %d]", layers, kMaxLayers);
+  if (!wts || !k_l || !v_l) return fail(DUET_EINVAL, "per-layer array is NULL");
+  int rc = check_device_ptr(x, "x");
+  if (rc) return rc;
+  if (!(eps > 0.0f)) return fail(DUET_EINVAL, "norm_eps must be > 0");
+  // Attention reads q from the block's own buffer and writes another one: check_call sees x as q
+  // and the workspace as the output (checked non-null and distinct from the caches).
+  std::vector<const void*> xs(layers, x), kc(k_l, k_l + layers), vc(v_l, v_l + layers);
+  std::vector<void*> outs(layers, workspace);
+  for (int l = 0; l < layers; ++l) {
+    const duet_block_weights& w = wts[l];
+    if ((rc = check_device_ptr(w.attn_norm, "attn_norm")) || (rc = check_device_ptr(w.w_qkv, "w_qkv")) ||
+        (rc = check_device_ptr(w.w_o, "w_o")) || (rc = check_device_ptr(w.ffn_norm, "ffn_norm")) ||
+        (rc = check_device_ptr(w.w_gate_up, "w_gate_up")) || (rc = check_device_ptr(w.w_down, "w_down")))
+      return rc;
+    if (x == k_l[l] || x == v_l[l]) return fail(DUET_EINVAL, "layer %d: x aliases a cache", l);
+  }
+  if ((rc = check_call(ctx, shape, layers, xs.data(), kc.data(), vc.data(), num_phys_pages, page_table,
+                       max_pages_per_req, batch, split, workspace, outs.data(), 0)))
+    return rc;
+  if ((rc = check_block_exec(shape, blk))) return rc;
+  int dec0 = 0, n_dec = 0, pre0 = 0, n_pre = 0;
+  kind_rows(batch, DUET_KIND_DECODE, &dec0, &n_dec);
+  kind_rows(batch, DUET_KIND_PREFILL, &pre0, &n_pre);
+  if (split.mode != DUET_AGG && (n_dec < 0 || n_pre < 0))
+    return fail(DUET_EUNSUPPORTED, "a split block forward needs each kind's rows to be one contiguous range");
+
+  std::lock_guard<std::mutex> lock(ctx->mu);
+  Plan& p = ctx->plan;
+  plan_batch(shape, batch, 1, 1, &p, true);
+  int64_t T = 0;
+  for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
+  const BlockLayout B = block_layout(shape, blk, T, p.total);
+  if (workspace_bytes < B.total)
+    return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, B.total);
+  if (!ctx->gemm && !(ctx->gemm = gemm_cache_create())) return fail(DUET_EHIP, "hipBLASLt initialisation failed");
+
+  hipStream_t order = static_cast<hipStream_t>(stream);
+  hipStream_t sd = order, sp = order;
+  HIP_TRY(hipSetDevice(ctx->device));
+  if (split.mode == DUET_SPLIT) {
+    if ((rc = get_stream(ctx, split.cus_decode, 0, &sd))) return rc;
+    if ((rc = get_stream(ctx, split.cus_prefill, 1, &sp))) return rc;
+  } else if (split.mode == DUET_CONCURRENT) {
+    if ((rc = get_stream(ctx, ctx->num_cus, 0, &sd))) return rc;
+    if ((rc = get_stream(ctx, ctx->num_cus, 1, &sp))) return rc;
+  }
+  const bool forked = split.mode != DUET_AGG;
+  char* ws = static_cast<char*>(workspace);
+  AttnArgs a;
+  WorkArgs w;
+  base_args(ctx, shape, p, ws, split, page_table, num_phys_pages, max_pages_per_req, &a, &w);
+  // Profiling brackets the call (fork to join) and, under a split, each partition's work: the
+  // decode partition as one look-ahead-style step (its tokens are ready at its end), the prefill
+  // partition as one layer span.
+  const bool prof = ctx->profiling >= 1;
+  if (prof && ((rc = ensure_step_events(ctx, 1)) || (rc = ensure_layer_events(ctx, 1)))) return rc;
+  if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
+  if ((rc = stage_upload(ctx, p, ws, order))) return rc;
+
+  // One partition: a stream, its token rows and its attention kernels.
+  struct Part {
+    hipStream_t st;
+    int row0, rows;
+    bool decode, prefill;
+    void* gemm_ws;
+  };
+  std::vector<Part> parts;
+  if (!forked) {
+    parts.push_back({order, 0, (int)T, w.n_dreq > 0, w.n_pitems > 0, ws + B.gemm_ws[0]});
+  } else {
+    if (n_dec > 0) parts.push_back({sd, dec0, n_dec, true, false, ws + B.gemm_ws[0]});
+    if (n_pre > 0) parts.push_back({sp, pre0, n_pre, false, true, ws + B.gemm_ws[1]});
+    HIP_TRY(hipEventRecord(ctx->ev_fork, order));
+    for (const Part& pt : parts) {
+      HIP_TRY(hipStreamWaitEvent(pt.st, ctx->ev_fork, 0));
+      if (prof) HIP_TRY(hipEventRecord(pt.decode ? ctx->ev_step[0] : ctx->ev_pre[0], pt.st));
+    }
+  }
+  const int d = shape->num_q_heads * shape->head_dim;
+  const int d_qkv = (shape->num_q_heads + 2 * shape->num_kv_heads) * shape->head_dim;
+  const int m = blk->ffn_dim;
+  __bf16* xb = static_cast<__bf16*>(x);
+  __bf16* hb = reinterpret_cast<__bf16*>(ws + B.h);
+  __bf16* qkvb = reinterpret_cast<__bf16*>(ws + B.qkv);
+  __bf16* qb = reinterpret_cast<__bf16*>(ws + B.q);
+  __bf16* ab = reinterpret_cast<__bf16*>(ws + B.attn);
+  __bf16* gub = reinterpret_cast<__bf16*>(ws + B.gu);
+  __bf16* actb = reinterpret_cast<__bf16*>(ws + B.act);
+  const char* msg = nullptr;
+  auto gemm = [&](const Part& pt, const __bf16* in, const void* wt, __bf16* out, int d_in, int d_out, bool acc) {
+    return gemm_bf16(ctx->gemm, in + (size_t)pt.row0 * d_in, wt, out + (size_t)pt.row0 * d_out, pt.rows, d_in, d_out,
+                     acc, pt.gemm_ws, pt.st, &msg);
+  };
+  for (int l = 0; l < layers; ++l) {
+    const duet_block_weights& wt = wts[l];
+    AttnArgs al = a;
+    al.q = qb;
+    al.k_cache = k_l[l];
+    al.v_cache = v_l[l];
+    al.out = ab;
+    for (const Part& pt : parts) {
+      const size_t r0 = (size_t)pt.row0;
+      HIP_TRY(launch_rmsnorm(xb + r0 * d, static_cast<const __bf16*>(wt.attn_norm), hb + r0 * d, pt.rows, d, eps, pt.st));
+      if (gemm(pt, hb, wt.w_qkv, qkvb, d, d_qkv, false)) return fail(DUET_EHIP, "QKV projection: %s", msg);
+      QkvSplitArgs qs;
+      qs.qkv = qkvb;
+      qs.q = qb;
+      qs.k_cache = static_cast<__bf16*>(k_l[l]);
+      qs.v_cache = static_cast<__bf16*>(v_l[l]);
+      qs.meta = w.meta;
+      qs.page_table = page_table;
+      qs.num_phys_pages = num_phys_pages;
+      qs.err = w.err;
+      qs.num_reqs = batch->num_reqs;
+      qs.max_pages = max_pages_per_req;
+      qs.h_q = shape->num_q_heads;
+      qs.h_kv = shape->num_kv_heads;
+      qs.head_dim = shape->head_dim;
+      qs.row0 = pt.row0;
+      HIP_TRY(launch_qkv_split(qs, pt.rows, pt.st));
+      if (pt.decode) {
+        HIP_TRY(launch_decode_partial(al, w, pt.st));
+        HIP_TRY(launch_decode_reduce(al, w, pt.st));
+      }
+      if (pt.prefill) HIP_TRY(launch_prefill(al, w, pt.st));
+      if (gemm(pt, ab, wt.w_o, xb, d, d, true)) return fail(DUET_EHIP, "output projection: %s", msg);
+      HIP_TRY(launch_rmsnorm(xb + r0 * d, static_cast<const __bf16*>(wt.ffn_norm), hb + r0 * d, pt.rows, d, eps, pt.st));
+      if (gemm(pt, hb, wt.w_gate_up, gub, d, 2 * m, false)) return fail(DUET_EHIP, "gate-up projection: %s", msg);
+      HIP_TRY(launch_swiglu(gub + r0 * 2 * m, actb + r0 * m, pt.rows, m, pt.st));
+      if (gemm(pt, actb, wt.w_down, xb, m, d, true)) return fail(DUET_EHIP, "down projection: %s", msg);
+    }
+  }
+  bool dec_part = false, pre_part = false;
+  if (forked) {
+    hipEvent_t joins[2] = {ctx->ev_djoin, ctx->ev_pjoin};
+    for (size_t i = 0; i < parts.size(); ++i) {
+      if (prof) HIP_TRY(hipEventRecord(parts[i].decode ? ctx->ev_step[1] : ctx->ev_pre[1], parts[i].st));
+      dec_part |= parts[i].decode;
+      pre_part |= parts[i].prefill;
+      HIP_TRY(hipEventRecord(joins[i], parts[i].st));
+      HIP_TRY(hipStreamWaitEvent(order, joins[i], 0));
+    }
+  }
+  if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
+  ctx->prof_valid = prof;
+  ctx->prof_kernels = false;
+  ctx->prof_deferred = false;
+  ctx->prof_decode = dec_part;
+  ctx->prof_prefill = pre_part;
+  ctx->prof_layers = 1;
+  ctx->prof_steps = 1;
+  return DUET_OK;
+}
 
 }  // namespace
 
@@ -925,6 +1142,11 @@ int duet_init(int device, duet_ctx** out) {
 int duet_destroy(duet_ctx* ctx) {
   if (!ctx) return DUET_OK;
   (void)hipSetDevice(ctx->device);
+  if (ctx->gemm) {
+    (void)hipDeviceSynchronize();
+    duet::gemm_cache_destroy(ctx->gemm);
+    ctx->gemm = nullptr;
+  }
   for (auto& kv : ctx->streams) {
     (void)hipStreamSynchronize(kv.second);
     (void)hipStreamDestroy(kv.second);
@@ -964,6 +1186,32 @@ int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_
   plan_batch(shape, batch, shape->num_layers, 1, &p, false);
   *bytes = p.total;
   return DUET_OK;
+}
+
+int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
+                               size_t* bytes) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if ((rc = check_block_exec(shape, block))) return rc;
+  if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
+  Plan p;
+  plan_batch(shape, batch, 1, 1, &p, false);
+  int64_t T = 0;
+  for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
+  *bytes = block_layout(shape, block, T, p.total).total;
+  return DUET_OK;
+}
+
+int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* block,
+                       const duet_block_weights* weights, float norm_eps, void* x, void* const* k_cache,
+                       void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                       int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  clear_error();
+  return block_forward(ctx, shape, block, weights, norm_eps, x, k_cache, v_cache, num_phys_pages, page_table,
+                       max_pages_per_req, batch, split, workspace, workspace_bytes, stream);
 }
 
 int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
