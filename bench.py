@@ -439,6 +439,8 @@ def block_main(args):
     rows.append({"mode": "AGG", "us": round(agg_us, 1), "decode_ready_us": round(agg_ready, 1),
                  "predicted_us": round(agg_pred, 1)})
     splits = [(sp_, 256 - sp_) for sp_ in range(32, 256, 32)]
+    if args.split:  # one split only (besides AGG), e.g. for a profile
+        splits = [tuple(int(v) for v in args.split.split(","))]
     if chosen.mode == duet.SPLIT and (chosen.cus_prefill, chosen.cus_decode) not in splits:
         splits.append((chosen.cus_prefill, chosen.cus_decode))
     for s_p, s_d in splits:
