@@ -174,6 +174,9 @@ def trace_main(args):
     from paper_2511_04791_amd.calibration import calibrate_model
 
     L = args.layers if args.layers is not None else 32
+    full = args.block  # whole blocks (duet_block_forward) and the full-model estimate
+    ffn = 14336
+    block = duet.BlockShape(ffn, 0, duet.BLOCK_GQA_QKV | duet.BLOCK_FUSED_GATE_UP)
     ctx = duet.Context(0)
     if not args.no_calibrate:
         calibrate_model(ctx)
@@ -189,12 +192,16 @@ def trace_main(args):
     vcs = [(torch.randn(pool, 8, 128, 16, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
     qs = [(torch.randn(max_tok, 32, 128, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
     outs = [torch.empty_like(q) for q in qs]
+    if full:
+        del qs, outs
+        weights = wl.block_weights(sh, ffn, L, gen)
+        xbuf = torch.randn(max_tok, 32 * 128, generator=gen, device="cuda").to(torch.bfloat16)
     rng = np.random.default_rng(1005)
     modes = {"agg": [], "adaptive_50ms": [], "adaptive_tight": []}
     ready = {name: [] for name in modes}   # fork to the end of the last decode kernel (TBT)
     chosen = {"adaptive_50ms": [], "adaptive_tight": []}
     tokens = []
-    ctx.set_profiling(2)
+    ctx.set_profiling(1 if full else 2)
     for bi, rows in enumerate(batches):
         n_tok = sum(q for _, q, _ in rows)
         starts = np.cumsum([0] + [q for _, q, _ in rows])[:-1]
@@ -207,26 +214,37 @@ def trace_main(args):
             table[r, :n] = pages[off:off + n]
             off += n
         pt = torch.as_tensor(table, device="cuda")
-        q_l = [q[:n_tok] for q in qs]
-        o_l = [o[:n_tok] for o in outs]
         rows3 = [(int(k), int(q), int(c)) for k, q, c in rows]
-        t_agg = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), sh, ctx.model)
+        if full:
+            predict = lambda sp_: duet.predict_model_latency(rows3, sp_, sh, block, ctx.model)
+            choose = lambda tau_: duet.choose_cu_split_model(rows3, tau_, sh, block, ctx.model, max_decode_steps=1)
+            x_it = xbuf[:n_tok]
+            run = lambda sp_: ctx.block_forward(x_it, weights, kcs, vcs, pt, meta, ffn, sp_)
+        else:
+            predict = lambda sp_: duet.predict_iter_latency(rows3, sp_, sh, ctx.model)
+            choose = lambda tau_: duet.choose_cu_split(rows3, tau_, sh, ctx.model, max_decode_steps=1)
+            q_l = [q[:n_tok] for q in qs]
+            o_l = [o[:n_tok] for o in outs]
+            run = lambda sp_: ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp_, outs=o_l)
+        t_agg = predict(duet.CuSplit.agg())
         for name in modes:
             if name == "agg":
                 sp = duet.CuSplit.agg()
             else:
                 tau = 50000.0 if name == "adaptive_50ms" else 0.99 * t_agg
-                sp, pred = duet.choose_cu_split(rows3, tau, sh, ctx.model, max_decode_steps=1)[:2]
+                sp, pred = choose(tau)[:2]
                 if name == "adaptive_tight" and sp.mode == duet.SPLIT and pred >= t_agg:
                     sp = duet.CuSplit.agg()   # this mode only splits when the model predicts a gain
                 chosen[name].append(sp.mode == duet.SPLIT)
             for rep in range(2):  # the first call on a new CU split creates its streams
-                ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
+                run(sp)
                 kt = ctx.last_kernel_times()
             modes[name].append(kt["iteration_us"])
             ready[name].append(kt["decode_start_us"] + kt["decode_total_us"] if kt["decode_total_us"] > 0
                                else kt["iteration_us"])
         tokens.append(n_tok)
+        if bi % 25 == 24:
+            print(f"trace: {bi + 1}/{len(batches)} iterations", file=sys.stderr, flush=True)
     ctx.set_profiling(0)
     tot_tok = float(sum(tokens))
     res = {}
@@ -242,11 +260,13 @@ def trace_main(args):
         if name in chosen:
             res[name]["split_fraction"] = round(float(np.mean(chosen[name])), 3)
     n_pre = sum(1 for b in batches if any(k == 0 for k, _, _ in b))
-    line = {"metric": "serving-trace decode TBT p99, attention share (us)", "value": res["adaptive_50ms"]["decode_ready_p99_us"],
+    line = {"metric": "serving-trace decode TBT p99, " + ("full model" if full else "attention share") + " (us)",
+            "value": res["adaptive_50ms"]["decode_ready_p99_us"],
             "unit": "us", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": f"serving trace: {len(batches)} iterations, Poisson 4 req/s, prompts LogN(mean 4096, "
                                    f"sigma 1.0) <= 32768, outputs LogN(mean 256, sigma 0.7), budget 8192, {L} layers, "
-                                   "llama3-8b attention shapes", "iterations_with_prefill": n_pre,
+                                   + (f"llama3-8b transformer blocks (random-init weights, FFN {ffn})" if full else
+                                      "llama3-8b attention shapes"), "iterations_with_prefill": n_pre,
                        "mean_decodes": round(float(np.mean([sum(1 for k, _, _ in b if k == 1) for b in batches])), 1),
                        "mean_tokens": round(float(np.mean(tokens)), 1)},
             "modes": res, "agg_decode_ready_p99_us": res["agg"]["decode_ready_p99_us"],

@@ -332,6 +332,27 @@ def serving_trace(num_iters: int = 200, seed: int = 1005, *, rate: float = 4.0, 
     return out
 
 
+def block_weights(sh: AttnShape, ffn_dim: int, layers: int, gen):
+    """Per-layer bf16 weight dicts drawn from the torch generator `gen` (on its device), per layer
+    in the order attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down: norm weights 1 + 0.1 N(0,1),
+    a [d_in, d_out] matrix N(0,1) / sqrt(d_in)."""
+    import torch
+
+    dev = gen.device
+    d = sh.num_q_heads * sh.head_dim
+    d_qkv = (sh.num_q_heads + 2 * sh.num_kv_heads) * sh.head_dim
+    m = int(ffn_dim)
+
+    def mat(d_in, d_out):
+        return (torch.randn(d_in, d_out, generator=gen, device=dev) / math.sqrt(d_in)).to(torch.bfloat16)
+
+    def norm_w(n):
+        return (1.0 + 0.1 * torch.randn(n, generator=gen, device=dev)).to(torch.bfloat16)
+
+    return [{"attn_norm": norm_w(d), "w_qkv": mat(d, d_qkv), "w_o": mat(d, d), "ffn_norm": norm_w(d),
+             "w_gate_up": mat(d, 2 * m), "w_down": mat(m, d)} for _ in range(layers)]
+
+
 def make_block_tensors(batch: Batch, ffn_dim: int, layers: int, seed: int, *, device="cpu"):
     """Inputs of an L-block forward (bf16): the residual stream x [T, h_q d], per-layer weight
     dicts and per-layer (k_cache, v_cache).  Drawn with a torch generator on `device`, in this
@@ -348,21 +369,9 @@ def make_block_tensors(batch: Batch, ffn_dim: int, layers: int, seed: int, *, de
     gen = torch.Generator(device=dev)
     gen.manual_seed(int(seed))
     d = sh.num_q_heads * sh.head_dim
-    d_qkv = (sh.num_q_heads + 2 * sh.num_kv_heads) * sh.head_dim
     m = int(ffn_dim)
-
-    def mat(d_in, d_out):
-        return (torch.randn(d_in, d_out, generator=gen, device=dev) / math.sqrt(d_in)).to(torch.bfloat16)
-
-    def norm_w(n):
-        return (1.0 + 0.1 * torch.randn(n, generator=gen, device=dev)).to(torch.bfloat16)
-
     x = torch.randn(batch.num_tokens, d, generator=gen, device=dev).to(torch.bfloat16)
-    weights = []
-    for _ in range(layers):
-        w = {"attn_norm": norm_w(d), "w_qkv": mat(d, d_qkv), "w_o": mat(d, d), "ffn_norm": norm_w(d),
-             "w_gate_up": mat(d, 2 * m), "w_down": mat(m, d)}
-        weights.append(w)
+    weights = block_weights(sh, m, layers, gen)
     caches = []
     for l in range(layers):
         _, kc, vc = make_tensors(batch, seed + 1 + l, device=device)
