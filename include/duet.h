@@ -329,6 +329,38 @@ int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_
                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/* ---- serving engine: continuous batching with chunked prefill (Sections 2-4) ------------------
+ *
+ * The batch former of the serving loop and its paged KV-cache allocator (host only).  Requests
+ * wait in arrival order.  Each step schedules, under a token budget, first one token for every
+ * running request whose prompt is fully prefilled (in admission order), then prompt tokens of
+ * the partly prefilled requests and then of the waiting ones, chunking the last prompt taken.
+ * The pages the step's tokens need are reserved from a free list; a request keeps its pages
+ * until it has produced its output tokens.  The caller runs the step on the GPU (e.g.
+ * duet_block_forward, which writes the scheduled tokens' keys and values into those pages), then
+ * calls duet_engine_complete. */
+typedef struct duet_engine duet_engine;
+
+/* token_budget >= 1 tokens per step; page_size 16; num_pages cache pages (ids 0 .. num_pages - 1,
+ * handed out in order, or in a splitmix64 Fisher-Yates permutation when shuffle_seed != 0);
+ * page-table rows of max_pages_per_req entries. */
+int duet_engine_create(int32_t token_budget, int32_t page_size, int64_t num_pages, int32_t max_pages_per_req,
+                       uint64_t shuffle_seed, duet_engine** out);
+int duet_engine_destroy(duet_engine* engine);
+/* Queues a request; *id (may be NULL) receives its id (0, 1, ... in call order).  DUET_EINVAL if a
+ * length is < 1 or prompt + output tokens need more than max_pages_per_req pages. */
+int duet_engine_add_request(duet_engine* engine, int32_t prompt_len, int32_t output_len, int64_t* id);
+/* Forms the next step into host arrays of max_reqs rows: meta (rows packed, decodes first, q_start
+ * running), page_table [max_reqs, max_pages_per_req] (-1 padded) and req_ids (may be NULL);
+ * *num_reqs may be 0.  DUET_ENOMEM when the free pages do not cover the step (nothing changes),
+ * DUET_EINVAL when max_reqs is too small or the previous step is not completed. */
+int duet_engine_step(duet_engine* engine, duet_seq_meta* meta, int32_t* page_table, int64_t* req_ids,
+                     int32_t max_reqs, int32_t* num_reqs);
+/* Marks the last step done: chunks advance, each decode gains its token, finished requests release
+ * their pages. */
+int duet_engine_complete(duet_engine* engine);
+int duet_engine_stats(const duet_engine* engine, int64_t* waiting, int64_t* running, int64_t* free_pages);
+
 /* ---- look-ahead decode (Section 4.3, interruption-free dispatch) -------------------------------
  *
  * Decode requests get KV slots for k future steps ahead of time, and the k decode steps run back

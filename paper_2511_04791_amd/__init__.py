@@ -229,6 +229,56 @@ def block_workspace_bytes(shape: AttnShape, block: BlockShape, seq_meta) -> int:
     return n.value
 
 
+class Engine:
+    """The serving engine's batch former and page allocator (duet_engine_*), host only."""
+
+    def __init__(self, token_budget: int, num_pages: int, max_pages_per_req: int, *, page_size: int = 16,
+                 shuffle_seed: int = 0):
+        h = ctypes.c_void_p()
+        N.check(N.lib().duet_engine_create(int(token_budget), int(page_size), int(num_pages), int(max_pages_per_req),
+                                           int(shuffle_seed), ctypes.byref(h)), "duet_engine_create")
+        self.handle, self.max_pages, self.budget = h, int(max_pages_per_req), int(token_budget)
+
+    def add_request(self, prompt_len: int, output_len: int) -> int:
+        rid = ctypes.c_int64()
+        N.check(N.lib().duet_engine_add_request(self.handle, int(prompt_len), int(output_len), ctypes.byref(rid)),
+                "duet_engine_add_request")
+        return rid.value
+
+    def stats(self) -> tuple[int, int, int]:
+        """(waiting, running, free pages)."""
+        w, r, f = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        N.check(N.lib().duet_engine_stats(self.handle, ctypes.byref(w), ctypes.byref(r), ctypes.byref(f)),
+                "duet_engine_stats")
+        return w.value, r.value, f.value
+
+    def step(self):
+        """The next step: (seq_meta int32 [R, 4], page_table int32 [R, max_pages], request ids int64 [R])."""
+        w, r, _ = self.stats()
+        cap = int(w + r) + 1
+        meta = np.zeros((cap, 4), dtype=np.int32)
+        table = np.zeros((cap, self.max_pages), dtype=np.int32)
+        ids = np.zeros(cap, dtype=np.int64)
+        n = ctypes.c_int32()
+        N.check(N.lib().duet_engine_step(self.handle, meta.ctypes.data, table.ctypes.data, ids.ctypes.data, cap,
+                                         ctypes.byref(n)), "duet_engine_step")
+        return meta[:n.value].copy(), table[:n.value].copy(), ids[:n.value].copy()
+
+    def complete(self) -> None:
+        N.check(N.lib().duet_engine_complete(self.handle), "duet_engine_complete")
+
+    def close(self) -> None:
+        if self.handle:
+            N.lib().duet_engine_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 BLOCK_WEIGHT_NAMES = ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")
 
 

@@ -268,6 +268,20 @@ class _Live:
     generated: int = 0
 
 
+def trace_requests(seed: int = 1005, *, rate: float = 4.0, prompt_mean: float = 4096, prompt_sigma: float = 1.0,
+                   output_mean: float = 256, output_sigma: float = 0.7, cap: int = 32768, n_req: int = 200000):
+    """The request stream of the serving trace: Poisson arrival times (s), lognormal prompt and output
+    lengths (means as given, clipped to [1, cap]), drawn in that order from PCG64(seed)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pmu, psg = lognormal_mean_params(prompt_mean, prompt_sigma)
+    omu, osg = lognormal_mean_params(output_mean, output_sigma)
+    gaps = rng.exponential(1.0 / rate, size=n_req)
+    arrivals = np.cumsum(gaps)
+    prompts = np.clip(np.rint(rng.lognormal(pmu, psg, size=n_req)), 1, cap).astype(np.int64)
+    outputs = np.clip(np.rint(rng.lognormal(omu, osg, size=n_req)), 1, cap).astype(np.int64)
+    return arrivals, prompts, outputs
+
+
 def serving_trace(num_iters: int = 200, seed: int = 1005, *, rate: float = 4.0, prompt_mean: float = 4096,
                   prompt_sigma: float = 1.0, output_mean: float = 256, output_sigma: float = 0.7,
                   cap: int = 32768, token_budget: int = 8192, warmup_iters: int = 200,
@@ -279,15 +293,9 @@ def serving_trace(num_iters: int = 200, seed: int = 1005, *, rate: float = 4.0, 
     Returns a list of request lists [(kind, q_len, cached_len), ...], one per recorded iteration,
     after `warmup_iters` unrecorded iterations.  `iter_seconds(reqs)` advances the clock.
     """
-    rng = np.random.Generator(np.random.PCG64(seed))
-    pmu, psg = lognormal_mean_params(prompt_mean, prompt_sigma)
-    omu, osg = lognormal_mean_params(output_mean, output_sigma)
-    n_req = 200000
-    gaps = rng.exponential(1.0 / rate, size=n_req)
-    arrivals = np.cumsum(gaps)
-    prompts = np.clip(np.rint(rng.lognormal(pmu, psg, size=n_req)), 1, cap).astype(np.int64)
-    outputs = np.clip(np.rint(rng.lognormal(omu, osg, size=n_req)), 1, cap).astype(np.int64)
-
+    arrivals, prompts, outputs = trace_requests(seed, rate=rate, prompt_mean=prompt_mean, prompt_sigma=prompt_sigma,
+                                                output_mean=output_mean, output_sigma=output_sigma, cap=cap)
+    n_req = len(arrivals)
     clock = 0.0
     nxt = 0
     waiting: list[_Live] = []
