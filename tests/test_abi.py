@@ -134,3 +134,31 @@ def test_lookahead_rejects_null_context_and_bad_steps(native):
                                     ctypes.byref(b), N.CuSplit(0, 256, 0, 0), 1, 1 << 20, ptrs, ptrs, None)
     assert rc == -1
     assert native.duet_set_decode_graphs(None, 1) == -1
+
+
+def test_block_workspace_and_validation(native):
+    arr, b = _batch([(0, 0, 100, 20), (1, 100, 1, 500)])
+    attn, blk = ctypes.c_size_t(), ctypes.c_size_t()
+    full = N.BlockShape(1024, 0, 3)
+    assert native.duet_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(b), ctypes.byref(attn)) == 0
+    assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(full), ctypes.byref(b),
+                                             ctypes.byref(blk)) == 0
+    T, d, d_qkv, m = 101, 4096, 6144, 1024
+    # the attention workspace, six activation buffers and two 32 MiB GEMM workspaces
+    assert blk.value >= attn.value + T * 2 * (3 * d + d_qkv + 2 * m + m) + 2 * (32 << 20)
+    for bad, code in ((N.BlockShape(1024, 0, 0), -2), (N.BlockShape(1020, 0, 3), -1), (N.BlockShape(0, 0, 3), -1)):
+        assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(bad), ctypes.byref(b),
+                                                 ctypes.byref(blk)) == code
+    assert native.duet_block_workspace_bytes(ctypes.byref(_shape(dtype=N.F32, head_dim=64, num_q_heads=4,
+                                                                 num_kv_heads=2)), ctypes.byref(full),
+                                             ctypes.byref(b), ctypes.byref(blk)) == -2
+
+
+def test_block_forward_rejects_bad_arguments_before_any_launch(native):
+    arr, b = _batch([(0, 0, 10, 0)])
+    w = (N.BlockWeights * 1)(N.BlockWeights(1, 1, 1, 1, 1, 1))
+    caches = (ctypes.c_void_p * 1)(16)
+    # no context
+    assert native.duet_block_forward(None, ctypes.byref(_shape()), ctypes.byref(N.BlockShape(1024, 0, 3)), w, 1e-5,
+                                     32, caches, caches, 10, 64, 1, ctypes.byref(b), N.CuSplit(N.AGG, 256, 0, 1), 48,
+                                     1 << 30, None) == -1
