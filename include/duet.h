@@ -352,8 +352,9 @@ int duet_engine_destroy(duet_engine* engine);
 int duet_engine_add_request(duet_engine* engine, int32_t prompt_len, int32_t output_len, int64_t* id);
 /* Forms the next step into host arrays of max_reqs rows: meta (rows packed, decodes first, q_start
  * running), page_table [max_reqs, max_pages_per_req] (-1 padded) and req_ids (may be NULL);
- * *num_reqs may be 0.  DUET_ENOMEM when the free pages do not cover the step (nothing changes),
- * DUET_EINVAL when max_reqs is too small or the previous step is not completed. */
+ * *num_reqs may be 0.  DUET_ENOMEM when the free pages do not cover the step (nothing changes;
+ * there is no preemption, so the pool must hold the pages of every running request), DUET_EINVAL
+ * when max_reqs is too small or the previous step is not completed. */
 int duet_engine_step(duet_engine* engine, duet_seq_meta* meta, int32_t* page_table, int64_t* req_ids,
                      int32_t max_reqs, int32_t* num_reqs);
 /* Marks the last step done: chunks advance, each decode gains its token, finished requests release
