@@ -304,11 +304,12 @@ typedef struct {
   const void* w_down;    /* [ffn_dim, d] */
 } duet_block_weights;
 
-/* Workspace of duet_block_forward: duet_workspace_bytes' layout, the activations of every
- * scheduled token ([T, d] x4, [T, (h_q + 2 h_kv) head_dim], [T, 2 ffn_dim], [T, ffn_dim], bf16)
- * and two hipBLASLt workspaces.  Host only. */
+/* Workspace of duet_block_forward with k_decode_steps decode steps: duet_workspace_bytes' layout
+ * (with the work lists of look-ahead steps 1 .. k - 1), the activations of every scheduled token
+ * ([T, d] x4, [T, (h_q + 2 h_kv) head_dim], [T, 2 ffn_dim], [T, ffn_dim], bf16) and two hipBLASLt
+ * workspaces.  Host only. */
 int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
-                               size_t* bytes);
+                               int32_t k_decode_steps, size_t* bytes);
 
 /* Runs shape->num_layers blocks in place on the residual stream x [T, d] (bf16, rows packed per
  * request in batch order).  weights, k_cache and v_cache are host arrays of num_layers entries
@@ -320,12 +321,18 @@ int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* 
  * to back, and needs each kind's rows to be one contiguous range (DUET_EUNSUPPORTED otherwise).
  * Requests must not share cache pages.  A page id outside [0, num_phys_pages) met while writing
  * or reading the cache is not dereferenced and sets the error word.  Stream, ownership and
- * validation rules as for duet_attn_iteration.  With profiling on, duet_last_kernel_times()
- * reports iteration_us (fork to join) and, under a split, decode_total_us / decode_start_us (the
- * decode partition: its tokens are ready at its end) and prefill_total_us / prefill_start_us. */
+ * validation rules as for duet_attn_iteration.  Look-ahead (Section 4.3): with
+ * split.k_decode_steps = k > 1 the decode requests run k steps in the call; step s = 1 .. k - 1
+ * takes their next residual rows from x_ahead[s - 1] ([R_d, d] bf16 device memory, decode requests
+ * in batch order, updated in place), writes those tokens' keys and values at position
+ * cached_len + s (the page table must cover cached_len + k tokens) and attends over them; under
+ * SPLIT the steps run back to back on the decode CUs while the prefill partition runs once.  With
+ * profiling on, duet_last_kernel_times() reports iteration_us (fork to join) and, under a split,
+ * decode_total_us / decode_start_us / decode_first_step_us (the decode partition; step s's tokens
+ * are ready at its end) and prefill_total_us / prefill_start_us. */
 int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* block,
-                       const duet_block_weights* weights, float norm_eps, void* x, void* const* k_cache,
-                       void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                       const duet_block_weights* weights, float norm_eps, void* x, void* const* x_ahead,
+                       void* const* k_cache, void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
                        size_t workspace_bytes, void* stream);
 

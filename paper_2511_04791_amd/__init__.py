@@ -220,12 +220,13 @@ def workspace_bytes(shape: AttnShape, seq_meta) -> int:
     return n.value
 
 
-def block_workspace_bytes(shape: AttnShape, block: BlockShape, seq_meta) -> int:
+def block_workspace_bytes(shape: AttnShape, block: BlockShape, seq_meta, k_decode_steps: int = 1) -> int:
     """Device workspace of duet_block_forward for this batch."""
     b = _BatchC(seq_meta)
     n = ctypes.c_size_t()
     N.check(N.lib().duet_block_workspace_bytes(ctypes.byref(_shape_c(shape)), ctypes.byref(block.to_c()),
-                                               ctypes.byref(b.c), ctypes.byref(n)), "duet_block_workspace_bytes")
+                                               ctypes.byref(b.c), int(k_decode_steps), ctypes.byref(n)),
+            "duet_block_workspace_bytes")
     return n.value
 
 
@@ -376,11 +377,13 @@ class Context:
         return out
 
     def block_forward(self, x, weights, k_caches, v_caches, page_table, seq_meta, ffn_dim: int,
-                      cu_split: CuSplit = CuSplit.agg(), *, norm_eps: float = 1e-5, workspace=None, stream=None,
-                      check_errors: bool = False):
+                      cu_split: CuSplit = CuSplit.agg(), *, x_ahead=None, norm_eps: float = 1e-5, workspace=None,
+                      stream=None, check_errors: bool = False):
         """len(weights) transformer blocks in place on the residual stream x [T, h_q d] (duet_block_forward).
         weights: per-layer dicts of contiguous bf16 device tensors named as BLOCK_WEIGHT_NAMES; the caches
-        receive every scheduled token's keys and values.  Returns x."""
+        receive every scheduled token's keys and values.  With cu_split.k_decode_steps = k > 1, x_ahead
+        holds k - 1 tensors [R_d, h_q d]: the decode requests' residual rows of look-ahead steps 1 .. k - 1
+        (updated in place).  Returns x."""
         import torch
         L = len(weights)
         if L < 1 or len(k_caches) != L or len(v_caches) != L:
@@ -405,13 +408,24 @@ class Context:
                     raise ValueError(f"layer {l}: {name} must be a contiguous bf16 device tensor {want[name]}")
             self._check_layer(x.view(n_tok, shape.num_q_heads, dh), k_caches[l], v_caches[l], page_table, b)
         block = BlockShape(int(ffn_dim), 0, BLOCK_GQA_QKV | BLOCK_FUSED_GATE_UP)
-        need = block_workspace_bytes(shape, block, b.rows)
+        k = int(cu_split.k_decode_steps)
+        n_dec = int((b.rows[:, 0] == KIND_DECODE).sum()) if len(b.rows) else 0
+        xa = list(x_ahead or [])
+        if k > 1 and n_dec > 0:
+            if len(xa) != k - 1:
+                raise ValueError(f"x_ahead must hold k - 1 = {k - 1} tensors")
+            for t in xa:
+                if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != (n_dec, d):
+                    raise ValueError(f"x_ahead tensors must be contiguous bf16 device tensors [{n_dec}, {d}]")
+        need = block_workspace_bytes(shape, block, b.rows, k)
         ws = self.workspace(need) if workspace is None else workspace
         wts = (N.BlockWeights * L)(*[N.BlockWeights(*[w[n].data_ptr() for n in BLOCK_WEIGHT_NAMES]) for w in weights])
         arr = lambda ts: (ctypes.c_void_p * L)(*[t.data_ptr() for t in ts])
         st = torch.cuda.current_stream(x.device).cuda_stream if stream is None else stream
         N.check(N.lib().duet_block_forward(self.handle, ctypes.byref(_shape_c(shape)), ctypes.byref(block.to_c()), wts,
-                                           float(norm_eps), x.data_ptr(), arr(k_caches), arr(v_caches),
+                                           float(norm_eps), x.data_ptr(),
+                                           (ctypes.c_void_p * max(1, len(xa)))(*[t.data_ptr() for t in xa]) if xa else None,
+                                           arr(k_caches), arr(v_caches),
                                            int(kc0.shape[0]), page_table.data_ptr(), int(page_table.shape[1]),
                                            ctypes.byref(b.c), cu_split.to_c(), ws.data_ptr(), ws.numel(),
                                            ctypes.c_void_p(st)), "duet_block_forward")

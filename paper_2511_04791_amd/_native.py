@@ -76,7 +76,7 @@ _SIGS = {
     "duet_destroy": (c_int32, [c_void_p]),
     "duet_ctx_model": (c_void_p, [c_void_p]),
     "duet_workspace_bytes": (c_int32, [P(Shape), P(Batch), P(c_size_t)]),
-    "duet_block_workspace_bytes": (c_int32, [P(Shape), P(BlockShape), P(Batch), P(c_size_t)]),
+    "duet_block_workspace_bytes": (c_int32, [P(Shape), P(BlockShape), P(Batch), c_int32, P(c_size_t)]),
     "duet_engine_create": (c_int32, [c_int32, c_int32, c_int64, c_int32, ctypes.c_uint64, P(c_void_p)]),
     "duet_engine_destroy": (c_int32, [c_void_p]),
     "duet_engine_add_request": (c_int32, [c_void_p, c_int32, c_int32, P(c_int64)]),
@@ -84,7 +84,7 @@ _SIGS = {
     "duet_engine_complete": (c_int32, [c_void_p]),
     "duet_engine_stats": (c_int32, [c_void_p, P(c_int64), P(c_int64), P(c_int64)]),
     "duet_block_forward": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(BlockWeights), ctypes.c_float, c_void_p,
-                                     P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,
+                                     P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,
                                      c_void_p, c_size_t, c_void_p]),
     "duet_attn_mixed_batch": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),

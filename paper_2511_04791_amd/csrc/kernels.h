@@ -117,6 +117,8 @@ struct QkvSplitArgs {
   __bf16* k_cache;         // [P, h_kv, 16, d]
   __bf16* v_cache;         // [P, h_kv, d, 16]
   const int4* meta;        // [R] (kind, q_start, q_len, cached_len), q_start rising
+  const int4* dreq;        // null: a row's request is found by q_start; else row i is decode request i
+                           //       (dreq[i].x) of a look-ahead step
   const int32_t* page_table;
   long long num_phys_pages;
   int32_t* err;

@@ -934,12 +934,14 @@ void kind_rows(const duet_batch* b, int kind, int* row0, int* rows) {
 }
 
 int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* blk, const duet_block_weights* wts,
-                  float eps, void* x, void* const* k_l, void* const* v_l, int64_t num_phys_pages,
+                  float eps, void* x, void* const* x_ahead, void* const* k_l, void* const* v_l, int64_t num_phys_pages,
                   const int32_t* page_table, int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split,
                   void* workspace, size_t workspace_bytes, void* stream) {
   if (!shape) return fail(DUET_EINVAL, "shape is NULL");
   const int layers = shape->num_layers;
   if (layers < 1 || layers > kMaxLayers) return fail(DUET_EINVAL, "num_layers %d not in [1, %d]", layers, kMaxLayers);
+  const int k = split.k_decode_steps;
+  if (k < 1 || k > kMaxLookahead) return fail(DUET_EINVAL, "k_decode_steps %d not in [1, %d]", k, kMaxLookahead);
   if (!wts || !k_l || !v_l) return fail(DUET_EINVAL, "per-layer array is NULL");
   int rc = check_device_ptr(x, "x");
   if (rc) return rc;
@@ -957,18 +959,27 @@ int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape
     if (x == k_l[l] || x == v_l[l]) return fail(DUET_EINVAL, "layer %d: x aliases a cache", l);
   }
   if ((rc = check_call(ctx, shape, layers, xs.data(), kc.data(), vc.data(), num_phys_pages, page_table,
-                       max_pages_per_req, batch, split, workspace, outs.data(), 0)))
+                       max_pages_per_req, batch, split, workspace, outs.data(), k - 1)))
     return rc;
   if ((rc = check_block_exec(shape, blk))) return rc;
   int dec0 = 0, n_dec = 0, pre0 = 0, n_pre = 0;
   kind_rows(batch, DUET_KIND_DECODE, &dec0, &n_dec);
   kind_rows(batch, DUET_KIND_PREFILL, &pre0, &n_pre);
-  if (split.mode != DUET_AGG && (n_dec < 0 || n_pre < 0))
-    return fail(DUET_EUNSUPPORTED, "a split block forward needs each kind's rows to be one contiguous range");
+  if ((split.mode != DUET_AGG || k > 1) && (n_dec < 0 || n_pre < 0))
+    return fail(DUET_EUNSUPPORTED,
+                "a split or look-ahead block forward needs each kind's rows to be one contiguous range");
+  const int steps = n_dec > 0 ? k : 1;  // decode steps of this call
+  if (steps > 1) {
+    if (!x_ahead) return fail(DUET_EINVAL, "x_ahead is NULL with k_decode_steps > 1");
+    for (int s = 0; s < steps - 1; ++s) {
+      if ((rc = check_device_ptr(x_ahead[s], "x_ahead"))) return rc;
+      if (x_ahead[s] == x) return fail(DUET_EINVAL, "x_ahead[%d] aliases x", s);
+    }
+  }
 
   std::lock_guard<std::mutex> lock(ctx->mu);
   Plan& p = ctx->plan;
-  plan_batch(shape, batch, 1, 1, &p, true);
+  plan_batch(shape, batch, 1, steps, &p, true);
   int64_t T = 0;
   for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
   const BlockLayout B = block_layout(shape, blk, T, p.total);
@@ -992,14 +1003,15 @@ int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape
   WorkArgs w;
   base_args(ctx, shape, p, ws, split, page_table, num_phys_pages, max_pages_per_req, &a, &w);
   // Profiling brackets the call (fork to join) and, under a split, each partition's work: the
-  // decode partition as one look-ahead-style step (its tokens are ready at its end), the prefill
-  // partition as one layer span.
+  // decode partition step by step (its tokens of step s are ready at the end of step s), the
+  // prefill partition as one span.
   const bool prof = ctx->profiling >= 1;
-  if (prof && ((rc = ensure_step_events(ctx, 1)) || (rc = ensure_layer_events(ctx, 1)))) return rc;
+  if (prof && ((rc = ensure_step_events(ctx, steps)) || (rc = ensure_layer_events(ctx, 1)))) return rc;
   if (prof) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
   if ((rc = stage_upload(ctx, p, ws, order))) return rc;
 
-  // One partition: a stream, its token rows and its attention kernels.
+  // One partition: a stream, its token rows (of x and of the activation buffers) and its
+  // attention kernels.
   struct Part {
     hipStream_t st;
     int row0, rows;
@@ -1021,7 +1033,6 @@ int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape
   const int d = shape->num_q_heads * shape->head_dim;
   const int d_qkv = (shape->num_q_heads + 2 * shape->num_kv_heads) * shape->head_dim;
   const int m = blk->ffn_dim;
-  __bf16* xb = static_cast<__bf16*>(x);
   __bf16* hb = reinterpret_cast<__bf16*>(ws + B.h);
   __bf16* qkvb = reinterpret_cast<__bf16*>(ws + B.qkv);
   __bf16* qb = reinterpret_cast<__bf16*>(ws + B.q);
@@ -1029,54 +1040,85 @@ int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape
   __bf16* gub = reinterpret_cast<__bf16*>(ws + B.gu);
   __bf16* actb = reinterpret_cast<__bf16*>(ws + B.act);
   const char* msg = nullptr;
-  auto gemm = [&](const Part& pt, const __bf16* in, const void* wt, __bf16* out, int d_in, int d_out, bool acc) {
-    return gemm_bf16(ctx->gemm, in + (size_t)pt.row0 * d_in, wt, out + (size_t)pt.row0 * d_out, pt.rows, d_in, d_out,
-                     acc, pt.gemm_ws, pt.st, &msg);
-  };
-  for (int l = 0; l < layers; ++l) {
+  // One layer of one partition over its rows: xr is its first residual row; the activation
+  // buffers use rows [pt.row0, pt.row0 + pt.rows).  Look-ahead steps (dreq != null) index their
+  // decode requests from 0, so their q / attention rows are addressed from the partition's first
+  // row; step 0 addresses every row absolutely (its requests' q_start).
+  auto run_layer = [&](const Part& pt, int l, __bf16* xr, const WorkArgs& wl, const int4* step_dreq) -> int {
     const duet_block_weights& wt = wts[l];
+    const size_t r0 = (size_t)pt.row0;
+    __bf16* h = hb + r0 * d;
+    __bf16* qkv = qkvb + r0 * d_qkv;
+    __bf16* gu = gub + r0 * 2 * m;
+    __bf16* act = actb + r0 * m;
+    auto gemm = [&](const __bf16* in, const void* wm, __bf16* out, int d_in, int d_out, bool acc) {
+      return gemm_bf16(ctx->gemm, in, wm, out, pt.rows, d_in, d_out, acc, pt.gemm_ws, pt.st, &msg);
+    };
     AttnArgs al = a;
-    al.q = qb;
+    al.q = step_dreq ? qb + r0 * d : qb;
     al.k_cache = k_l[l];
     al.v_cache = v_l[l];
-    al.out = ab;
-    for (const Part& pt : parts) {
-      const size_t r0 = (size_t)pt.row0;
-      HIP_TRY(launch_rmsnorm(xb + r0 * d, static_cast<const __bf16*>(wt.attn_norm), hb + r0 * d, pt.rows, d, eps, pt.st));
-      if (gemm(pt, hb, wt.w_qkv, qkvb, d, d_qkv, false)) return fail(DUET_EHIP, "QKV projection: %s", msg);
-      QkvSplitArgs qs;
-      qs.qkv = qkvb;
-      qs.q = qb;
-      qs.k_cache = static_cast<__bf16*>(k_l[l]);
-      qs.v_cache = static_cast<__bf16*>(v_l[l]);
-      qs.meta = w.meta;
-      qs.page_table = page_table;
-      qs.num_phys_pages = num_phys_pages;
-      qs.err = w.err;
-      qs.num_reqs = batch->num_reqs;
-      qs.max_pages = max_pages_per_req;
-      qs.h_q = shape->num_q_heads;
-      qs.h_kv = shape->num_kv_heads;
-      qs.head_dim = shape->head_dim;
-      qs.row0 = pt.row0;
-      HIP_TRY(launch_qkv_split(qs, pt.rows, pt.st));
-      if (pt.decode) {
-        HIP_TRY(launch_decode_partial(al, w, pt.st));
-        HIP_TRY(launch_decode_reduce(al, w, pt.st));
-      }
-      if (pt.prefill) HIP_TRY(launch_prefill(al, w, pt.st));
-      if (gemm(pt, ab, wt.w_o, xb, d, d, true)) return fail(DUET_EHIP, "output projection: %s", msg);
-      HIP_TRY(launch_rmsnorm(xb + r0 * d, static_cast<const __bf16*>(wt.ffn_norm), hb + r0 * d, pt.rows, d, eps, pt.st));
-      if (gemm(pt, hb, wt.w_gate_up, gub, d, 2 * m, false)) return fail(DUET_EHIP, "gate-up projection: %s", msg);
-      HIP_TRY(launch_swiglu(gub + r0 * 2 * m, actb + r0 * m, pt.rows, m, pt.st));
-      if (gemm(pt, actb, wt.w_down, xb, m, d, true)) return fail(DUET_EHIP, "down projection: %s", msg);
+    al.out = step_dreq ? ab + r0 * d : ab;
+    HIP_TRY(launch_rmsnorm(xr, static_cast<const __bf16*>(wt.attn_norm), h, pt.rows, d, eps, pt.st));
+    if (gemm(h, wt.w_qkv, qkv, d, d_qkv, false)) return fail(DUET_EHIP, "QKV projection: %s", msg);
+    QkvSplitArgs qs;
+    qs.qkv = step_dreq ? qkv : qkvb;
+    qs.q = static_cast<__bf16*>(const_cast<void*>(al.q));
+    qs.k_cache = static_cast<__bf16*>(k_l[l]);
+    qs.v_cache = static_cast<__bf16*>(v_l[l]);
+    qs.meta = wl.meta;
+    qs.dreq = step_dreq;
+    qs.page_table = page_table;
+    qs.num_phys_pages = num_phys_pages;
+    qs.err = w.err;
+    qs.num_reqs = batch->num_reqs;
+    qs.max_pages = max_pages_per_req;
+    qs.h_q = shape->num_q_heads;
+    qs.h_kv = shape->num_kv_heads;
+    qs.head_dim = shape->head_dim;
+    qs.row0 = step_dreq ? 0 : pt.row0;
+    HIP_TRY(launch_qkv_split(qs, pt.rows, pt.st));
+    if (pt.decode) {
+      HIP_TRY(launch_decode_partial(al, wl, pt.st));
+      HIP_TRY(launch_decode_reduce(al, wl, pt.st));
     }
+    if (pt.prefill) HIP_TRY(launch_prefill(al, wl, pt.st));
+    const __bf16* attn_rows = ab + r0 * d;
+    if (gemm(attn_rows, wt.w_o, xr, d, d, true)) return fail(DUET_EHIP, "output projection: %s", msg);
+    HIP_TRY(launch_rmsnorm(xr, static_cast<const __bf16*>(wt.ffn_norm), h, pt.rows, d, eps, pt.st));
+    if (gemm(h, wt.w_gate_up, gu, d, 2 * m, false)) return fail(DUET_EHIP, "gate-up projection: %s", msg);
+    HIP_TRY(launch_swiglu(gu, act, pt.rows, m, pt.st));
+    if (gemm(act, wt.w_down, xr, m, d, true)) return fail(DUET_EHIP, "down projection: %s", msg);
+    return DUET_OK;
+  };
+  __bf16* xb = static_cast<__bf16*>(x);
+  for (int l = 0; l < layers; ++l)
+    for (const Part& pt : parts)
+      if ((rc = run_layer(pt, l, xb + (size_t)pt.row0 * d, w, nullptr))) return rc;
+  // Look-ahead decode steps 1 .. steps - 1 (Section 4.3): the decode partition runs every layer
+  // again for its requests' next tokens, whose residual rows the caller passed in x_ahead; step s
+  // writes its tokens' keys and values at position cached_len + s before attending.
+  const Part dpart = forked ? parts[0] : Part{order, dec0, n_dec, true, false, ws + B.gemm_ws[0]};
+  if (prof && steps > 1 && forked) HIP_TRY(hipEventRecord(ctx->ev_step[1], dpart.st));
+  for (int st = 1; st < steps; ++st) {
+    const StepPlan& spl = p.ahead[st - 1];
+    WorkArgs wl = w;
+    wl.meta = reinterpret_cast<const int4*>(ws + spl.off_meta);
+    wl.dreq = reinterpret_cast<const int4*>(ws + spl.off_dreq);
+    wl.ditems = reinterpret_cast<const int4*>(ws + spl.off_ditems);
+    wl.n_dreq = (int)spl.dreq.size();
+    wl.n_ditems = (int)spl.ditems.size();
+    wl.max_split = spl.max_split;
+    for (int l = 0; l < layers; ++l)
+      if ((rc = run_layer(dpart, l, static_cast<__bf16*>(x_ahead[st - 1]), wl, wl.dreq))) return rc;
+    if (prof && forked) HIP_TRY(hipEventRecord(ctx->ev_step[st + 1], dpart.st));
   }
   bool dec_part = false, pre_part = false;
   if (forked) {
     hipEvent_t joins[2] = {ctx->ev_djoin, ctx->ev_pjoin};
     for (size_t i = 0; i < parts.size(); ++i) {
-      if (prof) HIP_TRY(hipEventRecord(parts[i].decode ? ctx->ev_step[1] : ctx->ev_pre[1], parts[i].st));
+      if (prof && (!parts[i].decode || steps == 1))
+        HIP_TRY(hipEventRecord(parts[i].decode ? ctx->ev_step[1] : ctx->ev_pre[1], parts[i].st));
       dec_part |= parts[i].decode;
       pre_part |= parts[i].prefill;
       HIP_TRY(hipEventRecord(joins[i], parts[i].st));
@@ -1090,7 +1132,7 @@ int block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape
   ctx->prof_decode = dec_part;
   ctx->prof_prefill = pre_part;
   ctx->prof_layers = 1;
-  ctx->prof_steps = 1;
+  ctx->prof_steps = steps;
   return DUET_OK;
 }
 
@@ -1189,15 +1231,17 @@ int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_
 }
 
 int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
-                               size_t* bytes) {
+                               int32_t k_decode_steps, size_t* bytes) {
   clear_error();
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_batch(shape, batch, false))) return rc;
   if ((rc = check_block_exec(shape, block))) return rc;
   if (!bytes) return fail(DUET_EINVAL, "bytes is NULL");
+  if (k_decode_steps < 1 || k_decode_steps > kMaxLookahead)
+    return fail(DUET_EINVAL, "k_decode_steps %d not in [1, %d]", k_decode_steps, kMaxLookahead);
   Plan p;
-  plan_batch(shape, batch, 1, 1, &p, false);
+  plan_batch(shape, batch, 1, k_decode_steps, &p, false);
   int64_t T = 0;
   for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
   *bytes = block_layout(shape, block, T, p.total).total;
@@ -1205,13 +1249,13 @@ int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* 
 }
 
 int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* block,
-                       const duet_block_weights* weights, float norm_eps, void* x, void* const* k_cache,
-                       void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                       const duet_block_weights* weights, float norm_eps, void* x, void* const* x_ahead,
+                       void* const* k_cache, void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,
                        int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
                        size_t workspace_bytes, void* stream) {
   clear_error();
-  return block_forward(ctx, shape, block, weights, norm_eps, x, k_cache, v_cache, num_phys_pages, page_table,
-                       max_pages_per_req, batch, split, workspace, workspace_bytes, stream);
+  return block_forward(ctx, shape, block, weights, norm_eps, x, x_ahead, k_cache, v_cache, num_phys_pages,
+                       page_table, max_pages_per_req, batch, split, workspace, workspace_bytes, stream);
 }
 
 int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,

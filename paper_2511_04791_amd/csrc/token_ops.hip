@@ -73,7 +73,8 @@ __global__ __launch_bounds__(256) void swiglu_bf16(const __bf16* gu, __bf16* a, 
 // Row r0 + blockIdx.x of the QKV projection [rows, (h_q + 2 h_kv) d]: its h_q d query columns go
 // to q (row stride h_q d); its key and value columns go to slot pos % 16 of the physical page
 // holding absolute position pos = cached_len + (row - q_start) of its request (found by binary
-// search over the request table, whose q_start rise with the request index).  A page id outside
+// search over the request table, whose q_start rise with the request index), or, in a look-ahead
+// step, of decode request `row` of the step (its token at the step's cached_len).  A page id outside
 // [0, num_phys_pages) is not written through: it sets bit 0 of the error word.
 __global__ __launch_bounds__(256) void qkv_split_bf16(QkvSplitArgs s) {
   const int row = s.row0 + blockIdx.x;
@@ -85,13 +86,17 @@ __global__ __launch_bounds__(256) void qkv_split_bf16(QkvSplitArgs s) {
     for (int c = threadIdx.x; c < nq / 8; c += blockDim.x) qd[c] = qs[c];
   }
   int lo = 0, hi = s.num_reqs - 1;  // last request with q_start <= row
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (s.meta[mid].y <= row) lo = mid;
-    else hi = mid - 1;
+  if (s.dreq) {
+    lo = s.dreq[row].x;
+  } else {
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s.meta[mid].y <= row) lo = mid;
+      else hi = mid - 1;
+    }
   }
   const int4 m = s.meta[lo];
-  const int pos = m.w + (row - m.y);
+  const int pos = s.dreq ? m.w : m.w + (row - m.y);
   const int id = s.page_table[(size_t)lo * s.max_pages + (pos >> 4)];
   if (id < 0 || (long long)id >= s.num_phys_pages) {
     if (threadIdx.x == 0) atomicOr(s.err, 1);

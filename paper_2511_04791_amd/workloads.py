@@ -385,3 +385,18 @@ def make_block_tensors(batch: Batch, ffn_dim: int, layers: int, seed: int, *, de
         _, kc, vc = make_tensors(batch, seed + 1 + l, device=device)
         caches.append((kc, vc))
     return x, weights, caches
+
+
+def make_block_ahead(batch: Batch, k: int, seed: int, *, device="cpu"):
+    """Residual rows of look-ahead decode steps 1 .. k - 1 for an L-block forward: k - 1 bf16
+    tensors [R_d, h_q d] (decode requests in batch order), N(0,1), drawn in step order with a
+    torch generator on `device`."""
+    import torch
+
+    sh = batch.shape
+    n_dec = int((batch.kinds == KIND_DECODE).sum())
+    gen = torch.Generator(device=torch.device(device))
+    gen.manual_seed(int(seed))
+    d = sh.num_q_heads * sh.head_dim
+    return [torch.randn(n_dec, d, generator=gen, device=torch.device(device)).to(torch.bfloat16)
+            for _ in range(k - 1)]

@@ -141,17 +141,19 @@ def test_block_workspace_and_validation(native):
     attn, blk = ctypes.c_size_t(), ctypes.c_size_t()
     full = N.BlockShape(1024, 0, 3)
     assert native.duet_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(b), ctypes.byref(attn)) == 0
-    assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(full), ctypes.byref(b),
+    assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(full), ctypes.byref(b), 1,
                                              ctypes.byref(blk)) == 0
     T, d, d_qkv, m = 101, 4096, 6144, 1024
     # the attention workspace, six activation buffers and two 32 MiB GEMM workspaces
     assert blk.value >= attn.value + T * 2 * (3 * d + d_qkv + 2 * m + m) + 2 * (32 << 20)
     for bad, code in ((N.BlockShape(1024, 0, 0), -2), (N.BlockShape(1020, 0, 3), -1), (N.BlockShape(0, 0, 3), -1)):
-        assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(bad), ctypes.byref(b),
+        assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(bad), ctypes.byref(b), 1,
                                                  ctypes.byref(blk)) == code
     assert native.duet_block_workspace_bytes(ctypes.byref(_shape(dtype=N.F32, head_dim=64, num_q_heads=4,
                                                                  num_kv_heads=2)), ctypes.byref(full),
-                                             ctypes.byref(b), ctypes.byref(blk)) == -2
+                                             ctypes.byref(b), 1, ctypes.byref(blk)) == -2
+    assert native.duet_block_workspace_bytes(ctypes.byref(_shape()), ctypes.byref(full), ctypes.byref(b), 0,
+                                             ctypes.byref(blk)) == -1
 
 
 def test_block_forward_rejects_bad_arguments_before_any_launch(native):
@@ -160,5 +162,5 @@ def test_block_forward_rejects_bad_arguments_before_any_launch(native):
     caches = (ctypes.c_void_p * 1)(16)
     # no context
     assert native.duet_block_forward(None, ctypes.byref(_shape()), ctypes.byref(N.BlockShape(1024, 0, 3)), w, 1e-5,
-                                     32, caches, caches, 10, 64, 1, ctypes.byref(b), N.CuSplit(N.AGG, 256, 0, 1), 48,
+                                     32, None, caches, caches, 10, 64, 1, ctypes.byref(b), N.CuSplit(N.AGG, 256, 0, 1), 48,
                                      1 << 30, None) == -1

@@ -112,3 +112,48 @@ def test_block_forward_rejects_interleaved_kinds_under_split(ctx):
     with pytest.raises(duet.DuetError):
         ctx.block_forward(*args, duet.CuSplit.split(128, 128))
     ctx.block_forward(*args, duet.CuSplit.agg(), check_errors=True)  # aggregated execution takes any order
+
+
+@pytest.mark.parametrize("split", ["agg", "96/160"])
+def test_block_forward_lookahead(ctx, split):
+    """k = 3 decode steps in one call: step s writes its tokens at cached_len + s and attends over
+    them; every step's residual rows against the oracle run step by step on the carried caches."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from oracle.block import block_forward
+    k, L, ffn = 3, 2, 512
+    sh = wl.AttnShape(4, 2, 128, "bf16")
+    b = wl.make_batch(sh, [(1, 1, 300), (1, 1, 17), (1, 1, 40), (0, 50, 10)], page_seed=4103, reserve_tokens=k)
+    x, weights, caches = wl.make_block_tensors(b, ffn, L, 4103, device="cpu")
+    xa = wl.make_block_ahead(b, k, 4104, device="cpu")
+    sp = duet.CuSplit.agg(k) if split == "agg" else duet.CuSplit.split(96, 160, k)
+    xg, xag = x.cuda(), [t.cuda() for t in xa]
+    kcs, vcs = [c[0].cuda() for c in caches], [c[1].cuda() for c in caches]
+    print(f"[block] look-ahead k={k} split={sp}", flush=True)
+    ctx.block_forward(xg, [{n: v.cuda() for n, v in w.items()} for w in weights], kcs, vcs,
+                      torch.as_tensor(b.page_table, device="cuda"), b.seq_meta, ffn, sp, x_ahead=xag,
+                      check_errors=True)
+    torch.cuda.synchronize()
+    w64 = [{n: to64(v) for n, v in w.items()} for w in weights]
+    kw = dict(h_q=4, h_kv=2, d_h=128, eps=EPS, page_size=16)
+    ref, kc, vc = block_forward(to64(x), w64, [to64(c[0]) for c in caches], [to64(c[1]) for c in caches],
+                                b.page_table, b.seq_meta, **kw)
+    outs = [(to64(xg), ref)]
+    dec = [r for r in range(b.num_reqs) if b.kinds[r] == 1]
+    for s in range(1, k):
+        meta = np.array([(1, i, 1, int(b.cached_lens[r]) + s) for i, r in enumerate(dec)], dtype=np.int32)
+        ref_s, kc, vc = block_forward(to64(xa[s - 1]), w64, kc, vc, b.page_table[dec], meta, **kw)
+        outs.append((to64(xag[s - 1]), ref_s))
+    for s, (got, want) in enumerate(outs):
+        err = np.abs(got - want)
+        print(f"[block] step {s}: max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
+        assert np.isfinite(got).all()
+        assert err.max() <= 9 * L * U * np.abs(want).max(), f"step {s}"
+        assert err.mean() <= 9 * L * U / 4 * np.abs(want).mean(), f"step {s}"
+    if split != "agg":
+        ctx.set_profiling(1)
+        ctx.block_forward(xg, [{n: v.cuda() for n, v in w.items()} for w in weights], kcs, vcs,
+                          torch.as_tensor(b.page_table, device="cuda"), b.seq_meta, ffn, sp, x_ahead=xag)
+        t = ctx.last_kernel_times()
+        ctx.set_profiling(0)
+        assert t["decode_steps"] == k and 0 < t["decode_first_step_us"] <= t["decode_total_us"] <= t["iteration_us"]
