@@ -489,6 +489,63 @@ def serve_main(args):
     ctx.close()
 
 
+def block_lookahead(args, L, ffn):
+    """Look-ahead decode over whole blocks (Section 4.3): one call runs the 2048-token chunk once
+    and --block-k decode steps of the 64 decodes (step s's residual rows are fresh synthetic rows).
+    Split 160/96 (prefill/decode CUs, k steps back to back on the decode CUs) against the same work
+    aggregated and against one aggregated step."""
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+
+    k = args.block_k
+    batch = wl.llama8b_mixed(reserve_tokens=k)
+    ctx = duet.Context(0)
+    x, weights, caches = wl.make_block_tensors(batch, ffn, L, seed=5005, device="cuda")
+    xa = wl.make_block_ahead(batch, k, 5006, device="cuda")
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    del caches
+    pt = torch.as_tensor(batch.page_table, device="cuda")
+    meta = batch.seq_meta
+    n_dec = int((batch.kinds == 1).sum())
+    q_pre = int(batch.q_lens[batch.kinds == 0].sum())
+    st = torch.cuda.current_stream()
+    rows = []
+    for name, sp in (("SPLIT(160,96)", duet.CuSplit.split(160, 96, k)), ("AGG", duet.CuSplit.agg(k)),
+                     ("AGG one step", duet.CuSplit.agg(1))):
+        kk = sp.k_decode_steps
+
+        def run(n):
+            for _ in range(n):
+                ctx.block_forward(x, weights, kcs, vcs, pt, meta, ffn, sp, x_ahead=xa[:kk - 1])
+
+        run(args.warmup)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        run(args.steps)
+        e1.record(st)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        ctx.set_profiling(1)
+        run(1)
+        t = ctx.last_kernel_times()
+        ctx.set_profiling(0)
+        row = {"mode": name, "k": kk, "call_us": round(us, 1), "decode_tokens_per_s": round(n_dec * kk / us * 1e6, 1),
+               "prefill_tokens_per_s": round(q_pre / us * 1e6, 1)}
+        if sp.mode == duet.SPLIT:
+            row["decode_step_us"] = round(t["decode_step_us"], 1)
+            row["first_decode_step_ready_us"] = round(t["decode_start_us"] + t["decode_first_step_us"], 1)
+        rows.append(row)
+    print(json.dumps({"metric": "block look-ahead call latency (us)", "value": rows[0]["call_us"], "unit": "us",
+                      "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": False,
+                      "dtype": "bf16", "data": "synthetic",
+                      "config": {"workload": f"llama3-8b, {L} transformer blocks (random-init weights, FFN {ffn}): 1 "
+                                             "prefill chunk of 2048 tokens + 64 decodes, k decode steps per call",
+                                 "k": k}, "rows": rows}), flush=True)
+    ctx.close()
+
+
 def block_main(args):
     """Whole transformer blocks (Section 4.1: the token-level operators around attention) on the
     Llama-3-8B mixed batch: --layers (default 32) blocks of random-init bf16 weights (d 4096,
@@ -503,6 +560,8 @@ def block_main(args):
 
     L = args.layers if args.layers is not None else 32
     ffn = 14336
+    if args.block_k > 1:
+        return block_lookahead(args, L, ffn)
     batch = wl.llama8b_mixed()
     ctx = duet.Context(0)
     if not args.no_calibrate:
@@ -612,6 +671,8 @@ def main():
     ap.add_argument("--serve", action="store_true",
                     help="run the serving loop: the native engine forms the trace's iterations over whole blocks, "
                          "aggregated vs adaptive vs static splits")
+    ap.add_argument("--block-k", type=int, default=1,
+                    help="with --block: decode steps per call (look-ahead), split 160/96 vs aggregated")
     ap.add_argument("--block", action="store_true",
                     help="run whole transformer blocks (token-level operators around attention) on the Llama-3-8B "
                          "mixed batch instead")
