@@ -55,6 +55,12 @@ static int plan_for(GemmCache* c, int n, int d_in, int d_out, GemmPlan** out, co
     *out = &it->second;
     return 0;
   }
+  // A serving loop meets many row counts: keep the cache bounded (plans are cheap to re-make).
+  constexpr size_t kMaxPlans = 512;
+  if (c->plans.size() >= kMaxPlans) {
+    for (auto& kv : c->plans) destroy_plan(kv.second);
+    c->plans.clear();
+  }
   GemmPlan p;
   const hipblasOperation_t no = HIPBLAS_OP_N;
   bool ok = hipblasLtMatmulDescCreate(&p.op, HIPBLAS_COMPUTE_32F, HIP_R_32F) == HIPBLAS_STATUS_SUCCESS &&
