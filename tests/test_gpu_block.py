@@ -157,3 +157,46 @@ def test_block_forward_lookahead(ctx, split):
         t = ctx.last_kernel_times()
         ctx.set_profiling(0)
         assert t["decode_steps"] == k and 0 < t["decode_first_step_us"] <= t["decode_total_us"] <= t["iteration_us"]
+
+
+def test_engine_driven_iterations_carry_the_cache(ctx):
+    """Six iterations formed by the serving engine (chunked prefill, then decodes) over one page
+    pool: each iteration's block forward appends its tokens' keys and values, and later iterations
+    attend over them.  Every iteration against the oracle run iteration by iteration on caches
+    carried from the previous one (split 128/128 whenever both kinds are present)."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from oracle.block import block_forward
+    sh = wl.AttnShape(4, 2, 128, "bf16")
+    L, ffn, pool, max_pages = 2, 256, 64, 16
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(4105)
+    weights = wl.block_weights(sh, ffn, L, gen)
+    kc = [(torch.randn(pool, 2, 16, 128, generator=gen) * 0.1).to(torch.bfloat16) for _ in range(L)]
+    vc = [(torch.randn(pool, 2, 128, 16, generator=gen) * 0.1).to(torch.bfloat16) for _ in range(L)]
+    wg = [{n: v.cuda() for n, v in w.items()} for w in weights]
+    w64 = [{n: to64(v) for n, v in w.items()} for w in weights]
+    kcg, vcg = [t.cuda() for t in kc], [t.cuda() for t in vc]
+    k64, v64 = [to64(t) for t in kc], [to64(t) for t in vc]
+    eng = duet.Engine(48, pool, max_pages, shuffle_seed=3)
+    eng.add_request(70, 4)
+    eng.add_request(20, 3)
+    kw = dict(h_q=4, h_kv=2, d_h=128, eps=EPS, page_size=16)
+    for it in range(6):
+        if it == 2:
+            eng.add_request(30, 2)
+        meta, table, _ = eng.step()
+        assert len(meta)
+        x = torch.randn(int(meta[:, 2].sum()), 512, generator=gen).to(torch.bfloat16)
+        both = (meta[:, 0] == 0).any() and (meta[:, 0] == 1).any()
+        sp = duet.CuSplit.split(128, 128) if both else duet.CuSplit.agg()
+        xg = x.cuda()
+        ctx.block_forward(xg, wg, kcg, vcg, torch.as_tensor(table, device="cuda"), meta, ffn, sp, check_errors=True)
+        torch.cuda.synchronize()
+        ref, k64, v64 = block_forward(to64(x), w64, k64, v64, table, meta, **kw)
+        err = np.abs(to64(xg) - ref)
+        print(f"[block] engine iteration {it}: rows={len(meta)} tokens={x.shape[0]} {sp} max_abs={err.max():.3e}",
+              flush=True)
+        assert err.max() <= 9 * L * U * np.abs(ref).max() and err.mean() <= 9 * L * U / 4 * np.abs(ref).mean()
+        eng.complete()
+    eng.close()
