@@ -233,15 +233,23 @@ int duet_choose_cu_split_model(const duet_model* m, const duet_shape* shape, con
 
 /* ---- GPU context ----------------------------------------------------------------------------- */
 
-/* Context on HIP device `device`: checks for gfx950 and 256 CUs, creates the CU-masked stream
+/* Infrastructure (no passage of its own): the device state every call below uses.
+ * Context on HIP device `device`: checks for gfx950 and 256 CUs, creates the CU-masked stream
  * pool lazily (one stream per distinct CU set, kept for the context's lifetime), events and
- * pinned staging buffers, and a latency model with nominal tables. */
+ * pinned staging buffers, and a latency model with nominal tables.  *out is owned by the caller
+ * and released with duet_destroy. */
 int duet_init(int device, duet_ctx** out);
+/* duet_init, then the context's latency model loaded from `model_path`, a file written by
+ * duet_model_save after calibration (Section 4.2: the per-partition throughput tables are
+ * profiled once, ahead of serving, and reused).  DUET_EIO if the file cannot be read or parsed;
+ * then nothing is created. */
+int duet_init_with_model(int device, const char* model_path, duet_ctx** out);
 int duet_destroy(duet_ctx* ctx);
 /* The context's own latency model (owned by the context; valid until duet_destroy). */
 duet_model* duet_ctx_model(duet_ctx* ctx);
 
-/* Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
+/* Infrastructure (memory sizing for the iteration of Section 4.3).
+ * Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
  * and batch: an error word, the decode work-queue counters, metadata, work lists and two
  * buffers of split-K partials (consecutive layers alternate between them).  The layers of a call
  * share all of it, so the size does not depend on shape->num_layers.  Host only. */
@@ -423,12 +431,16 @@ int duet_set_decode_graphs(duet_ctx* ctx, int32_t enable);
 /* Graphs held by the context, and how many decode-step graphs were captured / replayed so far. */
 int duet_decode_graph_stats(duet_ctx* ctx, int64_t* cached, int64_t* captured, int64_t* replayed);
 
-/* Synchronises `stream`, reads the workspace's error word and clears it: DUET_OK or DUET_EPAGE. */
+/* Infrastructure (the page-table contract of the paged cache, Section 2): the kernels never
+ * dereference a page id outside [0, num_phys_pages) and record one in the workspace's error word.
+ * Synchronises `stream`, reads the error word and clears it: DUET_OK or DUET_EPAGE. */
 int duet_check_device_error(duet_ctx* ctx, void* workspace, void* stream);
 
-/* Copy request `req`'s logical keys (which == 0, from a token-major cache) or values (which == 1,
+/* Section 2: attention reads each request's cached keys and values through its page table.
+ * Copy request `req`'s logical keys (which == 0, from a token-major cache) or values (which == 1,
  * from a dim-major cache) into out_contig [kv_len, h_kv, d] -- the page gather the attention
- * kernels perform, exported so it can be checked bit for bit. */
+ * kernels perform, exported so it can be checked bit for bit.  Device pointers are the
+ * caller's; page ids outside the pool set the error word of duet_check_device_error. */
 int duet_gather_kv(duet_ctx* ctx, const duet_shape* shape, int32_t which, const void* cache,
                    int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
                    int32_t req, int32_t kv_len, void* out_contig, void* stream);

@@ -310,13 +310,16 @@ class Context:
     created stream, not the legacy default one: HIP ties every launch on the CU-masked streams to
     work pending on the default stream, which slows back-to-back iterations by about 10%."""
 
-    def __init__(self, device: int = 0):
+    def __init__(self, device: int = 0, model_path: str | None = None):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU visible: the HIP library needs an MI355X")
         self.device = device
         h = ctypes.c_void_p()
-        N.check(N.lib().duet_init(device, ctypes.byref(h)), "duet_init")
+        if model_path is None:
+            N.check(N.lib().duet_init(device, ctypes.byref(h)), "duet_init")
+        else:
+            N.check(N.lib().duet_init_with_model(device, model_path.encode(), ctypes.byref(h)), "duet_init_with_model")
         self.handle = h
         self.model = Model(N.lib().duet_ctx_model(h), owner=self)
         self._ws = None

@@ -73,6 +73,7 @@ _SIGS = {
     "duet_choose_cu_split_model": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(Batch), c_double, c_int32,
                                              P(CuSplit), P(c_double), P(c_double), P(c_int32)]),
     "duet_init": (c_int32, [c_int32, P(c_void_p)]),
+    "duet_init_with_model": (c_int32, [c_int32, ctypes.c_char_p, P(c_void_p)]),
     "duet_destroy": (c_int32, [c_void_p]),
     "duet_ctx_model": (c_void_p, [c_void_p]),
     "duet_workspace_bytes": (c_int32, [P(Shape), P(Batch), P(c_size_t)]),

@@ -38,10 +38,7 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
-#ifndef DUET_DECODE_RING
-#define DUET_DECODE_RING 4
-#endif
-constexpr int kRing = DUET_DECODE_RING;  // page buffers per wave: kRing - 1 pages in flight
+constexpr int kRing = 4;  // page buffers per wave: kRing - 1 pages in flight
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
@@ -69,23 +66,12 @@ __device__ __forceinline__ float sum_rows(float x) {
   return __uint_as_float(s32[0]) + __uint_as_float(s32[1]);
 }
 
-// K/V pages are read exactly once per iteration.
-#ifdef DUET_DECODE_NT_LOADS
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-template <typename T>
-__device__ __forceinline__ T stream_load(const char* p) {
-  if constexpr (sizeof(T) == 16)
-    return __builtin_bit_cast(T, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
-  else
-    return __builtin_bit_cast(T, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p)));
-}
-#else
+// K/V pages are read exactly once per iteration (plain loads: non-temporal loads were measured
+// slower under the split).
 template <typename T>
 __device__ __forceinline__ T stream_load(const char* p) {
   return *reinterpret_cast<const T*>(p);
 }
-#endif
 
 __device__ __forceinline__ uint64_t low_elems_mask(int n) {  // keep the first n of 4 bf16
   return n >= 4 ? ~0ull : (n <= 0 ? 0ull : ((1ull << (16 * n)) - 1ull));
@@ -198,9 +184,6 @@ __device__ __forceinline__ void merge_pair(const AttnArgs& a, const WorkArgs& w,
 // the current item's last pages are computed.  Each item is processed in groups of kRing pages
 // (the last group padded with masked pages that re-read the item's last page), so a page's
 // buffer is known at compile time and a load is never separated from its use by an early exit.
-#ifndef DUET_DECODE_MIN_BLOCKS_PER_CU
-#define DUET_DECODE_MIN_BLOCKS_PER_CU 1
-#endif
 // Per-wave LDS staging of finished items' partials (floats): up to kStageFloats / (g d + 2 g)
 // items (7 for g = 4, d = 128) are written out together, when the buffer is full or the wave's
 // work is done.  A store's completion comes back late while the memory system streams reads, and
@@ -208,7 +191,7 @@ __device__ __forceinline__ void merge_pair(const AttnArgs& a, const WorkArgs& w,
 // after it until it completes: one burst per buffer instead of one per item.
 constexpr int kStageFloats = 4096;
 template <int D, int PPS>
-__global__ __launch_bounds__(256, DUET_DECODE_MIN_BLOCKS_PER_CU) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
+__global__ __launch_bounds__(256, 1) void decode_partial_bf16(AttnArgs a, WorkArgs w) {
   constexpr int R = kRing;
   static_assert(PPS % R == 0, "a split must hold whole groups of ring pages");
   const int lane = threadIdx.x & 63;
@@ -543,16 +526,12 @@ __global__ __launch_bounds__(256) void decode_reduce(AttnArgs a, WorkArgs w) {
 
 }  // namespace
 
-#ifndef DUET_DECODE_MIN_ROUNDS
-#define DUET_DECODE_MIN_ROUNDS 4
-#endif
-#ifndef DUET_DECODE_MIN_WAVES_PER_CU
-#define DUET_DECODE_MIN_WAVES_PER_CU 4
-#endif
+constexpr int kMinRounds = 4;      // items per wave the persistent grid is sized for, at least
+constexpr int kMinWavesPerCu = 4;  // waves per CU of the share, at least
 
 // Persistent grid size.  The memory system needs far fewer waves in flight than fit, so the grid
-// is sized for at least DUET_DECODE_MIN_ROUNDS items per wave (a short tail when the last items
-// finish), but never below DUET_DECODE_MIN_WAVES_PER_CU waves per CU (bandwidth on small CU
+// is sized for at least kMinRounds items per wave (a short tail when the last items
+// finish), but never below kMinWavesPerCu waves per CU (bandwidth on small CU
 // shares) nor above what is resident at once.
 template <int D>
 hipError_t launch_persistent(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
@@ -564,8 +543,8 @@ hipError_t launch_persistent(const AttnArgs& a, const WorkArgs& w, hipStream_t s
     if (per_cu < 1) per_cu = 1;
   }
   const int capacity = w.decode_cus * per_cu * 4;
-  const int floor_waves = w.decode_cus * DUET_DECODE_MIN_WAVES_PER_CU;
-  const int want = (w.n_ditems + DUET_DECODE_MIN_ROUNDS - 1) / DUET_DECODE_MIN_ROUNDS;
+  const int floor_waves = w.decode_cus * kMinWavesPerCu;
+  const int want = (w.n_ditems + kMinRounds - 1) / kMinRounds;
   const int waves = std::max(1, std::min(capacity, std::max(want, floor_waves)));
   hipLaunchKernelGGL((decode_partial_bf16<D, kDecodePagesPerSplit>), dim3((waves + 3) / 4), dim3(256), 0, s, a, w);
   return hipGetLastError();

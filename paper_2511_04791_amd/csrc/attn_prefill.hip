@@ -34,16 +34,10 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-#ifndef DUET_PREFILL_WAVES
-#define DUET_PREFILL_WAVES 8
-#endif
-constexpr int kWaves = DUET_PREFILL_WAVES;
+constexpr int kWaves = 8;  // two waves per SIMD
 constexpr int kThreads = 64 * kWaves;
-#ifndef DUET_PREFILL_STAGES
-#define DUET_PREFILL_STAGES 4
-#endif
 // LDS ring of kStages tiles: the tile in use plus kStages - 1 in flight.
-constexpr int kStages = DUET_PREFILL_STAGES;
+constexpr int kStages = 4;
 static_assert(kStages >= 2, "the ring needs a tile in use and one in flight");
 constexpr float kRescaleSlack = 8.0f;  // base-2 units: probabilities stay below 2^8
 
@@ -63,13 +57,8 @@ __device__ __forceinline__ int swap_bits23(int r) { return (r & ~12) | ((r & 4) 
 // LDS chunk swizzles.  A wave's K-operand reads touch rows swap_bits23(0..31) in groups of 8 or
 // 16 lanes; its V-operand reads touch rows 0..31 in order.  Both maps give every such lane group
 // distinct 16-byte bank groups, for both 8-lane and 16-lane LDS service.
-#ifndef DUET_PREFILL_PLAIN_SWIZZLE
 __device__ __forceinline__ int kswz(int row) { return swap_bits23(row & 15); }
 __device__ __forceinline__ int vswz(int row) { return (row & 7) ^ ((row >> 3) & 1); }
-#else
-__device__ __forceinline__ int kswz(int row) { return row & 15; }
-__device__ __forceinline__ int vswz(int row) { return row & 7; }
-#endif
 
 __device__ __forceinline__ uint32_t keep_pairs(uint32_t word, int n_valid_in_pair) {
   return n_valid_in_pair >= 2 ? word : (n_valid_in_pair == 1 ? (word & 0xffffu) : 0u);
@@ -436,12 +425,8 @@ hipError_t launch_bf16_nh(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   switch (prefill_heads_per_unit(a.group)) {
     case 1: return launch_bf16<D, 1>(a, w, s);
     case 2: return launch_bf16<D, 2>(a, w, s);
-#if DUET_PREFILL_WAVES >= 8
     case 4: return launch_bf16<D, 4>(a, w, s);
     default: return launch_bf16<D, 8>(a, w, s);
-#else
-    default: return launch_bf16<D, 4>(a, w, s);
-#endif
   }
 }
 

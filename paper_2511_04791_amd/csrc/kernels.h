@@ -56,36 +56,12 @@ struct AppendArgs {
   int32_t h_kv, head_dim, dtype;
 };
 
-#ifndef DUET_DECODE_PAGES_PER_SPLIT
-#define DUET_DECODE_PAGES_PER_SPLIT 32
-#endif
 // Decode split length in pages (bf16); fixed, so results do not depend on the CU split.
-constexpr int kDecodePagesPerSplit = DUET_DECODE_PAGES_PER_SPLIT;
+constexpr int kDecodePagesPerSplit = 32;
 constexpr int kDecodePagesPerSplitF32 = 2;
-#ifndef DUET_DECODE_TAIL_SPLITS
-#define DUET_DECODE_TAIL_SPLITS 0
-#endif
-#ifndef DUET_DECODE_TAIL_PAGES
-#define DUET_DECODE_TAIL_PAGES 8
-#endif
-// bf16 decode items: a (request, kv head) page range is cut into splits of kDecodePagesPerSplit
-// pages from its first page on; with kDecodeTailSplits > 0 the pages of its last kDecodeTailSplits
-// splits are cut into pieces of kDecodeTailPages instead, which run last, so the kernel ends with
-// short items (near its end a wave streams alone, at the rate its few pages in flight allow).  The
-// cut depends on the request's length only.  Off by default: measured, it shortens the tail on all
-// 256 CUs but costs more than it saves on smaller shares.
-constexpr int kDecodeTailSplits = DUET_DECODE_TAIL_SPLITS;
-constexpr int kDecodeTailPages = DUET_DECODE_TAIL_PAGES;
-static_assert(kDecodeTailPages <= kDecodePagesPerSplit, "tail pieces are shorter than splits");
 // Most logical pages of a bf16 decode request (an item's first page is a 22-bit field).
 constexpr long long kMaxDecodePages = (1LL << 22) - 1;
 
-#ifndef DUET_DECODE_QUEUES
-#define DUET_DECODE_QUEUES 8
-#endif
-#ifndef DUET_DECODE_QUEUE_STRIDE
-#define DUET_DECODE_QUEUE_STRIDE 32
-#endif
 // The persistent decode kernel's work queue is split into kDecodeQueues counters (items are dealt
 // round-robin to them), each on its own 128-byte line: atomics on one line are serialised, at a
 // few tens per microsecond.  A counter set is kDecodeQueues item queues followed by kDecodeQueues
@@ -93,8 +69,8 @@ constexpr long long kMaxDecodePages = (1LL << 22) - 1;
 // layers alternate: the upload zeroes both, a partial kernel clears the set the kernel before it
 // on the stream used (that kernel has finished), and a reduce kernel clears the set of the
 // partial kernel it follows.
-constexpr int kDecodeQueues = DUET_DECODE_QUEUES;
-constexpr int kDecodeQueueStride = DUET_DECODE_QUEUE_STRIDE;
+constexpr int kDecodeQueues = 8;
+constexpr int kDecodeQueueStride = 32;  // ints: one 128-byte line per counter
 constexpr int kDecodeSetLines = 2 * kDecodeQueues;
 constexpr int kDecodeSetInts = kDecodeSetLines * kDecodeQueueStride;
 constexpr int kDecodeCounterInts = 2 * kDecodeSetInts;

@@ -87,22 +87,10 @@ int pages_per_split_for(const duet_shape* s) {
 // Decode work of the batch's decode requests when each holds `extra` more tokens than seq_meta
 // states: per request (req, item_base, n_split, n_pages), and for bf16 the work items in
 // execution order -- every full split first, then the shorter last splits, longest first -- as
-// descriptors (q_start, req | kv head << 24, split | kv_len << 10, row of the split's partial).
-// With step_rows (look-ahead steps), decode request i reads its query from row i.
-// How a (request, kv head) range of n_pages pages is cut: n_long splits of pps pages from page 0
-// (the last one short when nothing follows it), then n_short tail pieces of kDecodeTailPages
-// pages (the last one short).  fp32 keeps uniform splits.
-struct SplitShape {
-  int n_long, n_short;
-};
-SplitShape split_shape(int n_pages, int pps, bool graded) {
-  const int n = (n_pages + pps - 1) / pps;
-  if (!graded || kDecodeTailSplits == 0) return {n, 0};
-  const int n_long = std::max(0, n - kDecodeTailSplits);
-  const int rest = n_pages - n_long * pps;
-  return {n_long, (rest + kDecodeTailPages - 1) / kDecodeTailPages};
-}
-
+// descriptors (q_start, req | kv head << 24, first page | (tokens - 1) << 22, row of the split's
+// partial).  With step_rows (look-ahead steps), decode request i reads its query from row i.
+// A (request, kv head) range of n_pages pages is cut into splits of pps pages from page 0, the
+// last one short.
 void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step_rows, bool fill,
                   std::vector<int4>* dreq, std::vector<int4>* ditems, int64_t* n_dreq, int64_t* n_items,
                   int* max_split) {
@@ -117,8 +105,7 @@ void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step
     if (q.kind != DUET_KIND_DECODE) continue;
     const int64_t L = (int64_t)q.cached_len + q.q_len + extra;
     const int n_pages = (int)((L + 15) / 16);
-    const SplitShape ss = split_shape(n_pages, pps, s->dtype == DUET_BF16);
-    const int n_split = ss.n_long + ss.n_short;
+    const int n_split = (n_pages + pps - 1) / pps;
     if (fill) dreq->push_back(make_int4(r, (int)*n_items, n_split, n_pages));
     *n_items += (int64_t)s->num_kv_heads * n_split;
     *max_split = std::max(*max_split, n_split);
@@ -136,12 +123,10 @@ void decode_lists(const duet_shape* s, const duet_batch* b, int extra, bool step
       const duet_seq_meta& q = b->reqs[d.x];
       const int L = q.cached_len + q.q_len + extra;
       const int q_start = step_rows ? (int)i : q.q_start;
-      const SplitShape ss = split_shape(d.w, pps, true);
       for (int j = 0; j < s->num_kv_heads; ++j)
         for (int sp = 0; sp < d.z; ++sp) {
-          const bool tail = sp >= ss.n_long;
-          const int first = tail ? ss.n_long * pps + (sp - ss.n_long) * kDecodeTailPages : sp * pps;
-          const int tokens = std::min(16 * (tail ? kDecodeTailPages : pps), L - 16 * first);
+          const int first = sp * pps;
+          const int tokens = std::min(16 * pps, L - 16 * first);
           const int pages = (tokens + 15) / 16;
           const int4 it = make_int4(q_start, d.x | (j << 24), first | ((tokens - 1) << 22), d.y + j * d.z + sp);
           if (pages == pps) ditems->push_back(it);
@@ -1194,6 +1179,21 @@ int duet_init(int device, duet_ctx** out) {
   if (hipMalloc(&ctx->dev_flag, 256) != hipSuccess || hipMemset(ctx->dev_flag, 0, 256) != hipSuccess)
     return cleanup(fail(DUET_EHIP, "device flag allocation failed"));
   ctx->dev_sink = reinterpret_cast<unsigned*>(ctx->dev_flag) + 16;
+  *out = ctx;
+  return DUET_OK;
+}
+
+int duet_init_with_model(int device, const char* model_path, duet_ctx** out) {
+  if (!out) return fail(DUET_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!model_path) return fail(DUET_EINVAL, "model_path is NULL");
+  duet_ctx* ctx = nullptr;
+  int rc = duet_init(device, &ctx);
+  if (rc) return rc;
+  if ((rc = duet_model_load(&ctx->model, model_path))) {
+    duet_destroy(ctx);
+    return rc;
+  }
   *out = ctx;
   return DUET_OK;
 }
