@@ -1,21 +1,31 @@
 #!/usr/bin/env python3
-"""Mixed-batch attention iteration on one MI355X: latency, decode HBM GB/s, prefill MFMA TFLOP/s.
+"""Mixed-batch attention on one MI355X: iteration latency, decode HBM GB/s, prefill MFMA TFLOP/s.
 
-Workload: the attention of one serving iteration of a Llama-3-8B-shaped model -- 32 layers of
-32 query heads, 8 kv heads, head_dim 128, bf16, page size 16 -- over a synthetic mixed batch: a
-2048-token prefill chunk at prefix 0 plus 64 decode requests with contexts uniform in
-[512, 4096], pages placed by a seeded random permutation, each layer with its own Q and KV
-cache.  Inputs are resident in HBM before timing starts.
+Default run (no mode flag): three workloads of the paper's mixed serving iterations, each a
+step of the whole hot path -- the latency model and Algorithm 1's CU-split choice on the host,
+then the attention of one iteration (work lists built and uploaded once, the decode split-K and
+reduce kernels and the prefill MFMA kernel of every layer on their CU-masked streams, the fork
+and the join; with look-ahead, the decode steps replayed from graphs on the decode CUs):
 
-A step is one pass of the whole hot path: the latency model and Algorithm 1's CU-split choice
-on the host, then duet_attn_iteration (work lists built and uploaded once, the decode split-K
-and reduce kernels and the prefill MFMA kernel of every layer on their CU-masked streams, the
-fork and the join).
+  cfg4 (headline)  Llama-3-70B attention shapes (64 q-heads / 8 kv-heads / head_dim 128), one
+                   layer: an 8192-token chunk after 24576 cached tokens plus 32 decodes at 2048;
+  cfg3             Llama-3-8B shapes, one layer: 256 decodes with lognormal contexts (median
+                   8192) plus a 512-token chunk after 16384 cached, in a ~70 GB page pool;
+  cfg2             Llama-3-8B shapes, 32 layers: a 2048-token chunk plus 64 decodes with
+                   contexts U[512, 4096].
 
-Prints one JSON line.  `value` is the wall-clock time per step of K back-to-back steps between
-two device synchronisations (lower is better).  Further passes give the fork-to-join latency
-of one iteration (HIP events on the caller's stream) and per-kernel durations (HIP events on
-each kernel's own stream) behind the roofline figures.
+Each workload's TBT bound is the paper's 50 ms per decode step of the whole model, scaled to the
+layers benchmarked (Llama-3-70B has 80 layers, Llama-3-8B 32).  Algorithm 1 runs on a model
+calibrated on generic batches that are none of these.  Inputs are seeded, synthetic and
+resident in HBM before timing starts.
+
+Prints one JSON line.  `value` is the headline workload's wall-clock time per step over K
+back-to-back steps between two device synchronisations (lower is better), on the split
+Algorithm 1 chose (with its k decode steps); `agg_us` is the same work on one stream.  The
+timed region runs last, on a GPU kept busy by the passes before it.  Further passes give the
+fork-to-join latency (HIP events on the caller's stream) and per-kernel durations (HIP events
+on each kernel's own stream) behind the roofline figures, and every split of the 32-CU grid
+measured beside the model's prediction.
 """
 from __future__ import annotations
 
@@ -66,10 +76,10 @@ def source_hash(name: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def committed_traffic(kernel: str, source: str, units: float):
-    """HBM bytes per launch from the committed counter summary, if the kernel source still
-    matches the one the counters were taken on; else None."""
-    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
+def committed_traffic(kernel: str, source: str, tag: str):
+    """HBM bytes per launch from the committed counter summary of `kernel` on workload `tag`, if
+    the kernel source still matches the one the counters were taken on; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{tag}_traffic.json")
     try:
         with open(path) as f:
             t = json.load(f)
@@ -80,18 +90,23 @@ def committed_traffic(kernel: str, source: str, units: float):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
-    """The fp64 oracle on the host cores over the same inputs: decode requests (all of them, or as
-    many as fit half the time budget) plus as many prefill query heads as fit the rest, each
-    extrapolated to all requests / heads of one layer."""
+def _blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max([p_.get("num_threads", 1) for p_ in threadpool_info()] or [1]))
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def _oracle_sample(batch, q, kc, vc, budget_s, row_block=512):
+    """Times the fp64 oracle on a sample of one layer: decode requests (all, or as many as fit half
+    the budget), then prefill (query head, block of `row_block` query rows) units until the budget
+    is spent.  Every prefill unit of a request costs the same (the oracle scores every key and
+    masks), so each part is extrapolated linearly.  Returns (decode s, prefill s, description,
+    measured s) for the whole layer."""
     import numpy as np
     import torch
     from oracle import attention as oa
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
     sh = batch.shape
     dec = [r for r in range(batch.num_reqs) if batch.kinds[r] == 1]
     pre = [r for r in range(batch.num_reqs) if batch.kinds[r] == 0]
@@ -111,29 +126,58 @@ def cpu_baseline(batch, q, kc, vc, budget_s=25.0):
         if dec_done > 0 and time.perf_counter() - t0 > budget_s / 2:
             break
         K, V = logical(r)
-        s = int(batch.q_starts[r])
-        oa.attend(to64(q[s:s + 1]), K, V, int(batch.kv_lens[r]) - 1)
+        s_ = int(batch.q_starts[r])
+        oa.attend(to64(q[s_:s_ + 1]), K, V, int(batch.kv_lens[r]) - 1)
         dec_done += 1
     t_dec = time.perf_counter() - t0
-    t_pre, heads_done, heads_total = 0.0, 0, 0
+    t_pre, units_done, units_total = 0.0, 0, 0
+    g = sh.num_q_heads // sh.num_kv_heads
     for r in pre:
+        s_, ql, c = int(batch.q_starts[r]), int(batch.q_lens[r]), int(batch.cached_lens[r])
+        blocks = -(-ql // row_block)
+        units_total += sh.num_q_heads * blocks
+        if t_dec + t_pre > budget_s and units_done > 0:
+            continue
         K, V = logical(r)
-        s, ql, c = int(batch.q_starts[r]), int(batch.q_lens[r]), int(batch.cached_lens[r])
-        qh = to64(q[s:s + ql])
-        heads_total += sh.num_q_heads
-        g = sh.num_q_heads // sh.num_kv_heads
+        qh = to64(q[s_:s_ + ql])
         for h in range(sh.num_q_heads):
-            if t_dec + t_pre > budget_s and heads_done > 0:
-                break
-            t1 = time.perf_counter()
-            oa.attend(qh[:, h:h + 1], K[:, h // g:h // g + 1], V[:, h // g:h // g + 1], c)
-            t_pre += time.perf_counter() - t1
-            heads_done += 1
-    full = (t_dec * len(dec) / dec_done if dec_done else 0.0) + (t_pre * heads_total / heads_done if heads_done else 0.0)
-    sample = (f"{dec_done}/{len(dec)} decode requests and {heads_done}/{heads_total} prefill query heads of one layer, "
-              f"fp64 numpy oracle, extrapolated to the full layer")
-    return {"value": round(full * 1e6, 1), "unit": "us", "cores": int(threads), "kind": "oracle", "sample": sample,
-            "measured_s": round(t_dec + t_pre, 3)}
+            for bi in range(blocks):
+                if t_dec + t_pre > budget_s and units_done > 0:
+                    break
+                i0, i1 = bi * row_block, min(ql, (bi + 1) * row_block)
+                t1 = time.perf_counter()
+                # rows i0 .. i1 of the chunk: the keys they see end at c + i1
+                oa.attend(qh[i0:i1, h:h + 1], K[:c + i1, h // g:h // g + 1], V[:c + i1, h // g:h // g + 1], c + i0)
+                t_pre += time.perf_counter() - t1
+                units_done += 1
+    full_dec = t_dec * len(dec) / dec_done if dec_done else 0.0
+    full_pre = t_pre * units_total / units_done if units_done else 0.0
+    desc = (f"{dec_done}/{len(dec)} decode requests and {units_done}/{units_total} prefill (query head, "
+            f"{row_block}-row block) units of one layer")
+    return full_dec, full_pre, desc, t_dec + t_pre
+
+
+def cpu_baseline(batch, q, kc, vc, layers: int, k_steps: int, budget_s: float = 15.0, one_core_budget_s: float = 6.0):
+    """The fp64 oracle on the host over the same inputs (one layer's bits read back from the
+    device), timed on a bounded sample and extrapolated to the benchmark step: `layers` layers of
+    one prefill pass and `k_steps` decode steps.  Measured with every BLAS thread, then again on
+    one core."""
+    threads = _blas_threads()
+    d_all, p_all, desc, meas = _oracle_sample(batch, q, kc, vc, budget_s)
+    value = layers * (k_steps * d_all + p_all)
+    res = {"value": round(value * 1e6, 1), "unit": "us", "cores": threads, "kind": "oracle",
+           "sample": f"{desc}, fp64 numpy oracle on {threads} BLAS threads, extrapolated to {layers} layer(s) of one "
+                     f"prefill pass and {k_steps} decode step(s)",
+           "measured_s": round(meas, 2), "os_cpu_count": os.cpu_count()}
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            d1, p1, desc1, meas1 = _oracle_sample(batch, q, kc, vc, one_core_budget_s)
+        res["one_core"] = {"value": round(layers * (k_steps * d1 + p1) * 1e6, 1), "unit": "us", "cores": 1,
+                           "sample": desc1, "measured_s": round(meas1, 2)}
+    except Exception as e:  # threadpoolctl missing: report all-core only
+        res["one_core"] = {"error": str(e)}
+    return res
 
 
 WORKLOADS = {
@@ -146,11 +190,249 @@ WORKLOADS = {
                          "of 8192 tokens after 24576 cached + 32 decodes at context 2048, pages randomly placed",
 }
 
+SLO_US = 50000.0  # the paper's TBT bound: 50 ms per decode step of the whole model
+# key -> workload, benchmarked layers, layers of the whole model, most decode steps per call
+CONFIGS = {
+    "cfg4": {"workload": "prefill-heavy-70b", "layers": 1, "model_layers": 80, "k_cap": 64},
+    "cfg3": {"workload": "decode-heavy", "layers": 1, "model_layers": 32, "k_cap": 1},
+    "cfg2": {"workload": "llama8b-mixed", "layers": 32, "model_layers": 32, "k_cap": 1},
+}
 
-def make_workload(name):
+
+def make_workload(name, reserve_tokens: int = 0):
     from paper_2511_04791_amd import workloads as wl
-    return {"llama8b-mixed": wl.llama8b_mixed, "decode-heavy": wl.decode_heavy,
-            "prefill-heavy-70b": wl.prefill_heavy_70b}[name]()
+    if name == "prefill-heavy-70b":
+        return wl.prefill_heavy_70b(reserve_tokens=reserve_tokens)
+    if name == "llama8b-mixed":
+        return wl.llama8b_mixed(reserve_tokens=reserve_tokens)
+    return wl.decode_heavy()
+
+
+def _roof(achieved, peak, cus, unit, kernel, work, launch_us, probe_peak=None, traffic=None, bound="hbm"):
+    r = {"bound": bound, "kernel": kernel, "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+         "frac": round(achieved / peak, 4), "cus": cus, "share_peak": round(peak * cus / 256, 1),
+         "share_frac": round(achieved / (peak * cus / 256), 4), "launch_us": round(launch_us, 2),
+         ("algorithmic_bytes_per_launch" if bound == "hbm" else "algorithmic_flops_per_launch"): work,
+         "traffic": traffic}
+    if probe_peak:
+        r["probe_share_peak"] = round(probe_peak, 1)
+        r["probe_share_frac"] = round(achieved / probe_peak, 4)
+    return r
+
+
+def run_config(ctx, key, args, calib):
+    """One workload of the suite: Algorithm 1's choice at the workload's TBT bound against
+    aggregated execution of the same work, kernel rooflines, the split sweep and the timed steps."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+
+    spec = CONFIGS[key]
+    L, kcap = spec["layers"], spec["k_cap"]
+    batch = make_workload(spec["workload"], reserve_tokens=kcap if kcap > 1 else 0)
+    shape = dataclasses.replace(batch.shape, num_layers=L)
+    rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
+    tau = SLO_US * L / spec["model_layers"]
+    t0 = time.perf_counter()
+    chosen, pred, rho, flags = duet.choose_cu_split(rows3, tau, shape, ctx.model, max_decode_steps=kcap)
+    host_choose_us = (time.perf_counter() - t0) * 1e6
+    k = chosen.k_decode_steps
+    agg = duet.CuSplit.agg(k)                       # the same work on one stream
+    agg_pred = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), shape, ctx.model)
+    print(f"[bench] {key}: tau {tau:.0f} us -> {chosen} (predicted {pred:.0f} us, AGG {agg_pred:.0f} us, "
+          f"flags {flags})", file=sys.stderr, flush=True)
+
+    layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
+    qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
+    del layers
+    pt = torch.as_tensor(batch.page_table, device="cuda")
+    meta = batch.seq_meta
+    outs = [torch.empty_like(q) for q in qs]
+    la = [wl.make_lookahead_tensors(batch, kcap, seed=3003 + l, device="cuda") for l in range(L)] if kcap > 1 else None
+    torch.cuda.synchronize()
+
+    def caller(split):
+        kk = split.k_decode_steps
+        if kk > 1:
+            qa = [la[l][0][s_ - 1] for s_ in range(1, kk) for l in range(L)]
+            ka = [la[l][1][s_ - 1] for s_ in range(1, kk) for l in range(L)]
+            va = [la[l][2][s_ - 1] for s_ in range(1, kk) for l in range(L)]
+            oa_ = [torch.empty_like(x) for x in qa]
+            ws = ctx.workspace(duet.lookahead_workspace_bytes(shape, meta, kk))
+            return lambda: ctx.attn_lookahead(qs, qa, ka, va, kcs, vcs, pt, meta, split, outs=outs, outs_ahead=oa_,
+                                              workspace=ws)
+        ws = ctx.workspace(duet.workspace_bytes(shape, meta))
+        return lambda: ctx.attn_iteration(qs, kcs, vcs, pt, meta, split, outs=outs, workspace=ws)
+
+    def profiled(split, n=5, level=1, warm=2):
+        call = caller(split)
+        ctx.set_profiling(level)
+        rec = []
+        for i in range(warm + n):
+            call()
+            kt = ctx.last_kernel_times()
+            if i >= warm:
+                rec.append(kt)
+        ctx.set_profiling(0)
+        return {k_: statistics.fmean(r[k_] for r in rec) for k_ in rec[0]}
+
+    ctx.attn_iteration(qs, kcs, vcs, pt, meta, duet.CuSplit.agg(), outs=outs, check_errors=True)
+    # kernel durations on one decode step (k = 1) of the chosen split and of AGG
+    kern_split = profiled(duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT
+                          else duet.CuSplit.agg(), level=2)
+    kern_agg = profiled(duet.CuSplit.agg(), level=2)
+    it_chosen = profiled(chosen)
+    it_agg = profiled(agg)
+    # every split of the grid (one decode step), measured beside the model's prediction
+    sweep = []
+    for s_p in range(256 - 32, 0, -32):
+        sp_ = duet.CuSplit.split(s_p, 256 - s_p)
+        m_ = profiled(sp_, n=3, warm=1)
+        sweep.append({"Sp": s_p, "Sd": 256 - s_p, "measured_us": round(m_["iteration_us"], 1),
+                      "predicted_us": round(duet.predict_iter_latency(rows3, sp_, shape, ctx.model), 1)})
+    agg1 = it_agg if k == 1 else profiled(duet.CuSplit.agg())
+    sweep_agg = {"measured_us": round(agg1["iteration_us"], 1), "predicted_us": round(agg_pred, 1)}
+    best = min(sweep, key=lambda r: r["measured_us"])
+    errs = [(r["predicted_us"] - r["measured_us"]) / r["measured_us"] for r in sweep]
+    # Algorithm 1 under a bound 1% below the aggregated estimate: it must split, and its pick is
+    # compared with the measured sweep (the predictor's out-of-sample ranking test)
+    tight, tight_pred = duet.choose_cu_split(rows3, 0.99 * agg_pred, shape, ctx.model, max_decode_steps=1)[:2]
+    tight_row = next((r for r in sweep if tight.mode == duet.SPLIT and r["Sp"] == tight.cus_prefill), None)
+
+    # rooflines: one launch of each kernel under the chosen split and on all 256 CUs
+    dbytes, pflops = decode_bytes(batch), prefill_causal_flops(batch)
+    sd_cus = chosen.cus_decode if chosen.mode == duet.SPLIT else 256
+    sp_cus = chosen.cus_prefill if chosen.mode == duet.SPLIT else 256
+    probe = lambda name, cus: calib[name][cus // 8 - 1] if calib else None
+    dec_split = _roof(dbytes / kern_split["decode_partial_us"] / 1e3, PEAK_HBM_GBPS, sd_cus, "GB/s", "decode_partial_bf16",
+                      int(dbytes), kern_split["decode_partial_us"],
+                      probe("probe_read_tbps", sd_cus) and probe("probe_read_tbps", sd_cus) * 1e3,
+                      committed_traffic("decode_partial", "attn_decode.hip", key), "hbm")
+    dec_agg = _roof(dbytes / kern_agg["decode_partial_us"] / 1e3, PEAK_HBM_GBPS, 256, "GB/s", "decode_partial_bf16",
+                    int(dbytes), kern_agg["decode_partial_us"], probe("probe_read_tbps", 256) and
+                    probe("probe_read_tbps", 256) * 1e3, None, "hbm")
+    pre_split = _roof(pflops / kern_split["prefill_us"] / 1e6, PEAK_BF16_TFLOPS, sp_cus, "TFLOP/s", "prefill_bf16",
+                      pflops, kern_split["prefill_us"], probe("probe_mfma_tflops", sp_cus),
+                      committed_traffic("prefill", "attn_prefill.hip", key), "mfma")
+    pre_agg = _roof(pflops / kern_agg["prefill_us"] / 1e6, PEAK_BF16_TFLOPS, 256, "TFLOP/s", "prefill_bf16", pflops,
+                    kern_agg["prefill_us"], probe("probe_mfma_tflops", 256), None, "mfma")
+    decode_dominant = kern_split["decode_partial_us"] * 1 >= kern_split["prefill_us"]
+
+    # timed region, last: W warm-up steps, then K back-to-back steps, for the chosen split and for
+    # the same work aggregated
+    def timed(split):
+        call = caller(split)
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            call()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t1) / args.steps * 1e6
+
+    choose_ts = []
+
+    def timed_adaptive():
+        # the host's choice is part of every step
+        call = caller(chosen)
+
+        def step():
+            t2 = time.perf_counter()
+            duet.choose_cu_split(rows3, tau, shape, ctx.model, max_decode_steps=kcap)
+            choose_ts.append((time.perf_counter() - t2) * 1e6)
+            call()
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t1) / args.steps * 1e6
+
+    agg_wall = timed(agg)
+    wall = timed_adaptive()
+    n_dec = int((batch.kinds == 1).sum())
+    q_pre = int(batch.q_lens[batch.kinds == 0].sum())
+    res = {
+        "workload": WORKLOADS[spec["workload"]].format(L=L), "layers": L,
+        "tbt_slo_us": round(tau, 1),
+        "tbt_slo": f"{SLO_US / 1000:.0f} ms per decode step of the {spec['model_layers']}-layer model, scaled to {L} layer(s)",
+        "chosen": str(chosen), "k_decode_steps": k, "algorithm1_flags": flags,
+        "predicted_us": round(pred, 1), "agg_predicted_us": round(agg_pred, 1),
+        "host_choose_us": round(statistics.fmean(choose_ts) if choose_ts else host_choose_us, 2),
+        "wall_us": round(wall, 1), "agg_wall_us": round(agg_wall, 1), "speedup_vs_agg": round(agg_wall / wall, 4),
+        "iteration_us": round(it_chosen["iteration_us"], 1), "agg_iteration_us": round(it_agg["iteration_us"], 1),
+        "decode_tokens_per_s": round(n_dec * k / (wall * 1e-6), 1),
+        "prefill_tokens_per_s": round(q_pre / (wall * 1e-6), 1),
+        "agg_decode_tokens_per_s": round(n_dec * k / (agg_wall * 1e-6), 1),
+        "kernels_us": {k_.replace("_us", ""): round(v, 2) for k_, v in kern_split.items()},
+        "agg_kernels_us": {k_.replace("_us", ""): round(v, 2) for k_, v in kern_agg.items()},
+        "decode_roofline": {"split": dec_split, "standalone_256": dec_agg},
+        "prefill_roofline": {"split": pre_split, "standalone_256": pre_agg},
+        "roofline": dec_split if decode_dominant else pre_split,
+        "sweep": sweep, "sweep_agg": sweep_agg, "sweep_best": best,
+        "prediction_error": {"mean_abs": round(float(np.mean(np.abs(errs))), 4),
+                             "max_abs": round(float(np.max(np.abs(errs))), 4),
+                             "agg": round((agg_pred - agg1["iteration_us"]) / agg1["iteration_us"], 4)},
+        "algorithm1_tight": {"tau_us": round(0.99 * agg_pred, 1), "chosen": str(tight),
+                             "predicted_us": round(tight_pred, 1),
+                             "measured_us": tight_row and tight_row["measured_us"],
+                             "vs_sweep_best": tight_row and round(tight_row["measured_us"] / best["measured_us"], 4),
+                             "vs_agg": tight_row and round(tight_row["measured_us"] / sweep_agg["measured_us"], 4)},
+    }
+    if k > 1:
+        res["decode_step_us"] = round(it_chosen["decode_step_us"], 1)
+        res["decode_interval_max_us"] = round(it_chosen["decode_step_us"], 1)
+        res["agg_decode_interval_max_us"] = round(it_agg["prefill_total_us"] + it_agg["decode_first_step_us"], 1)
+    cpu = None
+    if not args.no_cpu_baseline and key == args.headline:
+        cpu = cpu_baseline(batch, qs[0], kcs[0], vcs[0], L, k)
+    res["cpu_baseline"] = cpu
+    del qs, kcs, vcs, outs, la
+    torch.cuda.empty_cache()
+    return res
+
+
+def suite_main(args):
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd.calibration import calibrate_model
+
+    keys = [k_.strip() for k_ in args.configs.split(",") if k_.strip()]
+    if args.headline not in keys:
+        keys.insert(0, args.headline)
+    ctx = duet.Context(0)
+    calib = {}
+    if not args.no_calibrate:
+        t0 = time.perf_counter()
+        calib = calibrate_model(ctx)
+        calib["seconds"] = round(time.perf_counter() - t0, 2)
+        print(f"[bench] calibrated in {calib['seconds']} s", file=sys.stderr, flush=True)
+    results = {}
+    for key in keys:
+        results[key] = run_config(ctx, key, args, calib)
+        print(f"[bench] {key}: {results[key]['wall_us']} us per step, AGG {results[key]['agg_wall_us']} us",
+              file=sys.stderr, flush=True)
+    h = results[args.headline]
+    line = {
+        "metric": "mixed-batch attn iter latency (us) + decode HBM GB/s + prefill MFMA TFLOP/s",
+        "value": h["wall_us"], "unit": "us", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(h["wall_us"] / 1e3, 4), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": h["workload"] + (f"; Algorithm 1's {h['chosen']}: the chunk once and "
+                                                f"{h['k_decode_steps']} decode steps per step" if h["k_decode_steps"] > 1
+                                                else f"; Algorithm 1's {h['chosen']}"),
+                   "key": args.headline, "layers": h["layers"], "tbt_slo_us": h["tbt_slo_us"], "split": h["chosen"]},
+        "agg_us": h["agg_wall_us"], "speedup_vs_agg": h["speedup_vs_agg"], "iteration_us": h["iteration_us"],
+        "roofline": h["roofline"], "cpu_baseline": h["cpu_baseline"],
+        "configs": results, "calibration": calib,
+    }
+    print(json.dumps(line), flush=True)
+    ctx.close()
 
 
 def trace_main(args):
@@ -248,28 +530,37 @@ def trace_main(args):
     ctx.set_profiling(0)
     tot_tok = float(sum(tokens))
     res = {}
+    has_dec = np.array([any(k == 1 for k, _, _ in b) for b in batches])
     for name, lat in modes.items():
         a = np.array(lat)
         r = np.array(ready[name])
+        # one decode step per iteration: a running request's next token comes from the next
+        # iteration, so its time between tokens is the iteration latency
+        tbt = a[has_dec]
         res[name] = {"p50_us": round(float(np.percentile(a, 50)), 1), "p99_us": round(float(np.percentile(a, 99)), 1),
                      "mean_us": round(float(a.mean()), 1), "tokens_per_s": round(tot_tok / (a.sum() * 1e-6), 1),
+                     "tbt_p50_us": round(float(np.percentile(tbt, 50)), 1),
+                     "tbt_p99_us": round(float(np.percentile(tbt, 99)), 1),
+                     "tbt_slo_attainment": round(float(np.mean(tbt <= 50000.0)), 4),
                      "decode_ready_p50_us": round(float(np.percentile(r, 50)), 1),
                      "decode_ready_p99_us": round(float(np.percentile(r, 99)), 1),
-                     "decode_ready_max_us": round(float(r.max()), 1),
-                     "tbt_slo_attainment": round(float(np.mean(r <= 50000.0)), 4)}
+                     "decode_ready_max_us": round(float(r.max()), 1)}
         if name in chosen:
             res[name]["split_fraction"] = round(float(np.mean(chosen[name])), 3)
     n_pre = sum(1 for b in batches if any(k == 0 for k, _, _ in b))
-    line = {"metric": "serving-trace decode TBT p99, " + ("full model" if full else "attention share") + " (us)",
-            "value": res["adaptive_50ms"]["decode_ready_p99_us"],
+    line = {"metric": "serving-trace TBT p99 (latency of the iterations that carry decodes), " +
+                      ("full model" if full else "attention share") + " (us)",
+            "value": res["adaptive_50ms"]["tbt_p99_us"],
             "unit": "us", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": f"serving trace: {len(batches)} iterations, Poisson 4 req/s, prompts LogN(mean 4096, "
                                    f"sigma 1.0) <= 32768, outputs LogN(mean 256, sigma 0.7), budget 8192, {L} layers, "
                                    + (f"llama3-8b transformer blocks (random-init weights, FFN {ffn})" if full else
                                       "llama3-8b attention shapes"), "iterations_with_prefill": n_pre,
                        "mean_decodes": round(float(np.mean([sum(1 for k, _, _ in b if k == 1) for b in batches])), 1),
-                       "mean_tokens": round(float(np.mean(tokens)), 1)},
-            "modes": res, "agg_decode_ready_p99_us": res["agg"]["decode_ready_p99_us"],
+                       "mean_tokens": round(float(np.mean(tokens)), 1),
+                       "replay": "open loop: the trace's batches are formed in advance on a 50 ms iteration clock; "
+                                 "decode_ready is fork to the end of the decode partition within an iteration"},
+            "modes": res, "agg_tbt_p99_us": res["agg"]["tbt_p99_us"],
             "throughput_ratio_50ms_vs_agg": round(res["adaptive_50ms"]["tokens_per_s"] / res["agg"]["tokens_per_s"], 4)}
     print(json.dumps(line), flush=True)
     ctx.close()
@@ -433,7 +724,7 @@ def serve_main(args):
     for mode in modes:
         eng = duet.Engine(budget, pool, max_pages, shuffle_seed=1006)
         clock, nxt, it, recorded = 0.0, 0, 0, 0
-        lat, ready, split_used, toks = [], [], [], 0
+        lat, ready, split_used, toks, has_dec_it = [], [], [], 0, []
         while recorded < args.trace_iters:
             while nxt < len(arrivals) and arrivals[nxt] <= clock:
                 eng.add_request(int(prompts[nxt]), int(outputs[nxt]))
@@ -460,30 +751,37 @@ def serve_main(args):
                 ready.append(kt["decode_start_us"] + kt["decode_total_us"] if kt["decode_total_us"] > 0
                              else kt["iteration_us"])
                 split_used.append(sp.mode == duet.SPLIT)
+                has_dec_it.append(bool((meta[:, 0] == 1).any()))
                 toks += n_tok
                 recorded += 1
                 if recorded % 50 == 0:
                     print(f"serve {mode}: {recorded}/{args.trace_iters} iterations", file=sys.stderr, flush=True)
             eng.complete()
             it += 1
-            clock += 0.05
+            # the clock advances by the measured iteration (engine-only warm-up: 50 ms)
+            clock += lat[-1] * 1e-6 if it > 200 and lat else 0.05
         eng.close()
         a, r = np.array(lat), np.array(ready)
-        res[mode] = {"decode_ready_p50_us": round(float(np.percentile(r, 50)), 1),
+        tb = np.array([x for x, d in zip(lat, has_dec_it) if d])
+        res[mode] = {"tbt_p50_us": round(float(np.percentile(tb, 50)), 1),
+                     "tbt_p99_us": round(float(np.percentile(tb, 99)), 1),
+                     "tbt_slo_attainment": round(float(np.mean(tb <= tbt)), 4),
+                     "decode_ready_p50_us": round(float(np.percentile(r, 50)), 1),
                      "decode_ready_p99_us": round(float(np.percentile(r, 99)), 1),
                      "decode_ready_max_us": round(float(r.max()), 1),
-                     "tbt_slo_attainment": round(float(np.mean(r <= tbt)), 4),
                      "iteration_p50_us": round(float(np.percentile(a, 50)), 1),
                      "iteration_p99_us": round(float(np.percentile(a, 99)), 1),
                      "tokens_per_s": round(toks / (a.sum() * 1e-6), 1),
                      "split_fraction": round(float(np.mean(split_used)), 3)}
     ctx.set_profiling(0)
-    line = {"metric": "serving-loop decode TBT p99, full model (us)", "value": res["adaptive_50ms"]["decode_ready_p99_us"],
+    line = {"metric": "serving-loop TBT p99 (latency of the iterations that carry decodes), full model (us)",
+            "value": res["adaptive_50ms"]["tbt_p99_us"],
             "unit": "us", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": f"serving loop: native engine, {args.trace_iters} iterations after 200 warm-up, Poisson "
                                    "4 req/s, prompts LogN(mean 4096, sigma 1.0) <= 32768, outputs LogN(mean 256, sigma "
                                    f"0.7), budget {budget}, {L} llama3-8b blocks (random-init weights, FFN {ffn}), "
-                                   f"KV pages persistent per request, TBT bound {tbt / 1000:.0f} ms"},
+                                   f"KV pages persistent per request, TBT bound {tbt / 1000:.0f} ms; closed loop: arrivals are admitted "
+                                   "on a clock advanced by each measured iteration"},
             "modes": res}
     print(json.dumps(line), flush=True)
     ctx.close()
@@ -565,7 +863,7 @@ def block_main(args):
     batch = wl.llama8b_mixed()
     ctx = duet.Context(0)
     if not args.no_calibrate:
-        calibrate_model(ctx, shape=batch.shape, batch=batch)
+        calibrate_model(ctx, shape=batch.shape)
     x, weights, caches = wl.make_block_tensors(batch, ffn, L, seed=5005, device="cuda")
     kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
     del caches
@@ -640,27 +938,19 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    # The first time a run of split calls is queued several deep, the runtime settles for a few
-    # dozen steps (measured: the first 20-step back-to-back loop at 4480-4830 us per step, every
-    # later one at 4355), so the default warm-up queues 30 steps before the timed region.
-    ap.add_argument("--warmup", type=int, default=30)
-    ap.add_argument("--layers", type=int, default=None,
-                    help="attention layers per iteration (default 32 for the Llama-3-8B mixed batch, 1 otherwise)")
-    ap.add_argument("--workload", choices=list(WORKLOADS), default="llama8b-mixed",
-                    help="the mixed batch (default), the decode-heavy batch in a ~70 GB pool, or the prefill-heavy "
-                         "Llama-3-70B batch")
-    ap.add_argument("--mode", choices=["adaptive", "agg", "split"], default="adaptive")
-    ap.add_argument("--split", default="", help="Sp,Sd for --mode split")
-    ap.add_argument("--tbt-slo-us", type=float, default=None,
-                    help="TBT bound for Algorithm 1 (default: 1%% under the aggregated estimate, so the "
-                         "spatial branch is taken whenever the model finds a split that helps)")
-    ap.add_argument("--no-sweep", action="store_true", help="skip the S_p = 24..232 step-8 split sweep")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--configs", default="cfg4,cfg3,cfg2",
+                    help="workloads of the default run: cfg4 (Llama-3-70B prefill-heavy), cfg3 (decode-heavy, ~70 GB "
+                         "pool), cfg2 (Llama-3-8B mixed, 32 layers)")
+    ap.add_argument("--headline", default="cfg4", choices=list(CONFIGS), help="the workload `value` reports")
+    ap.add_argument("--layers", type=int, default=None, help="layers per iteration of the --trace/--serve/--block modes")
+    ap.add_argument("--tbt-slo-us", type=float, default=None, help="TBT bound of the --lookahead and --block modes")
+    ap.add_argument("--split", default="", help="Sp,Sd: the one split of --block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibrate", action="store_true")
-    ap.add_argument("--no-agg", action="store_true",
-                    help="skip the aggregated reference passes (every launch then runs in the timed mode)")
-    ap.add_argument("--copy-reference", action="store_true",
-                    help="end with a plain 1 GiB device-to-device copy, the reference for HBM counters")
+    ap.add_argument("--counters", action="store_true",
+                    help="a short fixed pass of --headline's workload for rocprofv3 counters: Algorithm 1's split "
+                         "(one decode step) for a few calls, then a plain 1 GiB device-to-device copy as the reference")
     ap.add_argument("--trace", action="store_true",
                     help="run the serving-trace configuration instead (adaptive vs always-aggregated)")
     ap.add_argument("--trace-iters", type=int, default=200)
@@ -682,12 +972,7 @@ def main():
               "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
-    import dataclasses
     import torch
-    import paper_2511_04791_amd as duet
-    from paper_2511_04791_amd import workloads as wl
-    from paper_2511_04791_amd.calibration import calibrate_model
-
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
@@ -696,226 +981,50 @@ def main():
     # fork, the previous call's join), which costs a back-to-back split iteration about 10%.
     torch.cuda.set_stream(torch.cuda.Stream())
     if args.trace:
-        trace_main(args)
-        return
+        return trace_main(args)
     if args.lookahead:
-        lookahead_main(args)
-        return
+        return lookahead_main(args)
     if args.serve:
-        serve_main(args)
-        return
+        return serve_main(args)
     if args.block:
-        block_main(args)
-        return
-    L = args.layers if args.layers is not None else (32 if args.workload == "llama8b-mixed" else 1)
-    if args.workload == "decode-heavy" and L != 1:
-        print("the decode-heavy batch holds a ~70 GB page pool: one layer only", file=sys.stderr)
-        sys.exit(2)
-    batch = make_workload(args.workload)
-    ctx = duet.Context(0)
-    calib = {}
-    if not args.no_calibrate:
-        t0 = time.perf_counter()
-        # the headline batch profiles itself; the 70 GB decode-heavy and the 8192-token 70B batches
-        # would take minutes, so they use the default representative batch at their head shape
-        calib = calibrate_model(ctx, shape=batch.shape, batch=batch if args.workload == "llama8b-mixed" else None)
-        calib["seconds"] = round(time.perf_counter() - t0, 2)
+        return block_main(args)
+    if args.counters:
+        return counters_main(args)
+    return suite_main(args)
 
+
+def counters_main(args):
+    """A short fixed pass for hardware counters: the headline workload's kernels under Algorithm 1's
+    split (one decode step per call, 4 calls), then a plain 1 GiB elementwise device copy whose
+    FETCH_SIZE / WRITE_SIZE readings scale the counters to bytes."""
+    import dataclasses
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    spec = CONFIGS[args.headline]
+    L = spec["layers"]
+    batch = make_workload(spec["workload"])
+    shape = dataclasses.replace(batch.shape, num_layers=L)
+    rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
+    ctx = duet.Context(0)
+    chosen = duet.choose_cu_split(rows3, SLO_US * L / spec["model_layers"], shape, ctx.model,
+                                  max_decode_steps=spec["k_cap"])[0]
+    split = duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT else duet.CuSplit.agg()
     layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
     qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
-    del layers
     pt = torch.as_tensor(batch.page_table, device="cuda")
-    meta = batch.seq_meta
-    rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
     outs = [torch.empty_like(q) for q in qs]
-    shape = dataclasses.replace(batch.shape, num_layers=L)
-    ws = ctx.workspace(duet.workspace_bytes(shape, meta))
+    for _ in range(4):
+        ctx.attn_iteration(qs, kcs, vcs, pt, batch.seq_meta, split, outs=outs)
     torch.cuda.synchronize()
-
-    agg_pred = duet.predict_iter_latency(rows3, duet.CuSplit.agg(), shape, ctx.model)
-    tau = args.tbt_slo_us if args.tbt_slo_us is not None else 0.99 * agg_pred
-    choose_us = []
-
-    def choose():
-        # Algorithm 1 proposes a split once the aggregated estimate passes tau; the benchmark keeps
-        # aggregated execution when the model predicts the proposed split to be slower.
-        t0 = time.perf_counter()
-        sp, pred, rho, flags = duet.choose_cu_split(rows3, tau, shape, ctx.model, max_decode_steps=1)
-        if sp.mode == duet.SPLIT and pred >= agg_pred:
-            sp = duet.CuSplit.agg()
-        choose_us.append((time.perf_counter() - t0) * 1e6)
-        return sp
-
-    if args.mode == "agg":
-        fixed = duet.CuSplit.agg()
-    elif args.mode == "split":
-        sp_, sd_ = (int(x) for x in args.split.split(","))
-        fixed = duet.CuSplit.split(sp_, sd_)
-    else:
-        fixed = None
-
-    def step(split=None):
-        sp = split if split is not None else (fixed if fixed is not None else choose())
-        ctx.attn_iteration(qs, kcs, vcs, pt, meta, sp, outs=outs, workspace=ws)
-        return sp
-
-    def profiled(n, warm, level, split):
-        """n steps at profiling level 1 or 2, each read back: mean of the event times."""
-        ctx.set_profiling(level)
-        rec = []
-        for i in range(warm + n):
-            step(split)
-            kt = ctx.last_kernel_times()
-            if i >= warm:
-                rec.append(kt)
-        ctx.set_profiling(0)
-        return {k: statistics.fmean(r[k] for r in rec) for k in rec[0]}
-
-    # timed region: K back-to-back steps, host choice included, synchronised on both sides
-    for _ in range(args.warmup):
-        used = step()
+    del qs, kcs, vcs, outs, layers
+    torch.cuda.empty_cache()
+    # an elementwise kernel (not a DMA copy) that reads 1 GiB and writes 1 GiB
+    src = torch.zeros(1 << 28, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.bitwise_not(src, out=dst)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        used = step()
-    torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) / args.steps
-    choose_mean = statistics.fmean(choose_us) if choose_us else 0.0
-
-    n_prof = max(5, args.steps // 2)
-    it = profiled(n_prof, 2, 1, used)
-    kern = profiled(n_prof, 2, 2, used)
-    if args.no_agg:
-        agg_it = agg_kern = agg_wall = conc_it = None
-    else:
-        # control: both halves at once on two unpartitioned streams
-        conc_it = profiled(n_prof, 2, 1, duet.CuSplit.concurrent())
-        agg_it = profiled(n_prof, 2, 1, duet.CuSplit.agg())
-        agg_kern = profiled(n_prof, 2, 2, duet.CuSplit.agg())
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step(duet.CuSplit.agg())
-        torch.cuda.synchronize()
-        agg_wall = (time.perf_counter() - t0) / args.steps
-
-    sp_cus = used.cus_prefill if used.mode == duet.SPLIT else 256
-    sd_cus = used.cus_decode if used.mode == duet.SPLIT else 256
-    dbytes = decode_bytes(batch)          # per layer = per decode-partial launch
-    pflops = prefill_causal_flops(batch)  # per layer = per prefill launch
-    k2, k1 = kern["decode_partial_us"], kern["prefill_us"]
-    k2_gbps = dbytes / (k2 * 1e-6) / 1e9
-    dec_gbps = dbytes * L / (kern["decode_total_us"] * 1e-6) / 1e9
-    pre_tflops = pflops / (k1 * 1e-6) / 1e12
-    agg_k2_gbps = dbytes / (agg_kern["decode_partial_us"] * 1e-6) / 1e9 if agg_kern else None
-    agg_pre_tflops = pflops / (agg_kern["prefill_us"] * 1e-6) / 1e12 if agg_kern else None
-    rnd = lambda x, n: None if x is None else round(x, n)
-    # hardware ceiling of each share: the probes' streaming read and MFMA loop (nominal
-    # 8 TB/s and 2.5 PFLOP/s pro rata without calibration)
-    if calib:
-        b_share = calib["probe_read_tbps"][sd_cus // 8 - 1] * 1e3
-        p_share = calib["probe_mfma_tflops"][sp_cus // 8 - 1]
-    else:
-        b_share = PEAK_HBM_GBPS * sd_cus / 256
-        p_share = PEAK_BF16_TFLOPS * sp_cus / 256
-
-    sweep = None
-    if not args.no_sweep:
-        sweep = []
-        for s in range(24, 233, 8):
-            sp = duet.CuSplit.split(s, 256 - s)
-            r_ = profiled(3, 1, 1, sp)
-            sweep.append({"Sp": s, "Sd": 256 - s, "iteration_us": round(r_["iteration_us"], 1),
-                          "predicted_us": round(duet.predict_iter_latency(rows3, sp, shape, ctx.model), 1)})
-    cpu = None
-    if not args.no_cpu_baseline:
-        # layer after layer (each with its own Q and KV pool) until about 10 s of oracle work
-        per_layer, measured = [], 0.0
-        for l in range(L):
-            cpu = cpu_baseline(batch, qs[l], kcs[l], vcs[l])
-            per_layer.append(cpu["value"])
-            measured += cpu["measured_s"]
-            if measured >= 10.0:
-                break
-        cpu["value"] = round(sum(per_layer) / len(per_layer) * L, 1)
-        cpu["measured_s"] = round(measured, 3)
-        cpu["sample"] += (f"; {len(per_layer)} of {L} layers timed, their mean per-layer time x {L} layers")
-    if args.copy_reference:
-        # an elementwise kernel (not a DMA copy) that reads 1 GiB and writes 1 GiB
-        src = torch.zeros(1 << 28, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.bitwise_not(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
-
-    decode_dominant = k2 >= k1
-    if decode_dominant:
-        traffic = committed_traffic("decode_partial", "attn_decode.hip", 1)
-        roofline = {"bound": "hbm", "achieved": round(k2_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                    "frac": round(k2_gbps / PEAK_HBM_GBPS, 4), "traffic": traffic, "kernel": "decode_partial_bf16",
-                    "algorithmic_bytes_per_launch": int(dbytes), "launch_us": round(k2, 2), "cus": sd_cus,
-                    "share_peak": round(PEAK_HBM_GBPS * sd_cus / 256, 1),
-                    "share_frac": round(k2_gbps / (PEAK_HBM_GBPS * sd_cus / 256), 4)}
-    else:
-        traffic = committed_traffic("prefill", "attn_prefill.hip", 1)
-        roofline = {"bound": "mfma", "achieved": round(pre_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(pre_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": "prefill_bf16",
-                    "algorithmic_flops_per_launch": pflops, "launch_us": round(k1, 2), "cus": sp_cus,
-                    "share_peak": round(PEAK_BF16_TFLOPS * sp_cus / 256, 1),
-                    "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4)}
-
-    line = {
-        "metric": "mixed-batch attn iter latency (us) + decode HBM GB/s + prefill MFMA TFLOP/s",
-        "value": round(wall * 1e6, 1),
-        "unit": "us",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(wall * 1e3, 4),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": WORKLOADS[args.workload].format(L=L),
-                   "layers": L, "mode": args.mode, "split": str(used), "tbt_slo_us": round(tau, 1)},
-        "iteration_us": round(it["iteration_us"], 1),
-        "agg_us": rnd(agg_wall and agg_wall * 1e6, 1),
-        "agg_iteration_us": rnd(agg_it and agg_it["iteration_us"], 1),
-        "concurrent_unpartitioned_iteration_us": rnd(conc_it and conc_it["iteration_us"], 1),
-        "speedup_vs_agg": rnd(agg_wall and agg_wall / wall, 4),
-        "agg_pred_us": round(agg_pred, 1),
-        "chosen_pred_us": round(duet.predict_iter_latency(rows3, used, shape, ctx.model), 1),
-        "host_choose_us": round(choose_mean, 2),
-        "decode_half_hbm_gbps": round(dec_gbps, 1),
-        "decode_partial_gbps": round(k2_gbps, 1),
-        "prefill_mfma_tflops": round(pre_tflops, 1),
-        "kernels_us": {k.replace("_us", ""): round(v, 2) for k, v in kern.items()},
-        "agg_kernels_us": agg_kern and {k.replace("_us", ""): round(v, 2) for k, v in agg_kern.items()},
-        "roofline": roofline,
-        "decode_roofline": {"bound": "hbm", "kernel": "decode_partial_bf16", "peak": PEAK_HBM_GBPS,
-                            "split": {"cus": sd_cus, "achieved": round(k2_gbps, 1),
-                                      "frac": round(k2_gbps / PEAK_HBM_GBPS, 4),
-                                      "share_peak": round(PEAK_HBM_GBPS * sd_cus / 256, 1),
-                                      "share_frac": round(k2_gbps / (PEAK_HBM_GBPS * sd_cus / 256), 4),
-                                      "probe_share_peak": round(b_share, 1),
-                                      "probe_share_frac": round(k2_gbps / b_share, 4)},
-                            "standalone_256": {"achieved": rnd(agg_k2_gbps, 1),
-                                               "frac": rnd(agg_k2_gbps and agg_k2_gbps / PEAK_HBM_GBPS, 4)}},
-        "prefill_roofline": {"bound": "mfma", "kernel": "prefill_bf16", "peak": PEAK_BF16_TFLOPS,
-                             "split": {"cus": sp_cus, "achieved": round(pre_tflops, 1),
-                                       "share_peak": round(PEAK_BF16_TFLOPS * sp_cus / 256, 1),
-                                       "share_frac": round(pre_tflops / (PEAK_BF16_TFLOPS * sp_cus / 256), 4),
-                                       "probe_share_peak": round(p_share, 1)},
-                             "standalone_256": {"achieved": rnd(agg_pre_tflops, 1),
-                                                "frac": rnd(agg_pre_tflops and agg_pre_tflops / PEAK_BF16_TFLOPS, 4)}},
-        "calibration": calib,
-        "cpu_baseline": cpu,
-    }
-    if sweep is not None:
-        line["sweep_best"] = min(sweep, key=lambda x: x["iteration_us"])
-        line["sweep"] = sweep
-    print(json.dumps(line), flush=True)
+    print(json.dumps({"counters_pass": args.headline, "split": str(split), "layers": L}), flush=True)
     ctx.close()
 
 

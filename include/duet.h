@@ -82,6 +82,12 @@ extern "C" {
 
 #define DUET_TOTAL_CUS 256
 #define DUET_CU_STEP 8 /* CU shares are multiples of 8: one CU per XCD */
+/* The S_d grid of duet_choose_cu_split: multiples of 32 CUs.  CU-mask bit b selects a CU on XCD
+ * b mod 8 and shader engine (b / 8) mod 4; the dispatcher deals a kernel's workgroups evenly to
+ * the shader engines of each XCD, so only multiples of 32 give every shader engine the same
+ * number of CUs.  Other multiples of 8 are accepted by every call but run 25-35% slower than the
+ * multiple of 32 below them (measured on the decode kernel). */
+#define DUET_SPLIT_STEP 32
 
 /* ---- plain structs (same bytes on host and device) ------------------------------------------ */
 typedef struct {

@@ -24,7 +24,11 @@ Full-model estimate (Section 4.1, "Token-Level Operators", "Overall Estimation")
   true GQA QKV width (h_q + 2 h_kv) d_h and a fused gate-up of width 2 m.
 
 Readings where the paper is silent (each also listed in the design notes):
-  * CU shares are multiples of 8 (one CU per XCD), S_d runs 8, 16, ..., S - 8.
+  * The paper steps S_d by one TPC.  On MI355X the step is 32 CUs, S_d = 32, 64, ..., S - 32: a
+    CU-mask bit b selects a CU on XCD b mod 8 and shader engine (b / 8) mod 4, the dispatcher
+    deals a kernel's workgroups evenly to the shader engines of each XCD, and only multiples of
+    32 give every shader engine of every XCD the same number of CUs (measured: a decode share of
+    168 CUs runs 32% slower than one of 160).  The tables stay indexed by multiples of 8.
   * k = 0 is dropped: decode must make progress; k may be capped by the look-ahead depth.
   * No feasible S_d: fall back to aggregated execution and flag SLO_INFEASIBLE.
   * T_decode = number of decode requests; T_prefill = sum of the prefill requests' q.
@@ -36,7 +40,8 @@ import math
 from dataclasses import dataclass
 
 TOTAL_CUS = 256
-CU_STEP = 8
+CU_STEP = 8       # table index step: any multiple of 8 is a valid share
+SPLIT_STEP = 32   # the S_d grid Algorithm 1 searches
 NOMINAL_BF16_FLOPS = 2.5e15      # dense bf16 MFMA peak, FLOP/s
 NOMINAL_HBM_BYTES = 8.0e12       # HBM3E bandwidth, B/s
 
@@ -103,7 +108,7 @@ def predict(batch, mode, s_p, s_d, k, tables, *, h_q, h_kv, d_h, b, layers, tota
     return max(k * t_d, t_p)
 
 
-def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP, kmax=None):
+def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=SPLIT_STEP, kmax=None):
     """Algorithm 1.  Returns dict(mode, s_p, s_d, k, rho, t, flags).  kmax caps k at the number of
     decode steps the engine can launch ahead (Section 4.3): the two candidates are clamped to it;
     None leaves them as the paper states."""
@@ -216,7 +221,7 @@ def predict_model(batch, mode, s_p, s_d, k, tables, block, *, h_q, h_kv, d_h, b,
     return max(k * t_d, t_p)
 
 
-def choose_model(batch, tau, tables, block, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=CU_STEP,
+def choose_model(batch, tau, tables, block, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, step=SPLIT_STEP,
                  kmax=None):
     """Algorithm 1 on the full-model estimate (same steps as choose)."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)

@@ -16,7 +16,7 @@ BF16, F32 = 0, 1
 KIND_PREFILL, KIND_DECODE = 0, 1
 AGG, SPLIT, CONCURRENT = 0, 1, 2
 STATUS_SLO_INFEASIBLE, STATUS_UNCALIBRATED = 1, 2
-TOTAL_CUS, CU_STEP = 256, 8
+TOTAL_CUS, CU_STEP, SPLIT_STEP = 256, 8, 32
 
 
 class Shape(ctypes.Structure):

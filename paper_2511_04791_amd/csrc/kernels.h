@@ -117,6 +117,7 @@ hipError_t launch_gather(const void* cache, int which, int elem_bytes, int h_kv,
                          hipStream_t s);
 
 hipError_t launch_read_probe(const void* buf, size_t bytes, int blocks, unsigned* sink, hipStream_t s);
+size_t read_probe_bytes(size_t bytes, int blocks);
 hipError_t launch_mfma_probe(int blocks, int iters, float* sink, hipStream_t s);
 hipError_t launch_placement_probe(int blocks, uint32_t* out, hipStream_t s);
 

@@ -464,7 +464,7 @@ int choose_impl(const duet_model* m, const duet_shape* shape, const duet_block_s
   double best_rho = 0.0, best_t = 0.0;
   duet_cu_split best{-1, 0, 0, 0};
   const bool shared = has_both_kinds(batch);
-  for (int sd = DUET_CU_STEP; sd < DUET_TOTAL_CUS; sd += DUET_CU_STEP) {
+  for (int sd = DUET_SPLIT_STEP; sd < DUET_TOTAL_CUS; sd += DUET_SPLIT_STEP) {
     const double td = f_roofline(mm, shape, batch, DUET_KIND_DECODE, sd, shared, blk);
     if (td > tau) continue;
     const int sp = DUET_TOTAL_CUS - sd;

@@ -41,17 +41,19 @@ __global__ __launch_bounds__(256) void gather_kernel(const T* cache, int which, 
   }
 }
 
+// Each wave streams its own contiguous chunk of the buffer (n16 / waves 16-byte words, rounded
+// down to whole 1 KiB wave steps), four wave steps in flight per lane; a sequential run per wave
+// is the access pattern DRAM serves best, so the probe measures the share's ceiling.
 __global__ __launch_bounds__(256) void read_probe_kernel(const uint4* buf, size_t n16, unsigned* sink) {
+  const size_t waves = (size_t)gridDim.x * 4;
+  const size_t wave = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const size_t per_wave = (n16 / waves) & ~(size_t)255;  // whole groups of four 64-word steps
+  const uint4* p = buf + wave * per_wave + lane;
   uint32_t acc = 0;
-  const size_t stride = (size_t)gridDim.x * 256;
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const uint4 a = buf[i], b = buf[i + stride], c = buf[i + 2 * stride], d = buf[i + 3 * stride];
+  for (size_t i = 0; i < per_wave; i += 256) {
+    const uint4 a = p[i], b = p[i + 64], c = p[i + 128], d = p[i + 192];
     acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
-  }
-  for (; i < n16; i += stride) {
-    const uint4 a = buf[i];
-    acc ^= a.x ^ a.y ^ a.z ^ a.w;
   }
   if (acc == 0x9e3779b9u) sink[0] = acc;  // keeps the loads alive; practically never stores
 }
@@ -109,6 +111,12 @@ hipError_t launch_gather(const void* cache, int which, int elem_bytes, int h_kv,
     hipLaunchKernelGGL(gather_kernel<uint32_t>, dim3(blocks), dim3(256), 0, s, (const uint32_t*)cache, which, h_kv, d,
                        page_table, max_pages, num_phys, req, kv_len, (uint32_t*)out, err);
   return hipGetLastError();
+}
+
+// Bytes the read probe reads with `blocks` workgroups over a buffer of `bytes`.
+size_t read_probe_bytes(size_t bytes, int blocks) {
+  const size_t waves = (size_t)blocks * 4;
+  return ((bytes / 16 / waves) & ~(size_t)255) * waves * 16;
 }
 
 hipError_t launch_read_probe(const void* buf, size_t bytes, int blocks, unsigned* sink, hipStream_t s) {

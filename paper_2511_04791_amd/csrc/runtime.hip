@@ -1461,21 +1461,27 @@ int duet_probe_read_bw(duet_ctx* ctx, int32_t cus, const void* buf, size_t bytes
                        double* bytes_per_s) {
   clear_error();
   if (!ctx || !buf || !bytes_per_s) return fail(DUET_EINVAL, "NULL argument");
-  if (bytes < (1u << 20) || iters < 1) return fail(DUET_EINVAL, "need >= 1 MiB and iters >= 1");
+  if (bytes < (1u << 24) || iters < 1) return fail(DUET_EINVAL, "need >= 16 MiB and iters >= 1");
   std::lock_guard<std::mutex> lock(ctx->mu);
   hipStream_t st;
   int rc = get_stream(ctx, cus, 0, &st);
   if (rc) return rc;
-  const int blocks = cus * 8;
-  HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));  // warm-up
-  HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
-  for (int i = 0; i < iters; ++i) HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
-  HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
-  float ms = 0.f;
-  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
+  // The share's ceiling: the best of three grid sizes (8, 16 and 32 waves per CU), each warmed
+  // up once and then timed over `iters` launches.
+  double best = 0.0;
+  for (int blocks_per_cu : {2, 4, 8}) {
+    const int blocks = cus * blocks_per_cu;
+    HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));
+    HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
+    for (int i = 0; i < iters; ++i) HIP_TRY(launch_read_probe(buf, bytes, blocks, ctx->dev_sink, st));
+    HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
+    HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
+    best = std::max(best, (double)read_probe_bytes(bytes, blocks) * iters / (ms * 1e-3));
+  }
   ctx->prof_valid = false;
-  *bytes_per_s = (double)(bytes / 16 * 16) * iters / (ms * 1e-3);
+  *bytes_per_s = best;
   return DUET_OK;
 }
 
@@ -1489,16 +1495,22 @@ int duet_probe_mfma(duet_ctx* ctx, int32_t cus, int32_t iters, double* flops_per
   if (rc) return rc;
   const int blocks = cus * 2;  // 8 waves per CU, two per SIMD
   float* sink = reinterpret_cast<float*>(ctx->dev_sink);
-  HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
-  HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
-  HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
-  HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
-  float ms = 0.f;
-  HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
-  ctx->prof_valid = false;
+  // Clocks settle under sustained matrix load: warm up with four launches, then keep the best of
+  // three timed launches.
+  for (int i = 0; i < 4; ++i) HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
+  double best = 0.0;
   const double flops = (double)blocks * 4 /*waves*/ * iters * 4 /*chains*/ * (32.0 * 32 * 16 * 2);
-  *flops_per_s = flops / (ms * 1e-3);
+  for (int rep = 0; rep < 3; ++rep) {
+    HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
+    HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
+    HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
+    HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, ctx->prof[kEvA], ctx->prof[kEvB]));
+    best = std::max(best, flops / (ms * 1e-3));
+  }
+  ctx->prof_valid = false;
+  *flops_per_s = best;
   return DUET_OK;
 }
 
@@ -1524,7 +1536,7 @@ int duet_calibrate(duet_ctx* ctx, duet_model* m, const void* scratch, size_t scr
     cus[i] = DUET_CU_STEP * (i + 1);
     int rc = duet_probe_read_bw(ctx, cus[i], scratch, scratch_bytes, 3, &by[i]);
     if (rc) return rc;
-    if ((rc = duet_probe_mfma(ctx, cus[i], 2048, &fl[i]))) return rc;
+    if ((rc = duet_probe_mfma(ctx, cus[i], 8192, &fl[i]))) return rc;
   }
   return duet_model_set_tables(m, kNumCuSteps, cus.data(), fl.data(), by.data());
 }

@@ -109,7 +109,7 @@ def test_choose_model_matches_brute_force(seed):
             continue
         pre, dec = R.split_requests(batch)
         best = None
-        for s_d in range(8, 256, 8):
+        for s_d in range(R.SPLIT_STEP, 256, R.SPLIT_STEP):
             t_d = R.f_model(dec, s_d, t, blk, **kw)
             if t_d > tau:
                 continue

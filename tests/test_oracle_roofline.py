@@ -117,7 +117,7 @@ def _exhaustive(batch, tau, tables, kw, kmax=2000):
     pre, dec = orf.split_requests(batch)
     td_tok, tp_tok = len(dec), sum(q for q, _ in pre)
     best = (0.0, None)
-    for s_d in range(8, 256, 8):
+    for s_d in range(orf.SPLIT_STEP, 256, orf.SPLIT_STEP):
         t_d = orf.f_roofline(dec, s_d, tables, **kw)
         if t_d > tau:
             continue
@@ -173,7 +173,7 @@ def test_prefill_dominated_batch_takes_smallest_feasible_decode_share():
     tau = orf.f_roofline([(1, 1024)] * 4, 64, tab, **kw) * 1.0001
     r = orf.choose(batch, tau, tab, **kw)
     assert r["mode"] == orf.SPLIT
-    feasible = [s for s in range(8, 256, 8) if orf.f_roofline([(1, 1024)] * 4, s, tab, **kw) <= tau]
+    feasible = [s for s in range(orf.SPLIT_STEP, 256, orf.SPLIT_STEP) if orf.f_roofline([(1, 1024)] * 4, s, tab, **kw) <= tau]
     assert r["s_d"] == min(feasible) == 64
 
 
