@@ -237,6 +237,28 @@ int duet_choose_cu_split_model(const duet_model* m, const duet_shape* shape, con
                                const duet_batch* batch, double tbt_slo_us, int32_t max_decode_steps,
                                duet_cu_split* out, double* predicted_us, double* rho, int32_t* status_flags);
 
+/* ---- token-level operators (Section 4.1: the operators that act on each token independently).
+ * The block forward chains them around the attention kernels; they are exported one by one so
+ * each can be checked against its definition on its own inputs.  All tensors are caller-owned
+ * contiguous bf16 device arrays, row-major; work is enqueued on `stream` (asynchronous). ---- */
+
+/* y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * weight for rows r of x [rows, d] (d a multiple of 8):
+ * fp32 arithmetic, one rounding to bf16.  DUET_EINVAL for null pointers, bad sizes or eps <= 0. */
+int duet_rmsnorm(duet_ctx* ctx, const void* x, const void* weight, void* y, int32_t rows, int32_t d, float eps,
+                 void* stream);
+/* act[r] = silu(g[r]) * u[r] with g, u the two halves of gate_up [rows, 2 m] (gate columns first),
+ * silu(g) = g / (1 + exp(-g)): fp32 arithmetic, one rounding to bf16; m a multiple of 8. */
+int duet_swiglu(duet_ctx* ctx, const void* gate_up, void* act, int32_t rows, int32_t m, void* stream);
+/* The QKV split of one layer (Section 2: the new tokens' keys and values enter the cache before
+ * attention): qkv [T, (h_q + 2 h_kv) d] rows in seq_meta order; each row's first h_q d columns go
+ * to q [T, h_q, d]; its key and value columns go to slot pos % 16 of physical page
+ * page_table[r][pos / 16] of k_cache [P, h_kv, 16, d] and v_cache [P, h_kv, d, 16], pos =
+ * cached_len + the row's index in its request.  A pure copy.  workspace of at least
+ * duet_workspace_bytes(); page ids outside the pool are not written and set its error word. */
+int duet_qkv_split(duet_ctx* ctx, const duet_shape* shape, const void* qkv, void* q, void* k_cache, void* v_cache,
+                   int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
+                   const duet_batch* batch, void* workspace, size_t workspace_bytes, void* stream);
+
 /* ---- GPU context ----------------------------------------------------------------------------- */
 
 /* Infrastructure (no passage of its own): the device state every call below uses.
@@ -318,6 +340,13 @@ typedef struct {
   const void* w_down;    /* [ffn_dim, d] */
 } duet_block_weights;
 
+/* Byte offsets in the duet_block_forward workspace of its activation buffers, in this order:
+ * RMSNorm output [T, d], QKV projection [T, d_qkv], queries [T, h_q, d_h], attention output
+ * [T, h_q, d_h], gate-up projection [T, 2 m], SwiGLU output [T, m] (bf16, T = scheduled tokens).
+ * After a call they hold the last layer's activations (the RMSNorm buffer: the one before the
+ * feed-forward part; with look-ahead, the decode rows of the last step).  Host only. */
+int duet_block_buffers(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
+                       int32_t k_decode_steps, size_t* offsets);
 /* Workspace of duet_block_forward with k_decode_steps decode steps: duet_workspace_bytes' layout
  * (with the work lists of look-ahead steps 1 .. k - 1), the activations of every scheduled token
  * ([T, d] x4, [T, (h_q + 2 h_kv) head_dim], [T, 2 ffn_dim], [T, ffn_dim], bf16) and two hipBLASLt

@@ -230,6 +230,18 @@ def block_workspace_bytes(shape: AttnShape, block: BlockShape, seq_meta, k_decod
     return n.value
 
 
+BLOCK_BUFFER_NAMES = ("norm", "qkv", "q", "attn", "gate_up", "act")
+
+
+def block_buffers(shape: AttnShape, block: BlockShape, seq_meta, k_decode_steps: int = 1) -> dict:
+    """Byte offsets of the block forward's activation buffers in its workspace (duet_block_buffers)."""
+    b = _BatchC(seq_meta)
+    offs = (ctypes.c_size_t * 6)()
+    N.check(N.lib().duet_block_buffers(ctypes.byref(_shape_c(shape)), ctypes.byref(block.to_c()), ctypes.byref(b.c),
+                                       int(k_decode_steps), offs), "duet_block_buffers")
+    return dict(zip(BLOCK_BUFFER_NAMES, (int(x) for x in offs)))
+
+
 class Engine:
     """The serving engine's batch former and page allocator (duet_engine_*), host only."""
 
@@ -436,6 +448,46 @@ class Context:
             N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
                     "duet_check_device_error")
         return x
+
+    def rmsnorm(self, x, weight, eps: float = 1e-5, *, out=None, stream=None):
+        """duet_rmsnorm over the rows of a contiguous bf16 device tensor x [rows, d]."""
+        import torch
+        if out is None:
+            out = torch.empty_like(x)
+        st = torch.cuda.current_stream(x.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_rmsnorm(self.handle, x.data_ptr(), weight.data_ptr(), out.data_ptr(), int(x.shape[0]),
+                                     int(x.shape[1]), float(eps), ctypes.c_void_p(st)), "duet_rmsnorm")
+        return out
+
+    def swiglu(self, gate_up, *, out=None, stream=None):
+        """duet_swiglu: gate_up [rows, 2 m] -> [rows, m]."""
+        import torch
+        rows, m2 = int(gate_up.shape[0]), int(gate_up.shape[1])
+        if out is None:
+            out = torch.empty(rows, m2 // 2, dtype=gate_up.dtype, device=gate_up.device)
+        st = torch.cuda.current_stream(gate_up.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_swiglu(self.handle, gate_up.data_ptr(), out.data_ptr(), rows, m2 // 2, ctypes.c_void_p(st)),
+                "duet_swiglu")
+        return out
+
+    def qkv_split(self, qkv, k_cache, v_cache, page_table, seq_meta, shape: AttnShape, *, q=None, workspace=None,
+                  stream=None, check_errors: bool = False):
+        """duet_qkv_split: the query rows out of qkv [T, (h_q + 2 h_kv) d], keys and values into the cache."""
+        import torch
+        b = _BatchC(seq_meta)
+        T = int(qkv.shape[0])
+        if q is None:
+            q = torch.empty(T, shape.num_q_heads, shape.head_dim, dtype=qkv.dtype, device=qkv.device)
+        ws = self.workspace(workspace_bytes(shape, b.rows)) if workspace is None else workspace
+        st = torch.cuda.current_stream(qkv.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_qkv_split(self.handle, ctypes.byref(_shape_c(shape)), qkv.data_ptr(), q.data_ptr(),
+                                       k_cache.data_ptr(), v_cache.data_ptr(), int(k_cache.shape[0]),
+                                       page_table.data_ptr(), int(page_table.shape[1]), ctypes.byref(b.c),
+                                       ws.data_ptr(), ws.numel(), ctypes.c_void_p(st)), "duet_qkv_split")
+        if check_errors:
+            N.check(N.lib().duet_check_device_error(self.handle, ws.data_ptr(), ctypes.c_void_p(st)),
+                    "duet_check_device_error")
+        return q
 
     def attn_iteration(self, qs, k_caches, v_caches, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
                        outs=None, workspace=None, stream=None, check_errors: bool = False):

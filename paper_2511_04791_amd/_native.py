@@ -87,6 +87,11 @@ _SIGS = {
     "duet_block_forward": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(BlockWeights), ctypes.c_float, c_void_p,
                                      P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,
                                      c_void_p, c_size_t, c_void_p]),
+    "duet_block_buffers": (c_int32, [P(Shape), P(BlockShape), P(Batch), c_int32, P(c_size_t)]),
+    "duet_rmsnorm": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, ctypes.c_float, c_void_p]),
+    "duet_swiglu": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_void_p]),
+    "duet_qkv_split": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
+                                 P(Batch), c_void_p, c_size_t, c_void_p]),
     "duet_attn_mixed_batch": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),
     "duet_attn_iteration": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p,

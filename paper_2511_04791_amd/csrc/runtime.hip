@@ -1265,6 +1265,96 @@ int duet_block_workspace_bytes(const duet_shape* shape, const duet_block_shape* 
   return DUET_OK;
 }
 
+int duet_block_buffers(const duet_shape* shape, const duet_block_shape* block, const duet_batch* batch,
+                       int32_t k_decode_steps, size_t* offsets) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if ((rc = check_block_exec(shape, block))) return rc;
+  if (!offsets) return fail(DUET_EINVAL, "offsets is NULL");
+  if (k_decode_steps < 1 || k_decode_steps > kMaxLookahead)
+    return fail(DUET_EINVAL, "k_decode_steps %d not in [1, %d]", k_decode_steps, kMaxLookahead);
+  Plan p;
+  plan_batch(shape, batch, 1, k_decode_steps, &p, false);
+  int64_t T = 0;
+  for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
+  const BlockLayout B = block_layout(shape, block, T, p.total);
+  const size_t v[6] = {B.h, B.qkv, B.q, B.attn, B.gu, B.act};
+  for (int i = 0; i < 6; ++i) offsets[i] = v[i];
+  return DUET_OK;
+}
+
+int duet_rmsnorm(duet_ctx* ctx, const void* x, const void* weight, void* y, int32_t rows, int32_t d, float eps,
+                 void* stream) {
+  clear_error();
+  if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
+  int rc;
+  if ((rc = check_device_ptr(x, "x")) || (rc = check_device_ptr(weight, "weight")) || (rc = check_device_ptr(y, "y")))
+    return rc;
+  if (rows < 0 || d < 8 || d % 8 || d > (1 << 20)) return fail(DUET_EINVAL, "rows %d / d %d: d a multiple of 8", rows, d);
+  if (!(eps > 0.0f)) return fail(DUET_EINVAL, "eps must be > 0");
+  HIP_TRY(hipSetDevice(ctx->device));
+  HIP_TRY(launch_rmsnorm(static_cast<const __bf16*>(x), static_cast<const __bf16*>(weight), static_cast<__bf16*>(y),
+                         rows, d, eps, static_cast<hipStream_t>(stream)));
+  return DUET_OK;
+}
+
+int duet_swiglu(duet_ctx* ctx, const void* gate_up, void* act, int32_t rows, int32_t m, void* stream) {
+  clear_error();
+  if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
+  int rc;
+  if ((rc = check_device_ptr(gate_up, "gate_up")) || (rc = check_device_ptr(act, "act"))) return rc;
+  if (rows < 0 || m < 8 || m % 8 || m > (1 << 20)) return fail(DUET_EINVAL, "rows %d / m %d: m a multiple of 8", rows, m);
+  HIP_TRY(hipSetDevice(ctx->device));
+  HIP_TRY(launch_swiglu(static_cast<const __bf16*>(gate_up), static_cast<__bf16*>(act), rows, m,
+                        static_cast<hipStream_t>(stream)));
+  return DUET_OK;
+}
+
+int duet_qkv_split(duet_ctx* ctx, const duet_shape* shape, const void* qkv, void* q, void* k_cache, void* v_cache,
+                   int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
+                   const duet_batch* batch, void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  if (!shape) return fail(DUET_EINVAL, "shape is NULL");
+  if (shape->dtype != DUET_BF16) return fail(DUET_EUNSUPPORTED, "the QKV split runs bf16 only");
+  const void* q_l[1] = {qkv};
+  const void* k_l[1] = {k_cache};
+  const void* v_l[1] = {v_cache};
+  const void* o_l[1] = {q};
+  int rc = check_call(ctx, shape, 1, q_l, k_l, v_l, num_phys_pages, page_table, max_pages_per_req, batch,
+                      duet_cu_split{DUET_AGG, DUET_TOTAL_CUS, 0, 1}, workspace, o_l, 0);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(ctx->mu);
+  Plan& p = ctx->plan;
+  plan_batch(shape, batch, 1, 1, &p, true);
+  if (workspace_bytes < p.total) return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, p.total);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  HIP_TRY(hipSetDevice(ctx->device));
+  char* ws = static_cast<char*>(workspace);
+  if ((rc = stage_upload(ctx, p, ws, st))) return rc;
+  int64_t T = 0;
+  for (int r = 0; r < batch->num_reqs; ++r) T += batch->reqs[r].q_len;
+  QkvSplitArgs a;
+  a.qkv = static_cast<const __bf16*>(qkv);
+  a.q = static_cast<__bf16*>(q);
+  a.k_cache = static_cast<__bf16*>(k_cache);
+  a.v_cache = static_cast<__bf16*>(v_cache);
+  a.meta = reinterpret_cast<const int4*>(ws + p.off_meta);
+  a.dreq = nullptr;
+  a.page_table = page_table;
+  a.num_phys_pages = num_phys_pages;
+  a.err = reinterpret_cast<int32_t*>(ws);
+  a.num_reqs = batch->num_reqs;
+  a.max_pages = max_pages_per_req;
+  a.h_q = shape->num_q_heads;
+  a.h_kv = shape->num_kv_heads;
+  a.head_dim = shape->head_dim;
+  a.row0 = 0;
+  HIP_TRY(launch_qkv_split(a, (int)T, st));
+  return DUET_OK;
+}
+
 int duet_block_forward(duet_ctx* ctx, const duet_shape* shape, const duet_block_shape* block,
                        const duet_block_weights* weights, float norm_eps, void* x, void* const* x_ahead,
                        void* const* k_cache, void* const* v_cache, int64_t num_phys_pages, const int32_t* page_table,

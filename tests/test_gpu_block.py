@@ -1,15 +1,21 @@
 """GPU parity of the block forward (token-level operators around the attention kernels) against
 the fp64 block oracle, on seeded synthetic inputs.
 
-Tolerance, derived from the arithmetic: the GPU rounds to bf16 (relative error at most 2^-9)
-after each of 9 operators of a layer (RMSNorm, QKV projection, cache write, attention, output
-projection with the residual, RMSNorm, gate-up projection, SwiGLU, down projection with the
-residual).  To first order, with the operators' gains near one (RMSNorm output and weights
-scaled to unit variance), the error of the residual stream after L layers is bounded by
-9 L 2^-9 times its largest magnitude; the mean error by a quarter of that times the mean
-magnitude (roundings are unbiased and partly cancel).  Layer l's new cache rows carry the
-residual error of the l layers before them plus four roundings of their own (RMSNorm, the
-projection, its bf16 result, the cache store): (9 l + 4) 2^-9 times their largest magnitude.
+Operators one by one, each on its own bf16 input read back from the device: RMSNorm and SwiGLU
+compute in fp32 and round once to bf16, so each output is within one bf16 rounding of the fp64
+definition (relative 2^-8, the bf16 unit roundoff, plus a 2^-16 margin for the fp32 arithmetic
+before the rounding); the QKV split is a copy and must be bit-exact.  Inside a block, the
+attention output rows (before the output projection) are checked against the attention oracle
+run on the block's own queries and caches at the bf16 attention tolerance.
+
+Whole blocks, residual stream: per layer the stream takes two roundings of its own (after each
+residual add) and the errors of the branch activations (RMSNorm, QKV, attention, gate-up,
+SwiGLU: one rounding each) reach it through projections of gain near one (RMSNorm output and
+weights scaled to unit variance).  Measured (six cases, up to three layers), the stream's largest error is
+0.65-0.8 L u times its largest magnitude and its mean error 0.5-0.6 L u times its mean magnitude
+(u = 2^-8).  The bounds are 3 L u for the largest error and L u for the mean.  Layer l's new cache rows carry the residual error of the l layers before them
+plus four roundings of their own (RMSNorm, the projection, its bf16 result, the cache store):
+(3 l + 4) u times their largest magnitude.
 """
 import numpy as np
 import pytest
@@ -21,7 +27,8 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 EPS = 1e-5
-U = 2.0 ** -9
+U = 2.0 ** -8          # bf16 unit roundoff
+ONE_ROUNDING = U + 2.0 ** -16
 
 
 @pytest.fixture(scope="module")
@@ -55,11 +62,12 @@ def _run_case(ctx, reqs, ffn, layers, split, seed, shape=None):
                                     page_size=sh.page_size)
     got = to64(xg)
     err = np.abs(got - ref)
-    print(f"[block] max_abs={err.max():.3e} (bound {9 * layers * U * np.abs(ref).max():.3e}) "
-          f"mean_abs={err.mean():.3e} (bound {9 * layers * U / 4 * np.abs(ref).mean():.3e})", flush=True)
+    print(f"[block] max_abs={err.max():.3e} = {err.max() / (layers * U * np.abs(ref).max()):.2f} L u max|x| "
+          f"(bound 3) mean_abs={err.mean():.3e} = {err.mean() / (layers * U * np.abs(ref).mean()):.2f} L u mean|x| "
+          f"(bound 1)", flush=True)
     assert np.isfinite(got).all()
-    assert err.max() <= 9 * layers * U * np.abs(ref).max()
-    assert err.mean() <= 9 * layers * U / 4 * np.abs(ref).mean()
+    assert err.max() <= 3 * layers * U * np.abs(ref).max()
+    assert err.mean() <= layers * U * np.abs(ref).mean()
     # The scheduled tokens' cache rows, layer by layer.
     from oracle.attention import gather_kv
     for l in range(layers):
@@ -69,7 +77,7 @@ def _run_case(ctx, reqs, ffn, layers, split, seed, shape=None):
             for cache, refc, dim_major in ((kg, kref[l], False), (vg, vref[l], True)):
                 new = gather_kv(cache, b.page_table[r], c + q, sh.page_size, dim_major)[c:]
                 want = gather_kv(refc, b.page_table[r], c + q, sh.page_size, dim_major)[c:]
-                assert np.abs(new - want).max() <= (9 * l + 4) * U * np.abs(want).max(), f"layer {l} request {r}"
+                assert np.abs(new - want).max() <= (3 * l + 4) * U * np.abs(want).max(), f"layer {l} request {r}"
     # A profiled call (x moves on by another L layers; it was checked above) reports the partitions.
     ctx.set_profiling(1)
     ctx.block_forward(xg, wg, kcs, vcs, pt, b.seq_meta, ffn, split, norm_eps=EPS)
@@ -146,10 +154,22 @@ def test_block_forward_lookahead(ctx, split):
         outs.append((to64(xag[s - 1]), ref_s))
     for s, (got, want) in enumerate(outs):
         err = np.abs(got - want)
-        print(f"[block] step {s}: max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
+        print(f"[block] step {s}: max_abs={err.max():.3e} = {err.max() / (L * U * np.abs(want).max()):.2f} L u max|x| "
+              f"mean_abs={err.mean():.3e}", flush=True)
         assert np.isfinite(got).all()
-        assert err.max() <= 9 * L * U * np.abs(want).max(), f"step {s}"
-        assert err.mean() <= 9 * L * U / 4 * np.abs(want).mean(), f"step {s}"
+        assert err.max() <= 3 * L * U * np.abs(want).max(), f"step {s}"
+        assert err.mean() <= L * U * np.abs(want).mean(), f"step {s}"
+    # every layer's cache rows of every look-ahead position (cached_len + 1 .. cached_len + k - 1)
+    from oracle.attention import gather_kv
+    for l in range(L):
+        kg, vg = to64(kcs[l]), to64(vcs[l])
+        for r in dec:
+            c = int(b.cached_lens[r]) + 1
+            for cache, refc, dim_major in ((kg, kc[l], False), (vg, vc[l], True)):
+                new = gather_kv(cache, b.page_table[r], c + k - 1, 16, dim_major)[c:]
+                want = gather_kv(refc, b.page_table[r], c + k - 1, 16, dim_major)[c:]
+                assert new.shape[0] == k - 1 and np.isfinite(new).all()
+                assert np.abs(new - want).max() <= (3 * (L + l) + 4) * U * np.abs(want).max(), f"layer {l} request {r}"
     if split != "agg":
         ctx.set_profiling(1)
         ctx.block_forward(xg, [{n: v.cuda() for n, v in w.items()} for w in weights], kcs, vcs,
@@ -197,6 +217,98 @@ def test_engine_driven_iterations_carry_the_cache(ctx):
         err = np.abs(to64(xg) - ref)
         print(f"[block] engine iteration {it}: rows={len(meta)} tokens={x.shape[0]} {sp} max_abs={err.max():.3e}",
               flush=True)
-        assert err.max() <= 9 * L * U * np.abs(ref).max() and err.mean() <= 9 * L * U / 4 * np.abs(ref).mean()
+        assert err.max() <= 3 * L * U * np.abs(ref).max() and err.mean() <= L * U * np.abs(ref).mean()
         eng.complete()
     eng.close()
+
+
+def test_rmsnorm_one_rounding(ctx):
+    from oracle.block import rmsnorm
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(4201)
+    for rows, d in ((300, 4096), (7, 512), (1, 8)):
+        x = (torch.randn(rows, d, generator=gen) * 0.7).to(torch.bfloat16)
+        w = (1.0 + 0.1 * torch.randn(d, generator=gen)).to(torch.bfloat16)
+        y = ctx.rmsnorm(x.cuda(), w.cuda(), EPS)
+        torch.cuda.synchronize()
+        ref = rmsnorm(to64(x), to64(w), EPS)
+        err = np.abs(to64(y) - ref)
+        print(f"[op] rmsnorm {rows}x{d}: max rel {np.max(err / np.maximum(np.abs(ref), 1e-30)):.3e} (bound "
+              f"{ONE_ROUNDING:.3e})", flush=True)
+        assert (err <= ONE_ROUNDING * np.abs(ref)).all()
+
+
+def test_swiglu_one_rounding(ctx):
+    from oracle.block import silu
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(4202)
+    for rows, m in ((300, 1024), (5, 8), (64, 14336)):
+        gu = (torch.randn(rows, 2 * m, generator=gen) * 2.0).to(torch.bfloat16)
+        act = ctx.swiglu(gu.cuda())
+        torch.cuda.synchronize()
+        g, u = to64(gu[:, :m]), to64(gu[:, m:])
+        ref = silu(g) * u
+        err = np.abs(to64(act) - ref)
+        print(f"[op] swiglu {rows}x{m}: max rel {np.max(err / np.maximum(np.abs(ref), 1e-30)):.3e} (bound "
+              f"{U + 2.0 ** -14:.3e})", flush=True)
+        # exp and the division in fp32 (a few ulp) before the one rounding
+        assert (err <= (U + 2.0 ** -14) * np.abs(ref) + 1e-30).all()
+
+
+def test_qkv_split_bit_exact(ctx):
+    """Query columns out, key and value columns into the page slots of their positions: a copy,
+    bit for bit; every other slot of the caches unchanged."""
+    from oracle.attention import append_token
+    from paper_2511_04791_amd import workloads as wl
+    sh = wl.AttnShape(4, 2, 128, "bf16")
+    b = wl.make_batch(sh, [(0, 37, 11), (1, 1, 40), (0, 20, 0), (1, 1, 5), (1, 1, 15)], page_seed=4203)
+    _, kc, vc = wl.make_tensors(b, 4203, device="cpu")
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(4204)
+    T, nq, nk = b.num_tokens, 4 * 128, 2 * 128
+    qkv = torch.randn(T, nq + 2 * nk, generator=gen).to(torch.bfloat16)
+    kcg, vcg = kc.cuda(), vc.cuda()
+    q = ctx.qkv_split(qkv.cuda(), kcg, vcg, torch.as_tensor(b.page_table, device="cuda"), b.seq_meta, sh,
+                      check_errors=True)
+    torch.cuda.synchronize()
+    as16 = lambda t: t.view(torch.int16).numpy()
+    assert np.array_equal(as16(q.cpu()), as16(qkv[:, :nq].reshape(T, 4, 128).contiguous()))
+    kref, vref = as16(kc).copy(), as16(vc).copy()
+    q16 = as16(qkv)
+    for r in range(b.num_reqs):
+        _, q_start, q_len, cached = (int(x) for x in b.seq_meta[r])
+        for t in range(q_len):
+            row = q16[q_start + t]
+            append_token(kref, vref, b.page_table[r], cached + t, row[nq:nq + nk].reshape(2, 128),
+                         row[nq + nk:].reshape(2, 128), 16)
+    assert np.array_equal(as16(kcg.cpu()), kref)
+    assert np.array_equal(as16(vcg.cpu()), vref)
+
+
+@pytest.mark.parametrize("split", ["agg", "128/128"])
+def test_block_attention_rows_at_attention_tolerance(ctx, split):
+    """The attention output inside a block (before the output projection) against the attention
+    oracle on the block's own queries and caches, at the bf16 attention tolerance."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from _helpers import BF16_MAX_ABS, BF16_MEAN_ABS
+    from oracle.attention import mixed_batch
+    sh = wl.AttnShape(4, 2, 128, "bf16")
+    ffn = 512
+    b = wl.make_batch(sh, [(0, 100, 37), (0, 30, 0), (1, 1, 700), (1, 1, 16), (1, 1, 300), (1, 1, 1)], page_seed=4205)
+    x, weights, caches = wl.make_block_tensors(b, ffn, 1, 4205, device="cpu")
+    kcg, vcg = caches[0][0].cuda(), caches[0][1].cuda()
+    sp = duet.CuSplit.agg() if split == "agg" else duet.CuSplit.split(128, 128)
+    block = duet.BlockShape(ffn, 0, duet.BLOCK_GQA_QKV | duet.BLOCK_FUSED_GATE_UP)
+    ws = torch.empty(duet.block_workspace_bytes(sh, block, b.seq_meta), dtype=torch.uint8, device="cuda")
+    ctx.block_forward(x.cuda(), [{n: v.cuda() for n, v in weights[0].items()}], [kcg], [vcg],
+                      torch.as_tensor(b.page_table, device="cuda"), b.seq_meta, ffn, sp, workspace=ws, check_errors=True)
+    torch.cuda.synchronize()
+    off = duet.block_buffers(sh, block, b.seq_meta)
+    T, nq = b.num_tokens, 4 * 128
+    buf = lambda name: ws[off[name]:off[name] + T * nq * 2].view(torch.bfloat16).view(T, 4, 128)
+    q, attn = buf("q"), buf("attn")
+    want = mixed_batch(to64(q), to64(kcg), to64(vcg), b.page_table, b.seq_meta, 16)
+    err = np.abs(to64(attn) - want)
+    print(f"[block] attention rows ({split}): max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
+    assert err.max() <= BF16_MAX_ABS and err.mean() <= BF16_MEAN_ABS
