@@ -305,6 +305,26 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
                           int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split,
                           void* workspace, size_t workspace_bytes, void* out, void* stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): duet_attn_mixed_batch without the workspace argument.  The call's
+ * workspace is a file-scope device array of DUET_NOALLOC_SCRATCH_BYTES held by each device the
+ * library runs on until the process ends; the call allocates nothing (no device or pinned memory,
+ * no streams, no events).  Batches whose work lists and partials need more return
+ * DUET_EWORKSPACE, as do work lists beyond the 1 MiB of pinned staging duet_init preallocates.
+ * Under DUET_SPLIT or DUET_CONCURRENT the CU-masked streams must already exist: one earlier call
+ * of duet_attn_mixed_batch or duet_attn_iteration with the same split creates them (the context
+ * keeps its six most recently used); otherwise DUET_EINVAL.  Profiling is ignored.  The output is
+ * bit-identical to duet_attn_mixed_batch's.  Every call on a device shares that device's array,
+ * which keeps the last call's contents (each call's upload clears the parts that must start at
+ * zero): calls that overlap on one device, from any context or thread, race.  Page ids outside
+ * the pool are never dereferenced; the error word they set lives in the scratch and is not
+ * reported. */
+#define DUET_NOALLOC_SCRATCH_BYTES (32u << 20)
+int duet_attn_mixed_batch_noalloc(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
+                                  const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                                  int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* out,
+                                  void* stream);
+
 /* The attention of a whole serving iteration: shape->num_layers layers (at most 1024) over the
  * same batch and page table (Section 4.3: each partition runs its phase's layers as one stream of
  * work; Section 4.1: t_total = L * t_attn).  q, k_cache, v_cache and out are host arrays of

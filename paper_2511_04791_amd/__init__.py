@@ -391,6 +391,24 @@ class Context:
                     "duet_check_device_error")
         return out
 
+    def attn_mixed_batch_noalloc(self, q, k_cache, v_cache, page_table, seq_meta, cu_split: CuSplit = CuSplit.agg(), *,
+                                 out=None, stream=None):
+        """One layer without a workspace (duet_attn_mixed_batch_noalloc): the library's fixed device
+        scratch is used and nothing is allocated (`out` is allocated here when not given)."""
+        import torch
+        shape = shape_of(q, k_cache, 1)
+        b = _BatchC(seq_meta)
+        self._check_layer(q, k_cache, v_cache, page_table, b)
+        if out is None:
+            out = torch.empty_like(q)
+        st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
+        N.check(N.lib().duet_attn_mixed_batch_noalloc(self.handle, ctypes.byref(_shape_c(shape)), q.data_ptr(),
+                                                      k_cache.data_ptr(), v_cache.data_ptr(), int(k_cache.shape[0]),
+                                                      page_table.data_ptr(), int(page_table.shape[1]),
+                                                      ctypes.byref(b.c), cu_split.to_c(), out.data_ptr(),
+                                                      ctypes.c_void_p(st)), "duet_attn_mixed_batch_noalloc")
+        return out
+
     def block_forward(self, x, weights, k_caches, v_caches, page_table, seq_meta, ffn_dim: int,
                       cu_split: CuSplit = CuSplit.agg(), *, x_ahead=None, norm_eps: float = 1e-5, workspace=None,
                       stream=None, check_errors: bool = False):

@@ -94,6 +94,8 @@ _SIGS = {
                                  P(Batch), c_void_p, c_size_t, c_void_p]),
     "duet_attn_mixed_batch": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_int32,
                                         P(Batch), CuSplit, c_void_p, c_size_t, c_void_p, c_void_p]),
+    "duet_attn_mixed_batch_noalloc": (c_int32, [c_void_p, P(Shape), c_void_p, c_void_p, c_void_p, c_int64, c_void_p,
+                                                c_int32, P(Batch), CuSplit, c_void_p, c_void_p]),
     "duet_attn_iteration": (c_int32, [c_void_p, P(Shape), P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p,
                                       c_int32, P(Batch), CuSplit, c_void_p, c_size_t, P(c_void_p), c_void_p]),
     "duet_lookahead_workspace_bytes": (c_int32, [P(Shape), P(Batch), c_int32, P(c_size_t)]),

@@ -41,8 +41,19 @@ constexpr size_t kCounterOffset = 128;
 constexpr int kMaxLayers = 1024;
 constexpr int kMaxLookahead = 64;     // decode steps per look-ahead call
 constexpr size_t kMaxGraphs = 128;    // cached decode-step graphs per context
+// Scratch of duet_attn_mixed_batch_noalloc: the workspace of one call (work lists, decode queue
+// counters, split-K partials) in a file-scope device array, for callers that cannot allocate.
+// Each device the library runs on holds its own copy until the process ends.  In host code the
+// array's name is not a device address: its address on a device comes from hipGetSymbolAddress
+// (duet_init, with the device current) and is kept in the context.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+// Pinned staging allocated up front for each slot, so that the no-allocation path never grows it.
+constexpr size_t kStagingPrealloc = size_t(1) << 20;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+static __device__ __align__(256) char scratch[kScratchBytes];
+static_assert(kScratchBytes == DUET_NOALLOC_SCRATCH_BYTES, "the header states the scratch size");
 
 #define HIP_TRY(expr)                                                                       \
   do {                                                                                      \
@@ -347,6 +358,7 @@ struct duet_ctx {
   std::vector<hipEvent_t> ev_step;  // decode stream: before step 0, after each step
   int prof_steps = 0;               // decode steps of the last profiled call (0: not look-ahead)
   duet::GemmCache* gemm = nullptr;  // hipBLASLt handle and planned GEMMs of the block forward
+  void* scratch_dev = nullptr;      // this device's copy of `scratch` (no-allocation path)
 };
 
 namespace {
@@ -400,8 +412,11 @@ int ensure_layer_events(duet_ctx* ctx, int layers) {
   return DUET_OK;
 }
 
-int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st) {
+int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st, bool may_allocate = true) {
   StagingSlot& slot = ctx->slots[ctx->next_slot];
+  if (!may_allocate && slot.cap < p.upload_bytes)
+    return fail(DUET_EWORKSPACE, "work lists of %zu bytes exceed the %zu bytes of preallocated staging", p.upload_bytes,
+                slot.cap);
   ctx->next_slot = (ctx->next_slot + 1) % kStagingSlots;
   if (slot.pending) {
     HIP_TRY(hipEventSynchronize(slot.done));
@@ -530,10 +545,24 @@ void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char
   w->prefill_id_cap = p.prefill_id_cap;
 }
 
+// A masked stream the context already holds (no creation): the no-allocation path's lookup.
+int find_stream(duet_ctx* ctx, int cus, int high_end, hipStream_t* out) {
+  const auto key = std::make_pair(cus, cus == ctx->num_cus ? 0 : high_end);
+  auto it = ctx->streams.find(key);
+  if (it == ctx->streams.end())
+    return fail(DUET_EINVAL, "no CU-masked stream for %d CUs (%s end) yet: the no-allocation path creates none; run "
+                "one allocating call with this split first", cus, key.second ? "high" : "low");
+  ctx->last_use[key] = ++ctx->use_clock;
+  *out = it->second;
+  return DUET_OK;
+}
+
+// no_alloc: the workspace is the context's scratch, streams must exist, staging never grows and
+// no profiling events are created (profiling is ignored).
 int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* const* q_l,
                 const void* const* k_l, const void* const* v_l, int64_t num_phys_pages, const int32_t* page_table,
                 int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* workspace,
-                size_t workspace_bytes, void* const* out_l, void* stream) {
+                size_t workspace_bytes, void* const* out_l, void* stream, bool no_alloc = false) {
   int rc = check_call(ctx, shape, layers, q_l, k_l, v_l, num_phys_pages, page_table, max_pages_per_req, batch, split,
                       workspace, out_l, 0);
   if (rc) return rc;
@@ -543,18 +572,22 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   plan_batch(shape, batch, layers, 1, &p, true);
   if (split.mode == DUET_SPLIT) snake_prefill_rounds(&p.pitems);
   if (workspace_bytes < p.total)
-    return fail(DUET_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, p.total);
+    return fail(DUET_EWORKSPACE, "%s %zu bytes, need %zu", no_alloc ? "scratch holds" : "workspace", workspace_bytes,
+                p.total);
 
   hipStream_t order = static_cast<hipStream_t>(stream);
   hipStream_t sd = order, sp = order;
   HIP_TRY(hipSetDevice(ctx->device));
+  auto stream_for = [&](int cus, int high_end, hipStream_t* out) {
+    return no_alloc ? find_stream(ctx, cus, high_end, out) : get_stream(ctx, cus, high_end, out);
+  };
   if (split.mode == DUET_SPLIT) {
-    if ((rc = get_stream(ctx, split.cus_decode, 0, &sd))) return rc;
-    if ((rc = get_stream(ctx, split.cus_prefill, 1, &sp))) return rc;
+    if ((rc = stream_for(split.cus_decode, 0, &sd))) return rc;
+    if ((rc = stream_for(split.cus_prefill, 1, &sp))) return rc;
   } else if (split.mode == DUET_CONCURRENT) {
     // two streams whose masks both cover every CU
-    if ((rc = get_stream(ctx, ctx->num_cus, 0, &sd))) return rc;
-    if ((rc = get_stream(ctx, ctx->num_cus, 1, &sp))) return rc;
+    if ((rc = stream_for(ctx->num_cus, 0, &sd))) return rc;
+    if ((rc = stream_for(ctx->num_cus, 1, &sp))) return rc;
   }
   const bool forked = split.mode != DUET_AGG;
 
@@ -562,12 +595,12 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
   AttnArgs a;
   WorkArgs w;
   base_args(ctx, shape, p, ws, split, page_table, num_phys_pages, max_pages_per_req, &a, &w);
-  const bool prof_iter = ctx->profiling >= 1;
-  const bool prof = ctx->profiling >= 2;
+  const bool prof_iter = ctx->profiling >= 1 && !no_alloc;
+  const bool prof = ctx->profiling >= 2 && !no_alloc;
   const bool has_decode = w.n_dreq > 0, has_prefill = w.n_pitems > 0;
 
   if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvFork], order));
-  if ((rc = stage_upload(ctx, p, ws, order))) return rc;
+  if ((rc = stage_upload(ctx, p, ws, order, !no_alloc))) return rc;
   auto layer_args = [&](int l) {
     AttnArgs al = a;
     al.q = q_l[l];
@@ -629,6 +662,7 @@ int attn_layers(duet_ctx* ctx, const duet_shape* shape, int layers, const void* 
     HIP_TRY(hipStreamWaitEvent(order, ctx->ev_pjoin, 0));
   }
   if (prof_iter) HIP_TRY(hipEventRecord(ctx->prof[kEvJoin], order));
+  if (no_alloc) return DUET_OK;  // the last profiled call's events stay valid
   ctx->prof_valid = prof_iter;
   ctx->prof_kernels = prof;
   ctx->prof_deferred = defer;
@@ -1178,6 +1212,17 @@ int duet_init(int device, duet_ctx** out) {
       return cleanup(fail(DUET_EHIP, "event creation failed"));
   if (hipMalloc(&ctx->dev_flag, 256) != hipSuccess || hipMemset(ctx->dev_flag, 0, 256) != hipSuccess)
     return cleanup(fail(DUET_EHIP, "device flag allocation failed"));
+  // This device's copy of the no-allocation scratch (the device is current).
+  {
+    const hipError_t e = hipGetSymbolAddress(&ctx->scratch_dev, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ctx->scratch_dev)
+      return cleanup(fail(DUET_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e)));
+  }
+  for (auto& sl : ctx->slots) {
+    if (hipHostMalloc(&sl.host, kStagingPrealloc, hipHostMallocDefault) != hipSuccess)
+      return cleanup(fail(DUET_ENOMEM, "pinned staging allocation of %zu bytes failed", kStagingPrealloc));
+    sl.cap = kStagingPrealloc;
+  }
   ctx->dev_sink = reinterpret_cast<unsigned*>(ctx->dev_flag) + 16;
   *out = ctx;
   return DUET_OK;
@@ -1372,6 +1417,17 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
   clear_error();
   return attn_layers(ctx, shape, 1, &q, &k_cache, &v_cache, num_phys_pages, page_table, max_pages_per_req, batch,
                      split, workspace, workspace_bytes, &out, stream);
+}
+
+int duet_attn_mixed_batch_noalloc(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
+                                  const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
+                                  int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* out,
+                                  void* stream) {
+  clear_error();
+  if (!ctx) return fail(DUET_EINVAL, "ctx is NULL");
+  if (!ctx->scratch_dev) return fail(DUET_EHIP, "the context holds no scratch address");
+  return attn_layers(ctx, shape, 1, &q, &k_cache, &v_cache, num_phys_pages, page_table, max_pages_per_req, batch,
+                     split, ctx->scratch_dev, kScratchBytes, &out, stream, true);
 }
 
 int duet_attn_iteration(duet_ctx* ctx, const duet_shape* shape, const void* const* q, const void* const* k_cache,
