@@ -181,12 +181,21 @@ int duet_model_get_sharing_tables(const duet_model* m, int32_t n, int32_t* cus, 
  * decode latency is never under-predicted (appendix: under-prediction is the harmful
  * direction). */
 int duet_model_set_efficiency(duet_model* m, double prefill_eff, double decode_eff);
+/* Fixed latency tables, seconds per layer: when the requests a prediction covers include
+ * prefill (decode) requests, each layer adds prefill_s[i] (decode_s[i]) of the share cus[i] =
+ * 8 (i + 1).  An extension of the Section 4.1 roofline for what a roofline leaves out (kernel
+ * launches, the decode kernel's tail when its last work items finish); all zero by default,
+ * which is the paper's model.  Entries >= 0 and finite; not cleared by duet_model_set_tables. */
+int duet_model_set_launch_tables(duet_model* m, int32_t n, const int32_t* cus, const double* prefill_s,
+                                 const double* decode_s);
+int duet_model_get_launch_tables(const duet_model* m, int32_t n, int32_t* cus, double* prefill_s, double* decode_s);
 int duet_model_save(const duet_model* m, const char* path); /* small JSON file */
 int duet_model_load(duet_model* m, const char* path);
 
 /* Predicted latency (microseconds) of one iteration of shape->num_layers layers.
- * AGG: L * sum_r max(F_r / Pi(256), B_r / B(256)) over all requests.
- * SPLIT: max(k * t_d(S_d), t_p(S_p)) with t_X(S) = L * sum_{r in X} max(F_r / Pi(S), B_r / B(S)).
+ * AGG: L * (sum_r max(F_r / Pi(256), B_r / B(256)) + the launch terms of the kinds present).
+ * SPLIT: max(k * t_d(S_d), t_p(S_p)) with t_X(S) = L * (sum_{r in X} max(F_r / Pi(S), B_r / B(S))
+ * + launch_X(S) if X holds a request).
  * F_r = 4 h_q q (q + c) d + 2 h_q q (q + c); B_r = 2 h_q q d b + 2 h_kv (q + c) d b.
  * m may be NULL (nominal tables). */
 int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
@@ -194,7 +203,7 @@ int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, cons
 
 /* Algorithm 1: aggregated if the whole-GPU prediction meets tbt_slo_us, else the (S_p, S_d, k)
  * maximising (k T_decode + T_prefill) / max(k t_d, t_p) subject to t_d <= tbt_slo_us, with S_d in
- * 8, 16, ..., 248 and k in {floor(t_p/t_d), floor(t_p/t_d) + 1} minus 0.  Ties keep the first
+ * 32, 64, ..., 224 (DUET_SPLIT_STEP) and k in {floor(t_p/t_d), floor(t_p/t_d) + 1} minus 0.  Ties keep the first
  * (smallest S_d, then smaller k).  max_decode_steps > 0 caps k at the number of decode steps the
  * caller can launch ahead (Section 4.3, look-ahead decode): both candidates are clamped to the
  * cap, which keeps the best allowed k because rho rises in k up to floor(t_p/t_d) and falls after

@@ -23,6 +23,10 @@ Full-model estimate (Section 4.1, "Token-Level Operators", "Overall Estimation")
   residual add F = n d, B = 3 n d b; the classifier runs on one row per request; options give the
   true GQA QKV width (h_q + 2 h_kv) d_h and a fused gate-up of width 2 m.
 
+Extension (zero by default, which leaves the paper's model): a fixed latency per layer of each
+partition kind on S CUs -- kernel launches and the decode kernel's tail, which no roofline
+term sees -- added once per layer when the requests priced hold that kind.
+
 Readings where the paper is silent (each also listed in the design notes):
   * The paper steps S_d by one TPC.  On MI355X the step is 32 CUs, S_d = 32, 64, ..., S - 32: a
     CU-mask bit b selects a CU on XCD b mod 8 and shader engine (b / 8) mod 4, the dispatcher
@@ -61,15 +65,27 @@ def attn_bytes(q: int, c: int, h_q: int, h_kv: int, d_h: int, b: int) -> float:
 
 @dataclass
 class Tables:
-    """Achievable compute (FLOP/s) and HBM bandwidth (B/s) as functions of the CU count."""
+    """Achievable compute (FLOP/s) and HBM bandwidth (B/s) as functions of the CU count, and the
+    fixed seconds per layer of each partition kind (absent: zero, the paper's model)."""
     flops: dict
     bw: dict
+    launch_prefill: dict = None
+    launch_decode: dict = None
 
     def pi(self, s: int) -> float:
         return self.flops[s]
 
     def b(self, s: int) -> float:
         return self.bw[s]
+
+    def launch(self, kinds, s: int) -> float:
+        """Fixed seconds per layer for a set of requests holding the given kinds (0 prefill, 1 decode)."""
+        t = 0.0
+        if 0 in kinds and self.launch_prefill:
+            t += self.launch_prefill[s]
+        if 1 in kinds and self.launch_decode:
+            t += self.launch_decode[s]
+        return t
 
 
 def nominal_tables() -> Tables:
@@ -85,9 +101,14 @@ def t_attn(reqs, s: int, tables: Tables, h_q: int, h_kv: int, d_h: int, b: int) 
                for q, c in reqs)
 
 
-def f_roofline(reqs, s, tables, *, h_q, h_kv, d_h, b, layers) -> float:
-    """Seconds for the attention of all `layers` layers (t_total = L t_block, attention only)."""
-    return layers * t_attn(reqs, s, tables, h_q, h_kv, d_h, b)
+def f_roofline(reqs, s, tables, *, h_q, h_kv, d_h, b, layers, kinds=()) -> float:
+    """Seconds for the attention of all `layers` layers (t_total = L t_block, attention only);
+    `kinds`: the request kinds present, whose fixed per-layer latency is added."""
+    return layers * (t_attn(reqs, s, tables, h_q, h_kv, d_h, b) + tables.launch(kinds, s))
+
+
+def kinds_of(batch):
+    return {k for k, _, _ in batch}
 
 
 def split_requests(batch):
@@ -101,10 +122,10 @@ def predict(batch, mode, s_p, s_d, k, tables, *, h_q, h_kv, d_h, b, layers, tota
     """Predicted iteration latency in seconds: aggregated on all CUs, or max(k t_d(S_d), t_p(S_p))."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
     if mode == AGG:
-        return f_roofline([(q, c) for _, q, c in batch], total, tables, **kw)
+        return f_roofline([(q, c) for _, q, c in batch], total, tables, kinds=kinds_of(batch), **kw)
     pre, dec = split_requests(batch)
-    t_d = f_roofline(dec, s_d, tables, **kw) if dec else 0.0
-    t_p = f_roofline(pre, s_p, tables, **kw) if pre else 0.0
+    t_d = f_roofline(dec, s_d, tables, kinds={1}, **kw) if dec else 0.0
+    t_p = f_roofline(pre, s_p, tables, kinds={0}, **kw) if pre else 0.0
     return max(k * t_d, t_p)
 
 
@@ -114,7 +135,7 @@ def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, st
     None leaves them as the paper states."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
     mixed = [(q, c) for _, q, c in batch]
-    t_mixed = f_roofline(mixed, total, tables, **kw)
+    t_mixed = f_roofline(mixed, total, tables, kinds=kinds_of(batch), **kw)
     if t_mixed <= tau:
         return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=0)
     pre, dec = split_requests(batch)
@@ -122,11 +143,11 @@ def choose(batch, tau, tables, *, h_q, h_kv, d_h, b, layers, total=TOTAL_CUS, st
     t_prefill_tokens = sum(q for q, _ in pre)
     best_rho, best = 0.0, None
     for s_d in range(step, total, step):
-        t_d = f_roofline(dec, s_d, tables, **kw)
+        t_d = f_roofline(dec, s_d, tables, kinds={1} if dec else (), **kw)
         if t_d > tau:
             continue
         s_p = total - s_d
-        t_p = f_roofline(pre, s_p, tables, **kw)
+        t_p = f_roofline(pre, s_p, tables, kinds={0} if pre else (), **kw)
         base = math.floor(t_p / t_d) if t_d > 0 else 1
         # rho(k) rises up to k = base and falls from k = base + 1 on, so under a cap on the
         # decode steps the best allowed candidates are base and base + 1 clamped to the cap
@@ -201,11 +222,11 @@ def t_cls(n_rows, s, tables, block, *, h_q, d_h, b):
     return max(f / tables.pi(s), by / tables.b(s))
 
 
-def f_model(reqs, s, tables, block, *, h_q, h_kv, d_h, b, layers) -> float:
+def f_model(reqs, s, tables, block, *, h_q, h_kv, d_h, b, layers, kinds=()) -> float:
     """t_total = L (t_tok + t_attn) + t_cls for the requests [(q, c), ...] on s CUs."""
     n = sum(q for q, _ in reqs)
     per_layer = t_tok(n, s, tables, block, h_q=h_q, h_kv=h_kv, d_h=d_h, b=b) + \
-        t_attn(reqs, s, tables, h_q, h_kv, d_h, b)
+        t_attn(reqs, s, tables, h_q, h_kv, d_h, b) + tables.launch(kinds, s)
     return layers * per_layer + t_cls(len(reqs), s, tables, block, h_q=h_q, d_h=d_h, b=b)
 
 
@@ -214,10 +235,10 @@ def predict_model(batch, mode, s_p, s_d, k, tables, block, *, h_q, h_kv, d_h, b,
     partition runs all layers for its own tokens."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
     if mode == AGG:
-        return f_model([(q, c) for _, q, c in batch], total, tables, block, **kw)
+        return f_model([(q, c) for _, q, c in batch], total, tables, block, kinds=kinds_of(batch), **kw)
     pre, dec = split_requests(batch)
-    t_d = f_model(dec, s_d, tables, block, **kw)
-    t_p = f_model(pre, s_p, tables, block, **kw)
+    t_d = f_model(dec, s_d, tables, block, kinds={1} if dec else (), **kw)
+    t_p = f_model(pre, s_p, tables, block, kinds={0} if pre else (), **kw)
     return max(k * t_d, t_p)
 
 
@@ -225,7 +246,7 @@ def choose_model(batch, tau, tables, block, *, h_q, h_kv, d_h, b, layers, total=
                  kmax=None):
     """Algorithm 1 on the full-model estimate (same steps as choose)."""
     kw = dict(h_q=h_q, h_kv=h_kv, d_h=d_h, b=b, layers=layers)
-    t_mixed = f_model([(q, c) for _, q, c in batch], total, tables, block, **kw)
+    t_mixed = f_model([(q, c) for _, q, c in batch], total, tables, block, kinds=kinds_of(batch), **kw)
     if t_mixed <= tau:
         return dict(mode=AGG, s_p=total, s_d=0, k=1, rho=None, t=t_mixed, flags=0)
     pre, dec = split_requests(batch)
@@ -233,11 +254,11 @@ def choose_model(batch, tau, tables, block, *, h_q, h_kv, d_h, b, layers, total=
     t_prefill_tokens = sum(q for q, _ in pre)
     best_rho, best = 0.0, None
     for s_d in range(step, total, step):
-        t_d = f_model(dec, s_d, tables, block, **kw)
+        t_d = f_model(dec, s_d, tables, block, kinds={1} if dec else (), **kw)
         if t_d > tau:
             continue
         s_p = total - s_d
-        t_p = f_model(pre, s_p, tables, block, **kw)
+        t_p = f_model(pre, s_p, tables, block, kinds={0} if pre else (), **kw)
         base = math.floor(t_p / t_d) if t_d > 0 else 1
         cands = (base, base + 1) if kmax is None else tuple(sorted({min(base, kmax), min(base + 1, kmax)}))
         for k in cands:

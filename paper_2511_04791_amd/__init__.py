@@ -132,6 +132,20 @@ class Model:
                 "duet_model_get_sharing_tables")
         return list(cus), list(fl), list(by), bool(flag.value)
 
+    def set_launch_tables(self, prefill_s, decode_s):
+        """Fixed seconds per layer of each partition kind on every share (zero: the paper's model)."""
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus = (ctypes.c_int32 * n)(*range(N.CU_STEP, N.TOTAL_CUS + 1, N.CU_STEP))
+        lp = (ctypes.c_double * n)(*[float(x) for x in prefill_s])
+        ld = (ctypes.c_double * n)(*[float(x) for x in decode_s])
+        N.check(N.lib().duet_model_set_launch_tables(self.handle, n, cus, lp, ld), "duet_model_set_launch_tables")
+
+    def launch_tables(self):
+        n = N.TOTAL_CUS // N.CU_STEP
+        cus, lp, ld = (ctypes.c_int32 * n)(), (ctypes.c_double * n)(), (ctypes.c_double * n)()
+        N.check(N.lib().duet_model_get_launch_tables(self.handle, n, cus, lp, ld), "duet_model_get_launch_tables")
+        return list(cus), list(lp), list(ld)
+
     def set_efficiency(self, prefill_eff: float, decode_eff: float):
         N.check(N.lib().duet_model_set_efficiency(self.handle, prefill_eff, decode_eff), "duet_model_set_efficiency")
 

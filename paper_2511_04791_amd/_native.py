@@ -64,6 +64,8 @@ _SIGS = {
     "duet_model_set_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_get_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_set_efficiency": (c_int32, [c_void_p, c_double, c_double]),
+    "duet_model_set_launch_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
+    "duet_model_get_launch_tables": (c_int32, [c_void_p, c_int32, P(c_int32), P(c_double), P(c_double)]),
     "duet_model_save": (c_int32, [c_void_p, ctypes.c_char_p]),
     "duet_model_load": (c_int32, [c_void_p, ctypes.c_char_p]),
     "duet_predict_iter_latency": (c_int32, [c_void_p, P(Shape), P(Batch), CuSplit, P(c_double)]),

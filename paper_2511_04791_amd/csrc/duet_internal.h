@@ -29,6 +29,11 @@ struct duet_model {
   double flops_shared[duet::kNumCuSteps];
   double bytes_shared[duet::kNumCuSteps];
   bool has_shared = false;
+  // Fixed seconds per layer of each partition kind on S CUs, added once per layer when the batch
+  // holds requests of that kind (kernel launches and the decode kernel's tail); zero by default,
+  // which is the paper's model.
+  double launch_prefill[duet::kNumCuSteps];
+  double launch_decode[duet::kNumCuSteps];
   double prefill_eff = 1.0;
   double decode_eff = 1.0;
   bool calibrated = false;

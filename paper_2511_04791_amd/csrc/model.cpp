@@ -8,7 +8,10 @@
 // TBT bound; otherwise the split (S_p, S_d, k) that maximises token throughput
 // (k T_decode + T_prefill) / max(k t_d(S_d), t_p(S_p)) subject to t_d(S_d) <= tau.
 //
-// On MI355X the partition unit is 8 CUs (one per XCD), so tables hold S = 8, 16, ..., 256.
+// Tables hold S = 8, 16, ..., 256 (one CU per XCD per step); Algorithm 1 searches S_d in steps of
+// 32 CUs (one CU per shader engine of every XCD), the shares on which work spreads evenly.
+// Extension: a fixed latency per layer of each partition kind on S CUs (kernel launches, the
+// decode kernel's tail), zero by default, added when the batch holds requests of that kind.
 #include <cerrno>
 #include <cmath>
 #include <cstdarg>
@@ -79,6 +82,7 @@ double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b,
   const double bw = (tab ? m->bytes_shared[i] : m->bytes[i]) * (shared ? m->decode_eff : 1.0);
   double t = 0.0, n = 0.0;
   int n_req = 0;
+  bool any_pre = false, any_dec = false;
   for (int r = 0; r < b->num_reqs; ++r) {
     const duet_seq_meta& rq = b->reqs[r];
     if (kind >= 0 && rq.kind != kind) continue;
@@ -86,7 +90,9 @@ double f_roofline(const duet_model* m, const duet_shape* s, const duet_batch* b,
     t += std::fmax(rc.flops / pi, rc.bytes / bw);
     n += rq.q_len;
     ++n_req;
+    (rq.kind == DUET_KIND_DECODE ? any_dec : any_pre) = true;
   }
+  t += (any_pre ? m->launch_prefill[i] : 0.0) + (any_dec ? m->launch_decode[i] : 0.0);
   if (!blk || n_req == 0) return s->num_layers * t;
   double total = s->num_layers * (token_level(n, s, blk, pi, bw) + t);
   if (blk->vocab_size > 0) {
@@ -179,6 +185,7 @@ void model_init_nominal(duet_model* m) {
     m->bytes[i] = kNominalHbmBytes * frac;
   }
   m->has_shared = false;
+  for (int i = 0; i < kNumCuSteps; ++i) m->launch_prefill[i] = m->launch_decode[i] = 0.0;
   m->prefill_eff = 1.0;
   m->decode_eff = 1.0;
   m->calibrated = false;
@@ -291,6 +298,34 @@ int duet_model_get_tables(const duet_model* m, int32_t n, int32_t* cus, double* 
   return DUET_OK;
 }
 
+int duet_model_set_launch_tables(duet_model* m, int32_t n, const int32_t* cus, const double* prefill_s,
+                                 const double* decode_s) {
+  if (!m || !cus || !prefill_s || !decode_s) return fail(DUET_EINVAL, "NULL argument");
+  if (n != kNumCuSteps) return fail(DUET_EINVAL, "expected %d table entries, got %d", kNumCuSteps, n);
+  for (int i = 0; i < n; ++i) {
+    if (cus[i] != DUET_CU_STEP * (i + 1))
+      return fail(DUET_EINVAL, "cus[%d] = %d, expected %d", i, cus[i], DUET_CU_STEP * (i + 1));
+    if (!(prefill_s[i] >= 0) || !(decode_s[i] >= 0) || !std::isfinite(prefill_s[i]) || !std::isfinite(decode_s[i]))
+      return fail(DUET_EINVAL, "launch table entry %d not finite and >= 0", i);
+  }
+  for (int i = 0; i < n; ++i) {
+    m->launch_prefill[i] = prefill_s[i];
+    m->launch_decode[i] = decode_s[i];
+  }
+  return DUET_OK;
+}
+
+int duet_model_get_launch_tables(const duet_model* m, int32_t n, int32_t* cus, double* prefill_s, double* decode_s) {
+  if (!m || !cus || !prefill_s || !decode_s) return fail(DUET_EINVAL, "NULL argument");
+  if (n != kNumCuSteps) return fail(DUET_EINVAL, "expected %d table entries", kNumCuSteps);
+  for (int i = 0; i < n; ++i) {
+    cus[i] = DUET_CU_STEP * (i + 1);
+    prefill_s[i] = m->launch_prefill[i];
+    decode_s[i] = m->launch_decode[i];
+  }
+  return DUET_OK;
+}
+
 int duet_model_set_efficiency(duet_model* m, double prefill_eff, double decode_eff) {
   if (!m) return fail(DUET_EINVAL, "model is NULL");
   if (!(prefill_eff > 0 && prefill_eff <= 1) || !(decode_eff > 0 && decode_eff <= 1))
@@ -304,11 +339,13 @@ int duet_model_save(const duet_model* m, const char* path) {
   if (!m || !path) return fail(DUET_EINVAL, "NULL argument");
   FILE* f = std::fopen(path, "w");
   if (!f) return fail(DUET_EIO, "cannot open %s for writing", path);
-  std::fprintf(f, "{\"version\": 2, \"calibrated\": %d, \"prefill_eff\": %.17g, \"decode_eff\": %.17g,\n",
+  std::fprintf(f, "{\"version\": 3, \"calibrated\": %d, \"prefill_eff\": %.17g, \"decode_eff\": %.17g,\n",
                m->calibrated ? 1 : 0, m->prefill_eff, m->decode_eff);
-  const char* names[5] = {"cus", "flops_per_s", "bytes_per_s", "shared_flops_per_s", "shared_bytes_per_s"};
-  const double* tabs[5] = {nullptr, m->flops, m->bytes, m->flops_shared, m->bytes_shared};
-  const int n_arrays = m->has_shared ? 5 : 3;
+  const char* names[7] = {"cus", "flops_per_s", "bytes_per_s", "launch_prefill_s", "launch_decode_s",
+                          "shared_flops_per_s", "shared_bytes_per_s"};
+  const double* tabs[7] = {nullptr, m->flops, m->bytes, m->launch_prefill, m->launch_decode, m->flops_shared,
+                           m->bytes_shared};
+  const int n_arrays = m->has_shared ? 7 : 5;
   for (int k = 0; k < n_arrays; ++k) {
     std::fprintf(f, " \"%s\": [", names[k]);
     for (int i = 0; i < kNumCuSteps; ++i) {
@@ -394,6 +431,12 @@ int duet_model_load(duet_model* m, const char* path) {
     if (sfl.size() != cus.size() || sby.size() != cus.size())
       return fail(DUET_EIO, "%s: sharing tables must hold %d entries", path, kNumCuSteps);
     if ((rc = duet_model_set_sharing_tables(&tmp, kNumCuSteps, ci.data(), sfl.data(), sby.data()))) return rc;
+  }
+  std::vector<double> lp, ld;
+  if (read_array(s, "launch_prefill_s", &lp) && read_array(s, "launch_decode_s", &ld)) {
+    if (lp.size() != cus.size() || ld.size() != cus.size())
+      return fail(DUET_EIO, "%s: launch tables must hold %d entries", path, kNumCuSteps);
+    if ((rc = duet_model_set_launch_tables(&tmp, kNumCuSteps, ci.data(), lp.data(), ld.data()))) return rc;
   }
   rc = duet_model_set_efficiency(&tmp, pe, de);
   if (rc) return rc;

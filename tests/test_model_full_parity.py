@@ -25,6 +25,13 @@ def _tables(rng):
     return pis, bws
 
 
+def _launch(rng):
+    """Fixed per-layer latencies: zero (the paper's model) for a third of the draws."""
+    if rng.uniform() < 1 / 3:
+        return [0.0] * 32, [0.0] * 32
+    return list(rng.uniform(0, 50e-6, 32)), list(rng.uniform(0, 50e-6, 32))
+
+
 def _batch(rng):
     rows = [(1, 1, int(rng.integers(16, 20000))) for _ in range(int(rng.integers(0, 96)))]
     for _ in range(int(rng.integers(0, 3))):
@@ -49,7 +56,9 @@ def test_predict_model_matches_oracle(shape):
         pis, bws = _tables(rng)
         model = duet.Model()
         model.set_tables(pis, bws)
-        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)))
+        lp, ld = _launch(rng)
+        model.set_launch_tables(lp, ld)
+        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)), dict(zip(CUS, lp)), dict(zip(CUS, ld)))
         rows = _batch(rng)
         want = orf.predict_model(rows, orf.AGG, 256, 0, 1, tab, _oblock(blk), **_kw(shape))
         got = duet.predict_model_latency(rows, duet.CuSplit.agg(), shape, blk, model)
@@ -71,7 +80,9 @@ def test_choose_model_matches_oracle(cap):
         pis, bws = _tables(rng)
         model = duet.Model()
         model.set_tables(pis, bws)
-        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)))
+        lp, ld = _launch(rng)
+        model.set_launch_tables(lp, ld)
+        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)), dict(zip(CUS, lp)), dict(zip(CUS, ld)))
         rows = _batch(rng)
         t_mixed = orf.predict_model(rows, orf.AGG, 256, 0, 1, tab, _oblock(blk), **_kw(shape))
         tau = t_mixed * float(rng.uniform(0.05, 1.2))

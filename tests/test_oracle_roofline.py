@@ -221,3 +221,25 @@ def test_capped_algorithm1_equals_exhaustive_search_over_allowed_k(kmax):
         assert got["rho"] == pytest.approx(rho, rel=1e-12)
         assert (got["s_p"], got["s_d"], got["k"]) == cfg
     assert checked >= 20
+
+
+def test_launch_terms_closed_form():
+    """The fixed per-layer latencies enter once per layer and per kind present, written out by hand
+    for a two-request batch; zero tables leave the paper's model unchanged."""
+    cus = range(8, 257, 8)
+    tab0 = orf.Tables({s: 1e15 for s in cus}, {s: 4e12 for s in cus})
+    tab = orf.Tables({s: 1e15 for s in cus}, {s: 4e12 for s in cus}, {s: 7e-6 for s in cus}, {s: 3e-6 for s in cus})
+    kw = dict(h_q=8, h_kv=2, d_h=64, b=2, layers=5)
+    batch = [(0, 100, 20), (1, 1, 999)]
+    # prefill request: F = 4*8*100*120*64 + 2*8*100*120, B = 2*8*100*64*2 + 2*2*120*64*2
+    fp, bp = 4 * 8 * 100 * 120 * 64 + 2 * 8 * 100 * 120, 2 * 8 * 100 * 64 * 2 + 2 * 2 * 120 * 64 * 2
+    # decode request: q = 1, c = 999
+    fd, bd = 4 * 8 * 1 * 1000 * 64 + 2 * 8 * 1000, 2 * 8 * 1 * 64 * 2 + 2 * 2 * 1000 * 64 * 2
+    tp, td = max(fp / 1e15, bp / 4e12), max(fd / 1e15, bd / 4e12)
+    agg = orf.predict(batch, orf.AGG, 256, 0, 1, tab, **kw)
+    assert agg == pytest.approx(5 * (tp + td + 7e-6 + 3e-6), rel=1e-14)
+    assert orf.predict(batch, orf.AGG, 256, 0, 1, tab0, **kw) == pytest.approx(5 * (tp + td), rel=1e-14)
+    split = orf.predict(batch, orf.SPLIT, 128, 128, 3, tab, **kw)
+    assert split == pytest.approx(max(3 * 5 * (td + 3e-6), 5 * (tp + 7e-6)), rel=1e-14)
+    # a decode-only batch carries no prefill launch term
+    assert orf.predict([(1, 1, 999)], orf.AGG, 256, 0, 1, tab, **kw) == pytest.approx(5 * (td + 3e-6), rel=1e-14)
