@@ -279,23 +279,50 @@ def run_config(ctx, key, args, calib):
         return {k_: statistics.fmean(r[k_] for r in rec) for k_ in rec[0]}
 
     ctx.attn_iteration(qs, kcs, vcs, pt, meta, duet.CuSplit.agg(), outs=outs, check_errors=True)
+
+    def fork_to_join(split, n=5, warm=2):
+        """Mean latency of one call, synchronised, from HIP events on the caller's stream around it
+        (the library's own profiling is off, so look-ahead decode steps run as one graph)."""
+        call = caller(split)
+        st = torch.cuda.current_stream()
+        ts = []
+        for i in range(warm + n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            call()
+            e1.record(st)
+            e1.synchronize()
+            if i >= warm:
+                ts.append(e0.elapsed_time(e1) * 1e3)
+        return statistics.fmean(ts)
     # kernel durations on one decode step (k = 1) of the chosen split and of AGG
     kern_split = profiled(duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT
                           else duet.CuSplit.agg(), level=2)
     kern_agg = profiled(duet.CuSplit.agg(), level=2)
     it_chosen = profiled(chosen)
     it_agg = profiled(agg)
-    # every split of the grid (one decode step), measured beside the model's prediction
+    ftj_chosen, ftj_agg = fork_to_join(chosen), fork_to_join(agg)
+    # every split of the grid (one decode step), measured beside the model's prediction of the
+    # iteration and of each half
     sweep = []
+    has_both = bool((batch.kinds == 0).any() and (batch.kinds == 1).any())
     for s_p in range(256 - 32, 0, -32):
         sp_ = duet.CuSplit.split(s_p, 256 - s_p)
-        m_ = profiled(sp_, n=3, warm=1)
-        sweep.append({"Sp": s_p, "Sd": 256 - s_p, "measured_us": round(m_["iteration_us"], 1),
-                      "predicted_us": round(duet.predict_iter_latency(rows3, sp_, shape, ctx.model), 1)})
+        m_ = profiled(sp_, n=3, warm=1, level=2)
+        row = {"Sp": s_p, "Sd": 256 - s_p, "measured_us": round(m_["iteration_us"], 1),
+               "predicted_us": round(duet.predict_iter_latency(rows3, sp_, shape, ctx.model), 1)}
+        if has_both:
+            row["decode_measured_us"] = round(m_["decode_total_us"], 1)
+            row["decode_predicted_us"] = round(duet.predict_partition_latency(rows3, 1, 256 - s_p, shape, ctx.model), 1)
+            row["prefill_measured_us"] = round(m_["prefill_total_us"], 1)
+            row["prefill_predicted_us"] = round(duet.predict_partition_latency(rows3, 0, s_p, shape, ctx.model), 1)
+        sweep.append(row)
     agg1 = it_agg if k == 1 else profiled(duet.CuSplit.agg())
     sweep_agg = {"measured_us": round(agg1["iteration_us"], 1), "predicted_us": round(agg_pred, 1)}
     best = min(sweep, key=lambda r: r["measured_us"])
     errs = [(r["predicted_us"] - r["measured_us"]) / r["measured_us"] for r in sweep]
+    dec_errs = [(r["decode_predicted_us"] - r["decode_measured_us"]) / r["decode_measured_us"] for r in sweep
+                if r.get("decode_measured_us")]
     # Algorithm 1 under a bound 1% below the aggregated estimate: it must split, and its pick is
     # compared with the measured sweep (the predictor's out-of-sample ranking test)
     tight, tight_pred = duet.choose_cu_split(rows3, 0.99 * agg_pred, shape, ctx.model, max_decode_steps=1)[:2]
@@ -365,7 +392,7 @@ def run_config(ctx, key, args, calib):
         "predicted_us": round(pred, 1), "agg_predicted_us": round(agg_pred, 1),
         "host_choose_us": round(statistics.fmean(choose_ts) if choose_ts else host_choose_us, 2),
         "wall_us": round(wall, 1), "agg_wall_us": round(agg_wall, 1), "speedup_vs_agg": round(agg_wall / wall, 4),
-        "iteration_us": round(it_chosen["iteration_us"], 1), "agg_iteration_us": round(it_agg["iteration_us"], 1),
+        "iteration_us": round(ftj_chosen, 1), "agg_iteration_us": round(ftj_agg, 1),
         "decode_tokens_per_s": round(n_dec * k / (wall * 1e-6), 1),
         "prefill_tokens_per_s": round(q_pre / (wall * 1e-6), 1),
         "agg_decode_tokens_per_s": round(n_dec * k / (agg_wall * 1e-6), 1),
@@ -377,7 +404,9 @@ def run_config(ctx, key, args, calib):
         "sweep": sweep, "sweep_agg": sweep_agg, "sweep_best": best,
         "prediction_error": {"mean_abs": round(float(np.mean(np.abs(errs))), 4),
                              "max_abs": round(float(np.max(np.abs(errs))), 4),
-                             "agg": round((agg_pred - agg1["iteration_us"]) / agg1["iteration_us"], 4)},
+                             "agg": round((agg_pred - agg1["iteration_us"]) / agg1["iteration_us"], 4),
+                             "decode_half_min": round(float(min(dec_errs)), 4) if dec_errs else None,
+                             "decode_half_max": round(float(max(dec_errs)), 4) if dec_errs else None},
         "algorithm1_tight": {"tau_us": round(0.99 * agg_pred, 1), "chosen": str(tight),
                              "predicted_us": round(tight_pred, 1),
                              "measured_us": tight_row and tight_row["measured_us"],
@@ -386,6 +415,8 @@ def run_config(ctx, key, args, calib):
     }
     if k > 1:
         res["decode_step_us"] = round(it_chosen["decode_step_us"], 1)
+        res["decode_step_predicted_us"] = round(
+            duet.predict_partition_latency(rows3, 1, chosen.cus_decode, shape, ctx.model), 1)
         res["decode_interval_max_us"] = round(it_chosen["decode_step_us"], 1)
         res["agg_decode_interval_max_us"] = round(it_agg["prefill_total_us"] + it_agg["decode_first_step_us"], 1)
     cpu = None
@@ -407,11 +438,15 @@ def suite_main(args):
         keys.insert(0, args.headline)
     ctx = duet.Context(0)
     calib = {}
-    if not args.no_calibrate:
+    if args.model:
+        ctx.model.load(args.model)
+    elif not args.no_calibrate:
         t0 = time.perf_counter()
         calib = calibrate_model(ctx)
         calib["seconds"] = round(time.perf_counter() - t0, 2)
         print(f"[bench] calibrated in {calib['seconds']} s", file=sys.stderr, flush=True)
+    if args.save_model:
+        ctx.model.save(args.save_model)
     results = {}
     for key in keys:
         results[key] = run_config(ctx, key, args, calib)
@@ -948,6 +983,9 @@ def main():
     ap.add_argument("--split", default="", help="Sp,Sd: the one split of --block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibrate", action="store_true")
+    ap.add_argument("--model", default="", help="load a calibrated latency model (duet_model_save file) instead of "
+                                               "calibrating")
+    ap.add_argument("--save-model", default="", help="write the calibrated latency model to this file")
     ap.add_argument("--counters", action="store_true",
                     help="a short fixed pass of --headline's workload for rocprofv3 counters: Algorithm 1's split "
                          "(one decode step) for a few calls, then a plain 1 GiB device-to-device copy as the reference")
@@ -994,9 +1032,10 @@ def main():
 
 
 def counters_main(args):
-    """A short fixed pass for hardware counters: the headline workload's kernels under Algorithm 1's
-    split (one decode step per call, 4 calls), then a plain 1 GiB elementwise device copy whose
-    FETCH_SIZE / WRITE_SIZE readings scale the counters to bytes."""
+    """A short fixed pass for profilers: --steps calls of --headline's workload under Algorithm 1's
+    split at one decode step (the configuration of the benchmark's per-kernel roofline figures),
+    then a plain 1 GiB elementwise device copy whose FETCH_SIZE / WRITE_SIZE readings scale the
+    counters to bytes.  Load the benchmark's calibration with --model to get its split."""
     import dataclasses
     import torch
     import paper_2511_04791_amd as duet
@@ -1007,6 +1046,8 @@ def counters_main(args):
     shape = dataclasses.replace(batch.shape, num_layers=L)
     rows3 = [(int(k), int(ql), int(c)) for k, ql, c in zip(batch.kinds, batch.q_lens, batch.cached_lens)]
     ctx = duet.Context(0)
+    if args.model:
+        ctx.model.load(args.model)
     chosen = duet.choose_cu_split(rows3, SLO_US * L / spec["model_layers"], shape, ctx.model,
                                   max_decode_steps=spec["k_cap"])[0]
     split = duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT else duet.CuSplit.agg()
@@ -1014,9 +1055,10 @@ def counters_main(args):
     qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
     pt = torch.as_tensor(batch.page_table, device="cuda")
     outs = [torch.empty_like(q) for q in qs]
-    for _ in range(4):
+    for i in range(args.steps):
         ctx.attn_iteration(qs, kcs, vcs, pt, batch.seq_meta, split, outs=outs)
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        print(f"[counters] {args.headline} {split}: call {i + 1}/{args.steps}", file=sys.stderr, flush=True)
     del qs, kcs, vcs, outs, layers
     torch.cuda.empty_cache()
     # an elementwise kernel (not a DMA copy) that reads 1 GiB and writes 1 GiB
@@ -1024,7 +1066,8 @@ def counters_main(args):
     dst = torch.empty_like(src)
     torch.bitwise_not(src, out=dst)
     torch.cuda.synchronize()
-    print(json.dumps({"counters_pass": args.headline, "split": str(split), "layers": L}), flush=True)
+    print(json.dumps({"counters_pass": args.headline, "split": str(split), "layers": L, "calls": args.steps}),
+          flush=True)
     ctx.close()
 
 

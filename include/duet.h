@@ -201,6 +201,13 @@ int duet_model_load(duet_model* m, const char* path);
 int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
                               duet_cu_split split, double* us);
 
+/* One partition's predicted time (microseconds) for shape->num_layers layers: t_X(S) of the
+ * requests of `kind` on `cus` CUs, the quantity Algorithm 1 compares (t_d(S_d), t_p(S_p)).
+ * shared != 0 prices a half that runs beside the other (the sharing tables and efficiencies)
+ * when the batch holds both kinds.  m may be NULL (nominal tables). */
+int duet_predict_partition_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                                   int32_t kind, int32_t cus, int32_t shared, double* us);
+
 /* Algorithm 1: aggregated if the whole-GPU prediction meets tbt_slo_us, else the (S_p, S_d, k)
  * maximising (k T_decode + T_prefill) / max(k t_d, t_p) subject to t_d <= tbt_slo_us, with S_d in
  * 32, 64, ..., 224 (DUET_SPLIT_STEP) and k in {floor(t_p/t_d), floor(t_p/t_d) + 1} minus 0.  Ties keep the first

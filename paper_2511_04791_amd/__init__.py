@@ -166,6 +166,17 @@ def predict_iter_latency(batch, cu_split: CuSplit, shape: AttnShape, model: Mode
     return us.value
 
 
+def predict_partition_latency(batch, kind: int, cus: int, shape: AttnShape, model: Model | None = None,
+                              shared: bool = True) -> float:
+    """Predicted time (us) of one partition: the requests of `kind` on `cus` CUs (t_d or t_p)."""
+    b = _BatchC(batch)
+    us = ctypes.c_double()
+    N.check(N.lib().duet_predict_partition_latency(model.handle if model else None, ctypes.byref(_shape_c(shape)),
+                                                   ctypes.byref(b.c), int(kind), int(cus), int(bool(shared)),
+                                                   ctypes.byref(us)), "duet_predict_partition_latency")
+    return us.value
+
+
 def choose_cu_split(batch, tbt_slo_us: float, shape: AttnShape, model: Model | None = None,
                     max_decode_steps: int = 0):
     """Algorithm 1: returns (CuSplit, predicted_us, rho, status_flags).  max_decode_steps > 0

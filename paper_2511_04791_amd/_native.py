@@ -69,6 +69,7 @@ _SIGS = {
     "duet_model_save": (c_int32, [c_void_p, ctypes.c_char_p]),
     "duet_model_load": (c_int32, [c_void_p, ctypes.c_char_p]),
     "duet_predict_iter_latency": (c_int32, [c_void_p, P(Shape), P(Batch), CuSplit, P(c_double)]),
+    "duet_predict_partition_latency": (c_int32, [c_void_p, P(Shape), P(Batch), c_int32, c_int32, c_int32, P(c_double)]),
     "duet_choose_cu_split": (c_int32, [c_void_p, P(Shape), P(Batch), c_double, c_int32, P(CuSplit), P(c_double),
                                        P(c_double), P(c_int32)]),
     "duet_predict_model_latency": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(Batch), CuSplit, P(c_double)]),

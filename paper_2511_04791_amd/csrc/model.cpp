@@ -552,6 +552,23 @@ int duet_predict_iter_latency(const duet_model* m, const duet_shape* shape, cons
   return predict_impl(m, shape, nullptr, batch, split, us);
 }
 
+int duet_predict_partition_latency(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
+                                   int32_t kind, int32_t cus, int32_t shared, double* us) {
+  clear_error();
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_batch(shape, batch, false))) return rc;
+  if (!us) return fail(DUET_EINVAL, "us is NULL");
+  if (kind != DUET_KIND_PREFILL && kind != DUET_KIND_DECODE) return fail(DUET_EINVAL, "kind %d", kind);
+  if (cus < DUET_CU_STEP || cus > DUET_TOTAL_CUS || cus % DUET_CU_STEP)
+    return fail(DUET_EINVAL, "cus %d must be a multiple of %d in [%d, %d]", cus, DUET_CU_STEP, DUET_CU_STEP,
+                DUET_TOTAL_CUS);
+  duet_model nominal;
+  const duet_model* mm = model_or_nominal(m, &nominal);
+  *us = f_roofline(mm, shape, batch, kind, cus, shared != 0 && has_both_kinds(batch), nullptr) * 1e6;
+  return DUET_OK;
+}
+
 int duet_choose_cu_split(const duet_model* m, const duet_shape* shape, const duet_batch* batch,
                          double tbt_slo_us, int32_t max_decode_steps, duet_cu_split* out,
                          double* predicted_us, double* rho, int32_t* status_flags) {

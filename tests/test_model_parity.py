@@ -192,3 +192,25 @@ def test_sharing_tables_replace_standalone_rates_for_mixed_splits(tmp_path):
     assert is_set and np.array_equal(fl, spis) and np.array_equal(by, sbws)
     m2.set_tables(pis, bws)          # new standalone tables drop stale sharing tables
     assert m2.sharing_tables()[3] is False
+
+
+def test_partition_latency_matches_oracle():
+    """t_d(S) and t_p(S) of one partition, standalone tables (shared=False or a one-kind batch)."""
+    rng = np.random.default_rng(77)
+    shape = wl.AttnShape(32, 8, 128, "bf16", num_layers=32)
+    for _ in range(40):
+        pis, bws = _tables(rng)
+        model = duet.Model()
+        model.set_tables(pis, bws)
+        lp, ld = _launch(rng)
+        model.set_launch_tables(lp, ld)
+        tab = orf.Tables(dict(zip(CUS, pis)), dict(zip(CUS, bws)), dict(zip(CUS, lp)), dict(zip(CUS, ld)))
+        rows = _batch(rng)
+        pre, dec = orf.split_requests(rows)
+        s = int(rng.integers(1, 33)) * 8
+        for kind, reqs in ((0, pre), (1, dec)):
+            if not reqs:
+                continue
+            want = orf.f_roofline(reqs, s, tab, kinds={kind}, **_kw(shape))
+            got = duet.predict_partition_latency(rows, kind, s, shape, model, shared=False)
+            assert got == pytest.approx(want * 1e6, rel=1e-12)
