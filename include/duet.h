@@ -294,9 +294,12 @@ duet_model* duet_ctx_model(duet_ctx* ctx);
 
 /* Infrastructure (memory sizing for the iteration of Section 4.3).
  * Bytes of device workspace duet_attn_mixed_batch and duet_attn_iteration need for this shape
- * and batch: an error word, the decode work-queue counters, metadata, work lists and two
- * buffers of split-K partials (consecutive layers alternate between them).  The layers of a call
- * share all of it, so the size does not depend on shape->num_layers.  Host only. */
+ * and batch: an error word, the decode work-queue counters, metadata, work lists, two buffers
+ * of decode split-K partials (consecutive layers alternate between them) and the partial states
+ * of prefill pieces (bf16: a prefill unit whose causal key range is long against the batch's
+ * total runs as several pieces over runs of its keys, merged by the last one to finish; at most
+ * 512 pieces write a partial, 128 KiB each at head_dim 128).  The layers of a call share all of
+ * it, so the size does not depend on shape->num_layers.  Host only. */
 int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
 
 /* One layer's attention over a mixed batch (Section 4.3: prefill and decode of one iteration
@@ -310,7 +313,7 @@ int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_
  * cus_prefill CUs) and joins back onto `stream`; work enqueued on `stream` before the call is complete before
  * either half starts, and work enqueued after it sees the whole output.  The result is
  * bit-identical for every split and every placement of the pages: all reduction orders depend
- * on logical token positions only.  Page ids read by a kernel outside [0, num_phys_pages) are
+ * on logical token positions and on the batch only.  Page ids read by a kernel outside [0, num_phys_pages) are
  * not dereferenced; they set an error word that duet_check_device_error() reports.  Invalid
  * arguments return DUET_EINVAL / DUET_EUNSUPPORTED / DUET_EWORKSPACE before anything is enqueued.
  * Calls on one context are serialised by the host (a mutex); the caller must not reuse a
@@ -335,7 +338,7 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
  * zero): calls that overlap on one device, from any context or thread, race.  Page ids outside
  * the pool are never dereferenced; the error word they set lives in the scratch and is not
  * reported. */
-#define DUET_NOALLOC_SCRATCH_BYTES (32u << 20)
+#define DUET_NOALLOC_SCRATCH_BYTES (64u << 20)
 int duet_attn_mixed_batch_noalloc(duet_ctx* ctx, const duet_shape* shape, const void* q, const void* k_cache,
                                   const void* v_cache, int64_t num_phys_pages, const int32_t* page_table,
                                   int32_t max_pages_per_req, const duet_batch* batch, duet_cu_split split, void* out,

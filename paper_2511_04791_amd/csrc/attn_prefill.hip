@@ -21,8 +21,16 @@
 // otherwise probabilities are taken against the stale max.  The result is the same softmax
 // (numerator and denominator share the reference), and the O rescale is skipped on most steps.
 // Key tiles past a wave's last query are skipped; only tiles crossing the diagonal are masked.
+//
+// A unit with a long key range may run as several pieces, each over a run of its key tiles
+// (kernels.h).  A piece keeps the same per-row state as a whole unit (reference max, denominator,
+// unnormalised O^T) and stores it; the last piece of the unit to finish combines the stored
+// states in piece order, m = max(m_a, m_b), O = 2^(m_a - m) O_a + 2^(m_b - m) O_b (likewise the
+// denominator), and writes the normalised rows.  Inside a piece a row may see no key at all
+// (its position lies before the piece's first key): its state stays (-inf, 0, 0).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "kernels.h"
@@ -91,7 +99,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   const int wave = uniform(tid >> 6);
   const int lane = tid & 63;
   const int hh = lane >> 5;
-  const int4 it = w.pitems[blockIdx.x];  // (req, first query head, q_row0, 0)
+  const int4 it = w.pitems[blockIdx.x];  // (req, first query head, q_row0, piece)
   const int r = it.x, h = it.y + wave / WPH, q_row0 = it.z;
   const int4 m = w.meta[r];
   const int q_start = m.y, q_len = m.z, c = m.w;
@@ -115,7 +123,15 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     }
   }
 
-  const int n_tiles = (c + min(q_row0 + QB - 1, q_len - 1)) / BN + 1;
+  // Key tiles [kt0, kt1) of the unit: all of them, or one piece's run.
+  const int unit_tiles = (c + min(q_row0 + QB - 1, q_len - 1)) / BN + 1;
+  const int piece = it.w & ((1 << kPrefillPieceBits) - 1);
+  const int split_unit = (it.w >> kPrefillPieceBits) - 1;  // -1: whole unit
+  // (first slot, pieces | tiles per piece << 16)
+  const int2 su = split_unit >= 0 ? w.psplit[split_unit] : make_int2(0, 1 | (unit_tiles << 16));
+  const int n_pieces = su.y & 0xffff, piece_tiles = su.y >> 16;
+  const int kt0 = piece * piece_tiles;
+  const int kt1 = min(unit_tiles, kt0 + piece_tiles);
   const int w_tiles = wrow0 < q_len ? (c + min(wrow0 + 31, q_len - 1)) / BN + 1 : 0;
   const int w_first_pos = c + wrow0;
 
@@ -125,10 +141,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   constexpr size_t kSlab = 16 * D * 2;  // bytes of one (page, kv head) slab, K or V
   int bad = 0;
 
-  // The unit's page ids go to LDS once, so a tile load never waits on a page-table read.
+  // The page ids of tiles kt0 .. kt1 - 1 go to LDS once (ids[i] = page 4 kt0 + i), so a tile
+  // load never waits on a page-table read.
   int* ids = reinterpret_cast<int*>(reinterpret_cast<char*>(lds) + PrefillSmem<D>::kTileBytes);
-  const int n_used_pages = min(n_pages, (n_tiles * BN + 15) >> 4);
-  for (int i = tid; i < n_used_pages; i += kThreads) ids[i] = prow[i];
+  const int id0 = (BN / 16) * kt0;
+  const int n_used_pages = min(n_pages, (kt1 * BN + 15) >> 4) - id0;
+  for (int i = tid; i < n_used_pages; i += kThreads) ids[i] = prow[id0 + i];
   __syncthreads();
 
   // Tiles arrive by direct global-to-LDS loads (16 bytes per lane; lane i of a wave writes bytes
@@ -160,7 +178,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       const int blk = wave + kWaves * i;
       int lp = 4 * kt + k_pi[i];
       bool in_range = lp < n_pages;
-      int id = in_range ? ids[min(lp, n_pages - 1)] : 0;  // the LDS read stays inside the table
+      int id = in_range ? ids[min(lp, n_pages - 1) - id0] : 0;  // the LDS read stays inside the table
       bool ok = in_range && page_ok(id, a.num_phys_pages);
       bad |= in_range & !ok;
       // A missing page reads page 0: its keys lie past the end (masked) or the request is
@@ -168,7 +186,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       load_lds16(kbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + k_off[i], kdst + blk * 512);
       lp = 4 * kt + v_pi[i];
       in_range = lp < n_pages;
-      id = in_range ? ids[min(lp, n_pages - 1)] : 0;
+      id = in_range ? ids[min(lp, n_pages - 1) - id0] : 0;
       ok = in_range && page_ok(id, a.num_phys_pages);
       bad |= in_range & !ok;
       load_lds16(vbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + v_off[i], vdst + blk * 512);
@@ -229,9 +247,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
 #pragma unroll
     for (int v = 0; v < 16; ++v) oacc[n][v] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
+  float m_sub = 0.f;  // m_ref where it is finite, else 0: a row with no key yet gets 2^-inf = 0
 
-  for (int t = 0; t < kStages - 1 && t < n_tiles; ++t) issue_tile(t);
-  publish(0, min(n_tiles - 1, kStages - 2));
+  for (int t = kt0; t < kt0 + kStages - 1 && t < kt1; ++t) issue_tile(t);
+  publish(kt0, min(kt1 - 1, kt0 + kStages - 2) - kt0);
   // The query fragments have landed before the loop (tile 0's wait above covers them in
   // hardware, but the compiler would otherwise keep them pending at the loop head and make every
   // step's first MFMA wait for all tile loads in flight, collapsing the ring to one tile).
@@ -262,7 +281,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
         sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[nb][kk], qf[kk], sacc[nb], 0, 0, 0);
   };
 
-  for (int kt = 0; kt < n_tiles; ++kt) {
+  for (int kt = kt0; kt < kt1; ++kt) {
     if (kt < w_tiles) {
       f32x16 sacc[2];
       scores(kt, sacc);
@@ -299,8 +318,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       // Move the reference max only when some score exceeds it by more than the slack.
       if (__any(mx > m_ref + kRescaleSlack)) {
         const float m_new = fmaxf(m_ref, mx);
-        const float alpha = fast_exp2(m_ref - m_new);
+        const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_ref - m_new);
         m_ref = m_new;
+        m_sub = m_new == -INFINITY ? 0.f : m_new;
         l_run *= alpha;
 #pragma unroll
         for (int n = 0; n < NO; ++n) oacc[n] *= alpha;
@@ -310,7 +330,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          pb[2 * nb + (v >> 3)][v & 7] = static_cast<__bf16>(fast_exp2(__builtin_fmaf(sacc[nb][v], a.scale_log2, -m_ref)));
+          pb[2 * nb + (v >> 3)][v & 7] = static_cast<__bf16>(fast_exp2(__builtin_fmaf(sacc[nb][v], a.scale_log2, -m_sub)));
       // The denominator sums the bf16 probabilities the PV product consumes.
       const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 #pragma unroll
@@ -326,15 +346,97 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
         for (int k2 = 0; k2 < 4; ++k2)
           oacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[n][k2], pb[k2], oacc[n], 0, 0, 0);
     }
-    if (kt + 1 < n_tiles) {
+    if (kt + 1 < kt1) {
       // Stage (kt + kStages - 1) % kStages was last read in step kt - 1, which every wave has
       // left (the barrier that published tile kt); tiles kt + 2 .. stay in flight.
-      if (kt + kStages - 1 < n_tiles) issue_tile(kt + kStages - 1);
-      publish(kt + 1, min(n_tiles - 1, kt + kStages - 1) - (kt + 1));
+      if (kt + kStages - 1 < kt1) issue_tile(kt + kStages - 1);
+      publish(kt + 1, min(kt1 - 1, kt + kStages - 1) - (kt + 1));
     }
   }
 
   if (bad) atomicOr(w.err, 1);
+  if (split_unit >= 0) {
+    // Slot layout, in float pairs: O as [wave][n][v / 2][lane], then (m, l) as [wave][lane]; every
+    // lane stores and later loads exactly its own registers.  The slots are written and read with
+    // relaxed device-scope atomic accesses (coherent across the XCDs' L2 caches without the
+    // whole-cache write-back and invalidation a device-scope fence costs every workgroup on the
+    // XCD); a piece counts itself only once its stores have completed.
+    constexpr size_t kSlotPairs = (size_t)kThreads * (D / 4 + 1);
+    typedef unsigned long long u64;
+    auto o_at = [&](int slot) {
+      return reinterpret_cast<u64*>(w.ppart) + (size_t)slot * kSlotPairs + (size_t)wave * NO * 8 * 64 + lane;
+    };
+    auto ml_at = [&](int slot) {
+      return reinterpret_cast<u64*>(w.ppart) + (size_t)slot * kSlotPairs + (size_t)kThreads * (D / 4) +
+             (size_t)wave * 64 + lane;
+    };
+    auto pack = [](float x, float y) {
+      return (u64)__float_as_uint(x) | ((u64)__float_as_uint(y) << 32);
+    };
+    auto lo = [](u64 v) { return __uint_as_float((unsigned)v); };
+    auto hi = [](u64 v) { return __uint_as_float((unsigned)(v >> 32)); };
+    {
+      u64* o = o_at(su.x + piece);
+#pragma unroll
+      for (int n = 0; n < NO; ++n)
+#pragma unroll
+        for (int v2 = 0; v2 < 8; ++v2)
+          __hip_atomic_store(o + (n * 8 + v2) * 64, pack(oacc[n][2 * v2], oacc[n][2 * v2 + 1]), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ml_at(su.x + piece), pack(m_ref, l_run), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's slot stores have completed
+    __syncthreads();
+    // The arrival flag reuses the page-id table's first word: no id is read after the key loop.
+    if (tid == 0) {
+      const int done = atomicAdd(w.pcount + split_unit, 1) + 1;
+      ids[0] = done == n_pieces;
+      if (done == n_pieces) atomicExch(w.pcount + split_unit, 0);  // ready for the next launch
+    }
+    __syncthreads();
+    if (!ids[0]) return;
+    // The last piece: combine the states in piece order (its own from registers, the others from
+    // their slots), so the result does not depend on which piece finished last.
+    f32x16 own[NO];
+#pragma unroll
+    for (int n = 0; n < NO; ++n) own[n] = oacc[n];
+    const u64 own_ml = pack(m_ref, l_run);
+    for (int pc = 0; pc < n_pieces; ++pc) {
+      f32x16 op[NO];
+      u64 ml;
+      if (pc == piece) {
+        ml = own_ml;
+#pragma unroll
+        for (int n = 0; n < NO; ++n) op[n] = own[n];
+      } else {
+        const u64* o = o_at(su.x + pc);
+        ml = __hip_atomic_load(ml_at(su.x + pc), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int n = 0; n < NO; ++n)
+#pragma unroll
+          for (int v2 = 0; v2 < 8; ++v2) {
+            const u64 v = __hip_atomic_load(o + (n * 8 + v2) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            op[n][2 * v2] = lo(v);
+            op[n][2 * v2 + 1] = hi(v);
+          }
+      }
+      if (pc == 0) {
+        m_ref = lo(ml);
+        l_run = hi(ml);
+#pragma unroll
+        for (int n = 0; n < NO; ++n) oacc[n] = op[n];
+      } else {
+        const float m_b = lo(ml);
+        const float m_new = fmaxf(m_ref, m_b);
+        const float fa = m_new == -INFINITY ? 1.f : fast_exp2(m_ref - m_new);
+        const float fb = m_new == -INFINITY ? 0.f : fast_exp2(m_b - m_new);
+        m_ref = m_new;
+        l_run = l_run * fa + hi(ml) * fb;
+#pragma unroll
+        for (int n = 0; n < NO; ++n) oacc[n] = oacc[n] * fa + op[n] * fb;
+      }
+    }
+  }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (row_ok) {
     const float inv = 1.0f / l_tot;
@@ -442,6 +544,13 @@ int prefill_heads_per_unit(int group) {
 int prefill_rows_per_unit(int group, int dtype) {
   return dtype == 0 ? 32 * kWaves / prefill_heads_per_unit(group) : kPrefillRows;
 }
+
+int prefill_piece_tiles_for(long long total_tiles) {
+  const long long even = (total_tiles + kPrefillPieceFill - 1) / kPrefillPieceFill;
+  return (int)std::max<long long>(kPrefillPieceMinTiles, even);
+}
+
+size_t prefill_slot_bytes(int head_dim) { return (size_t)kThreads * (head_dim / 2 + 2) * sizeof(float); }
 
 hipError_t launch_prefill(const AttnArgs& a, const WorkArgs& w, hipStream_t s) {
   if (w.n_pitems == 0) return hipSuccess;

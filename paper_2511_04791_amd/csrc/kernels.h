@@ -42,6 +42,12 @@ struct WorkArgs {
   int32_t pages_per_split;
   int32_t decode_cus;   // CUs the decode stream may use (sizes the persistent grid)
   int32_t prefill_id_cap;  // most pages of any prefill request (sizes the LDS page-id table)
+  // Prefill key split (bf16, see kPrefillPieceFill): a piece item carries
+  // ((split unit + 1) << kPrefillPieceBits) | piece in its w field (0: a whole unit).
+  float* ppart;               // [slots] partial state of every piece: unnormalised O, running max, denominator
+  const int2* psplit;         // [split units] (first slot, pieces | key tiles per piece << 16)
+  int32_t* pcount;            // [split units] pieces finished; zero before and after every launch
+  int32_t prefill_piece_tiles;  // P of the rule below (0: no unit is split)
 };
 
 // One decode step's cache write (look-ahead decode): new key and value rows in, paged cache out.
@@ -85,6 +91,23 @@ constexpr int kPrefillKeys = 64;   // keys per LDS stage (4 pages)
 // prefill_rows_per_unit(group, dtype) queries.  fp32 items are one head times kPrefillRows.
 int prefill_heads_per_unit(int group);
 int prefill_rows_per_unit(int group, int dtype);
+
+// Prefill key split (bf16).  Let T be the batch's total key tiles (kPrefillKeys keys) over all
+// units and P = max(kPrefillPieceMinTiles, ceil(T / kPrefillPieceFill)), an even share of the
+// batch over one workgroup per CU of the whole chip.  A unit whose causal key range spans more
+// than 1.5 P tiles runs as n = ceil(tiles / P) pieces of ceil(tiles / n) consecutive tiles (the
+// last may be shorter; n is recounted so that none is empty), so a short chunk after a long
+// cached prefix (few units, each long) still fills the CUs.  Every piece pays a fixed start-up
+// cost and a partial-state round trip, so units within 1.5 P of the share stay whole.  P depends
+// on the batch only, never on the CU split, so results are the same for every split.  Each piece
+// writes its partial state to a slot; the piece that finishes last (an arrival counter per unit)
+// merges the slots in piece order and writes the output.  Split units number at most
+// T / P <= kPrefillPieceFill and their slots at most 2 T / P.
+constexpr int kPrefillPieceMinTiles = 8;
+constexpr int kPrefillPieceFill = 256;
+constexpr int kPrefillPieceBits = 12;  // piece index field of an item's w (pieces <= 4095)
+int prefill_piece_tiles_for(long long total_tiles);
+size_t prefill_slot_bytes(int head_dim);  // one piece's partial state
 
 // The QKV-split step of a block (bf16): query rows out, new keys and values into the cache.
 struct QkvSplitArgs {

@@ -46,7 +46,7 @@ constexpr size_t kMaxGraphs = 128;    // cached decode-step graphs per context
 // Each device the library runs on holds its own copy until the process ends.  In host code the
 // array's name is not a device address: its address on a device comes from hipGetSymbolAddress
 // (duet_init, with the device current) and is kept in the context.
-constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr size_t kScratchBytes = size_t(64) << 20;
 // Pinned staging allocated up front for each slot, so that the no-allocation path never grows it.
 constexpr size_t kStagingPrealloc = size_t(1) << 20;
 
@@ -80,11 +80,14 @@ struct StepPlan {
 // Work lists of one iteration and where they live in the caller's workspace.
 struct Plan {
   std::vector<int4> meta, pitems, dreq;
+  std::vector<int2> psplit;  // per split prefill unit: (first partial slot, pieces | tiles per piece << 16)
   std::vector<int4> ditems;
   std::vector<StepPlan> ahead;  // look-ahead decode steps 1 .. steps - 1
   int steps = 1;
   int n_items_decode = 0, max_split = 0, pages_per_split = 0, group = 0, prefill_id_cap = 0;
-  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, upload_bytes = 0, total = 0;
+  int prefill_piece_tiles = 0, n_split_units = 0, n_slots = 0;
+  size_t off_meta = 0, off_pitems = 0, off_dreq = 0, off_ditems = 0, off_psplit = 0, off_pcount = 0, off_ppart = 0,
+         upload_bytes = 0, total = 0;
   // Two buffers of split-K partials: consecutive layers of a call alternate between them, so a
   // layer's partials survive until the next layer's decode kernel has merged them.
   size_t off_pacc[2] = {0, 0}, off_pml[2] = {0, 0};
@@ -160,7 +163,26 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   p->meta.clear();
   p->pitems.clear();
   p->steps = steps;
+  p->psplit.clear();
+  const bool bf16 = s->dtype == DUET_BF16;
+  // bf16: a unit is nh heads of one group x rows queries; fp32: one head x rows queries.
+  const int nh = bf16 ? prefill_heads_per_unit(g) : 1;
+  const int rows = prefill_rows_per_unit(g, bf16 ? 0 : 1);
+  const int units = s->num_q_heads / nh;
+  // Key tiles of row block t of a request (the causal range of its last row).
+  auto block_tiles = [&](const duet_seq_meta& q, int t) {
+    return (int)(((int64_t)q.cached_len + std::min(q.q_len, (t + 1) * rows) - 1) / kPrefillKeys + 1);
+  };
+  int64_t total_tiles = 0;
+  for (int r = 0; r < b->num_reqs; ++r) {
+    const duet_seq_meta& q = b->reqs[r];
+    if (q.kind != DUET_KIND_PREFILL) continue;
+    for (int t = 0; t * rows < q.q_len; ++t) total_tiles += (int64_t)block_tiles(q, t) * units;
+  }
+  const int P = bf16 && total_tiles > 0 ? prefill_piece_tiles_for(total_tiles) : 0;
+  p->prefill_piece_tiles = P;
   int64_t n_pitems = 0;
+  int n_su = 0, n_slots = 0;
   struct Tile {
     int64_t keys;
     int4 item;
@@ -170,29 +192,38 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
     const duet_seq_meta& q = b->reqs[r];
     if (fill) p->meta.push_back(make_int4(q.kind, q.q_start, q.q_len, q.cached_len));
     const int64_t L = (int64_t)q.cached_len + q.q_len;
-    if (q.kind == DUET_KIND_PREFILL) {
-      p->prefill_id_cap = std::max(p->prefill_id_cap, (int)((L + 15) / 16));
-      // bf16: a unit is nh heads of one group x rows queries; fp32: one head x rows queries.
-      const int nh = s->dtype == DUET_BF16 ? prefill_heads_per_unit(g) : 1;
-      const int rows = prefill_rows_per_unit(g, s->dtype == DUET_BF16 ? 0 : 1);
-      const int n_tiles = (q.q_len + rows - 1) / rows;
-      const int units = s->num_q_heads / nh;
-      n_pitems += (int64_t)n_tiles * units;
-      if (fill) {
-        for (int t = 0; t < n_tiles; ++t) {
-          const int64_t keys = q.cached_len + std::min(q.q_len, (t + 1) * rows);
-          // Units ordered so that workgroup index mod 8 follows the kv head: the units sharing
-          // one kv head land on one XCD and share its L2.
-          for (int u = 0; u < units; ++u) {
-            int h;
-            if (nh == 1) h = (u % s->num_kv_heads) * g + u / s->num_kv_heads;
-            else h = u * nh;
-            tiles.push_back({keys, make_int4(r, h, t * rows, 0)});
-          }
+    if (q.kind != DUET_KIND_PREFILL) continue;
+    p->prefill_id_cap = std::max(p->prefill_id_cap, (int)((L + 15) / 16));
+    for (int t = 0; t * rows < q.q_len; ++t) {
+      const int nt = block_tiles(q, t);
+      // Units longer than 1.5 P: n pieces of equal length (the last may be shorter), none empty
+      int pieces = P > 0 && 2 * nt > 3 * P ? (nt + P - 1) / P : 1;
+      const int len = (nt + pieces - 1) / pieces;
+      pieces = (nt + len - 1) / len;
+      n_pitems += (int64_t)pieces * units;
+      if (pieces > 1) {
+        if (fill)
+          for (int u = 0; u < units; ++u) p->psplit.push_back(make_int2(n_slots + u * pieces, pieces | (len << 16)));
+        n_su += units;
+        n_slots += units * pieces;
+      }
+      if (!fill) continue;
+      // Units ordered so that workgroup index mod 8 follows the kv head: the units sharing one kv
+      // head land on one XCD and share its L2.  Piece pc of every unit of a block, then piece
+      // pc + 1: pieces of equal length stay together through the sort below.
+      for (int pc = 0; pc < pieces; ++pc) {
+        const int64_t keys = pieces > 1 ? (int64_t)std::min(len, nt - pc * len) * kPrefillKeys
+                                        : q.cached_len + std::min(q.q_len, (t + 1) * rows);
+        for (int u = 0; u < units; ++u) {
+          const int h = nh == 1 ? (u % s->num_kv_heads) * g + u / s->num_kv_heads : u * nh;
+          const int su = pieces > 1 ? n_su - units + u : -1;
+          tiles.push_back({keys, make_int4(r, h, t * rows, ((su + 1) << kPrefillPieceBits) | (pieces > 1 ? pc : 0))});
         }
       }
     }
   }
+  p->n_split_units = n_su;
+  p->n_slots = n_slots;
   if (fill) {
     std::stable_sort(tiles.begin(), tiles.end(), [](const Tile& x, const Tile& y) { return x.keys > y.keys; });
     p->pitems.reserve(tiles.size());
@@ -212,6 +243,10 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   off = align_up(off + (size_t)n_dreq * sizeof(int4));
   p->off_ditems = off;
   off = align_up(off + (s->dtype == DUET_BF16 ? (size_t)n_items * sizeof(int4) : 0));
+  p->off_psplit = off;
+  off = align_up(off + (size_t)n_su * sizeof(int2));
+  p->off_pcount = off;  // zeroed by the upload
+  off = align_up(off + (size_t)n_su * sizeof(int32_t));
   // Look-ahead steps: each has its own metadata and decode lists; the split-K partials are
   // shared, since the steps run one after another on one stream.
   int64_t max_items = n_items;
@@ -245,6 +280,8 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
     p->off_pml[b] = off;
     off = align_up(off + (size_t)max_items * g * 2 * sizeof(float));
   }
+  p->off_ppart = off;
+  off = align_up(off + (size_t)n_slots * prefill_slot_bytes(s->head_dim));
   p->total = off;
 }
 
@@ -301,6 +338,7 @@ void append_key(std::vector<uint64_t>* k, const DecodeLaunch& l) {
                         bits(w.work_counter), bits(w.clear_counter), bits(w.merge_pacc), bits(w.merge_pml),
                         bits(w.merge_out), bits(w.n_merge), bits(w.n_pitems), bits(w.n_dreq), bits(w.max_split),
                         bits(w.n_ditems), bits(w.pages_per_split), bits(w.decode_cus), bits(w.prefill_id_cap),
+                        bits(w.ppart), bits(w.psplit), bits(w.pcount), bits(w.prefill_piece_tiles),
                         bits(p.k_cache), bits(p.v_cache), bits(p.k_new), bits(p.v_new), bits(p.page_table),
                         bits(p.num_phys_pages), bits(p.max_pages), bits(p.h_kv), bits(p.head_dim), bits(p.dtype)};
   k->insert(k->end(), std::begin(f), std::end(f));
@@ -437,6 +475,8 @@ int stage_upload(duet_ctx* ctx, const Plan& p, char* ws, hipStream_t st, bool ma
   std::memcpy(h + p.off_pitems, p.pitems.data(), p.pitems.size() * sizeof(int4));
   std::memcpy(h + p.off_dreq, p.dreq.data(), p.dreq.size() * sizeof(int4));
   std::memcpy(h + p.off_ditems, p.ditems.data(), p.ditems.size() * sizeof(int4));
+  std::memcpy(h + p.off_psplit, p.psplit.data(), p.psplit.size() * sizeof(int2));
+  std::memset(h + p.off_pcount, 0, (size_t)p.n_split_units * sizeof(int32_t));
   for (const StepPlan& sp : p.ahead) {
     std::memcpy(h + sp.off_meta, sp.meta.data(), sp.meta.size() * sizeof(int4));
     std::memcpy(h + sp.off_dreq, sp.dreq.data(), sp.dreq.size() * sizeof(int4));
@@ -543,6 +583,10 @@ void base_args(const duet_ctx* ctx, const duet_shape* shape, const Plan& p, char
   w->max_split = p.max_split;
   w->pages_per_split = p.pages_per_split;
   w->prefill_id_cap = p.prefill_id_cap;
+  w->ppart = reinterpret_cast<float*>(ws + p.off_ppart);
+  w->psplit = reinterpret_cast<const int2*>(ws + p.off_psplit);
+  w->pcount = reinterpret_cast<int32_t*>(ws + p.off_pcount);
+  w->prefill_piece_tiles = p.prefill_piece_tiles;
 }
 
 // A masked stream the context already holds (no creation): the no-allocation path's lookup.
