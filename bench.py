@@ -7,12 +7,13 @@ then the attention of one iteration (work lists built and uploaded once, the dec
 reduce kernels and the prefill MFMA kernel of every layer on their CU-masked streams, the fork
 and the join; with look-ahead, the decode steps replayed from graphs on the decode CUs):
 
-  cfg4 (headline)  Llama-3-70B attention shapes (64 q-heads / 8 kv-heads / head_dim 128), one
-                   layer: an 8192-token chunk after 24576 cached tokens plus 32 decodes at 2048;
-  cfg3             Llama-3-8B shapes, one layer: 256 decodes with lognormal contexts (median
-                   8192) plus a 512-token chunk after 16384 cached, in a ~70 GB page pool;
-  cfg2             Llama-3-8B shapes, 32 layers: a 2048-token chunk plus 64 decodes with
-                   contexts U[512, 4096].
+  prefill-heavy-70b (headline)  Llama-3-70B attention shapes (64 q-heads / 8 kv-heads /
+      head_dim 128), one layer: an 8192-token chunk after 24576 cached tokens plus 32 decodes at
+      2048;
+  decode-heavy  Llama-3-8B shapes, one layer: 256 decodes with lognormal contexts (median 8192)
+      plus a 512-token chunk after 16384 cached, in a ~70 GB page pool;
+  llama8b-mixed  Llama-3-8B shapes, 32 layers: a 2048-token chunk plus 64 decodes with contexts
+      U[512, 4096].
 
 Each workload's TBT bound is the paper's 50 ms per decode step of the whole model, scaled to the
 layers benchmarked (Llama-3-70B has 80 layers, Llama-3-8B 32).  Algorithm 1 runs on a model
@@ -193,9 +194,9 @@ WORKLOADS = {
 SLO_US = 50000.0  # the paper's TBT bound: 50 ms per decode step of the whole model
 # key -> workload, benchmarked layers, layers of the whole model, most decode steps per call
 CONFIGS = {
-    "cfg4": {"workload": "prefill-heavy-70b", "layers": 1, "model_layers": 80, "k_cap": 64},
-    "cfg3": {"workload": "decode-heavy", "layers": 1, "model_layers": 32, "k_cap": 1},
-    "cfg2": {"workload": "llama8b-mixed", "layers": 32, "model_layers": 32, "k_cap": 1},
+    "prefill-heavy-70b": {"workload": "prefill-heavy-70b", "layers": 1, "model_layers": 80, "k_cap": 64},
+    "decode-heavy": {"workload": "decode-heavy", "layers": 1, "model_layers": 32, "k_cap": 1},
+    "llama8b-mixed": {"workload": "llama8b-mixed", "layers": 32, "model_layers": 32, "k_cap": 1},
 }
 
 
@@ -974,13 +975,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--configs", default="cfg4,cfg3,cfg2",
-                    help="workloads of the default run: cfg4 (Llama-3-70B prefill-heavy), cfg3 (decode-heavy, ~70 GB "
-                         "pool), cfg2 (Llama-3-8B mixed, 32 layers)")
-    ap.add_argument("--headline", default="cfg4", choices=list(CONFIGS), help="the workload `value` reports")
+    ap.add_argument("--configs", default="prefill-heavy-70b,decode-heavy,llama8b-mixed",
+                    help="workloads of the default run: prefill-heavy-70b (Llama-3-70B), decode-heavy (~70 GB pool), "
+                         "llama8b-mixed (Llama-3-8B, 32 layers)")
+    ap.add_argument("--headline", default="prefill-heavy-70b", choices=list(CONFIGS),
+                    help="the workload `value` reports")
     ap.add_argument("--layers", type=int, default=None, help="layers per iteration of the --trace/--serve/--block modes")
     ap.add_argument("--tbt-slo-us", type=float, default=None, help="TBT bound of the --lookahead and --block modes")
-    ap.add_argument("--split", default="", help="Sp,Sd: the one split of --block")
+    ap.add_argument("--split", default="", help="Sp,Sd: the one split of --block; with --counters also 'agg'")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibrate", action="store_true")
     ap.add_argument("--model", default="", help="load a calibrated latency model (duet_model_save file) instead of "
@@ -1032,10 +1034,10 @@ def main():
 
 
 def counters_main(args):
-    """A short fixed pass for profilers: --steps calls of --headline's workload under Algorithm 1's
-    split at one decode step (the configuration of the benchmark's per-kernel roofline figures),
-    then a plain 1 GiB elementwise device copy whose FETCH_SIZE / WRITE_SIZE readings scale the
-    counters to bytes.  Load the benchmark's calibration with --model to get its split."""
+    """A short fixed pass for profilers: --steps calls of --headline's workload at one decode step
+    under --split ("agg" or "S_p,S_d", the split the benchmark's line reports for that workload; by
+    default Algorithm 1's choice under the --model latency model), then a plain 1 GiB elementwise
+    device copy whose FETCH_SIZE / WRITE_SIZE readings scale the counters to bytes."""
     import dataclasses
     import torch
     import paper_2511_04791_amd as duet
@@ -1048,9 +1050,16 @@ def counters_main(args):
     ctx = duet.Context(0)
     if args.model:
         ctx.model.load(args.model)
-    chosen = duet.choose_cu_split(rows3, SLO_US * L / spec["model_layers"], shape, ctx.model,
-                                  max_decode_steps=spec["k_cap"])[0]
-    split = duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT else duet.CuSplit.agg()
+    if args.split == "agg":
+        split = duet.CuSplit.agg()
+    elif args.split:
+        sp_, sd_ = (int(x) for x in args.split.split(","))
+        split = duet.CuSplit.split(sp_, sd_)
+    else:
+        chosen = duet.choose_cu_split(rows3, SLO_US * L / spec["model_layers"], shape, ctx.model,
+                                      max_decode_steps=spec["k_cap"])[0]
+        split = (duet.CuSplit.split(chosen.cus_prefill, chosen.cus_decode) if chosen.mode == duet.SPLIT
+                 else duet.CuSplit.agg())
     layers = [wl.make_tensors(batch, seed=2002 + l, device="cuda") for l in range(L)]
     qs, kcs, vcs = [x[0] for x in layers], [x[1] for x in layers], [x[2] for x in layers]
     pt = torch.as_tensor(batch.page_table, device="cuda")
