@@ -77,9 +77,15 @@ def source_hash(name: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def split_tag(split) -> str:
+    """Name of a CU split in profile file names: 'agg' or 'S_p-S_d'."""
+    from paper_2511_04791_amd import SPLIT
+    return f"{split.cus_prefill}-{split.cus_decode}" if split.mode == SPLIT else "agg"
+
+
 def committed_traffic(kernel: str, source: str, tag: str):
-    """HBM bytes per launch from the committed counter summary of `kernel` on workload `tag`, if
-    the kernel source still matches the one the counters were taken on; else None."""
+    """HBM bytes per launch from the committed counter summary of `kernel` on `tag` (workload and
+    CU split), if the kernel source still matches the one the counters were taken on; else None."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{tag}_traffic.json")
     try:
         with open(path) as f:
@@ -337,15 +343,17 @@ def run_config(ctx, key, args, calib):
     dec_split = _roof(dbytes / kern_split["decode_partial_us"] / 1e3, PEAK_HBM_GBPS, sd_cus, "GB/s", "decode_partial_bf16",
                       int(dbytes), kern_split["decode_partial_us"],
                       probe("probe_read_tbps", sd_cus) and probe("probe_read_tbps", sd_cus) * 1e3,
-                      committed_traffic("decode_partial", "attn_decode.hip", key), "hbm")
+                      committed_traffic("decode_partial", "attn_decode.hip", f"{key}_{split_tag(chosen)}"), "hbm")
     dec_agg = _roof(dbytes / kern_agg["decode_partial_us"] / 1e3, PEAK_HBM_GBPS, 256, "GB/s", "decode_partial_bf16",
                     int(dbytes), kern_agg["decode_partial_us"], probe("probe_read_tbps", 256) and
-                    probe("probe_read_tbps", 256) * 1e3, None, "hbm")
+                    probe("probe_read_tbps", 256) * 1e3, committed_traffic("decode_partial", "attn_decode.hip",
+                                                                           f"{key}_agg"), "hbm")
     pre_split = _roof(pflops / kern_split["prefill_us"] / 1e6, PEAK_BF16_TFLOPS, sp_cus, "TFLOP/s", "prefill_bf16",
                       pflops, kern_split["prefill_us"], probe("probe_mfma_tflops", sp_cus),
-                      committed_traffic("prefill", "attn_prefill.hip", key), "mfma")
+                      committed_traffic("prefill", "attn_prefill.hip", f"{key}_{split_tag(chosen)}"), "mfma")
     pre_agg = _roof(pflops / kern_agg["prefill_us"] / 1e6, PEAK_BF16_TFLOPS, 256, "TFLOP/s", "prefill_bf16", pflops,
-                    kern_agg["prefill_us"], probe("probe_mfma_tflops", 256), None, "mfma")
+                    kern_agg["prefill_us"], probe("probe_mfma_tflops", 256),
+                    committed_traffic("prefill", "attn_prefill.hip", f"{key}_agg"), "mfma")
     decode_dominant = kern_split["decode_partial_us"] * 1 >= kern_split["prefill_us"]
 
     # timed region, last: W warm-up steps, then K back-to-back steps, for the chosen split and for
