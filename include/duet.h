@@ -332,8 +332,8 @@ int duet_attn_mixed_batch(duet_ctx* ctx, const duet_shape* shape, const void* q,
  * DUET_EWORKSPACE, as do work lists beyond the 1 MiB of pinned staging duet_init preallocates.
  * Under DUET_SPLIT or DUET_CONCURRENT the CU-masked streams must already exist: one earlier call
  * of duet_attn_mixed_batch or duet_attn_iteration with the same split creates them (the context
- * keeps its six most recently used); otherwise DUET_EINVAL.  Profiling is ignored.  The output is
- * bit-identical to duet_attn_mixed_batch's.  Every call on a device shares that device's array,
+ * keeps the streams of its most recently used split or mode); otherwise DUET_EINVAL.  Profiling
+ * is ignored.  The output is bit-identical to duet_attn_mixed_batch's.  Every call on a device shares that device's array,
  * which keeps the last call's contents (each call's upload clears the parts that must start at
  * zero): calls that overlap on one device, from any context or thread, race.  Page ids outside
  * the pool are never dereferenced; the error word they set lives in the scratch and is not

@@ -33,7 +33,12 @@ namespace {
 using namespace duet;
 
 constexpr int kStagingSlots = 4;
-constexpr size_t kMaxMaskedStreams = 6;  // each CU-masked stream owns a hardware queue
+// Each CU-masked stream owns a hardware queue.  Only the current split's pair is kept: with more
+// masked queues alive, the decode half of a pair created second in a process ran 20-30% slower
+// and its reduce kernel 4-5x slower beside a running prefill (same CUs reached, measured with the
+// placement probe), while a pair that reuses the freed queues runs at full speed.  Changing the
+// split then recreates two streams, which a serving loop does only when Algorithm 1 switches.
+constexpr size_t kMaxMaskedStreams = 2;
 constexpr size_t kAlign = 256;
 // Workspace head: the device error word at offset 0 and the decode queue counters from
 // kCounterOffset on; the head is zeroed by every call's upload.
