@@ -749,7 +749,7 @@ def serve_main(args):
     from paper_2511_04791_amd.calibration import calibrate_model
 
     L = args.layers if args.layers is not None else 32
-    ffn, budget, max_pages, pool, tbt = 14336, 8192, 4096, 20000, 50000.0
+    ffn, budget, max_pages, pool, tbt = 14336, 8192, 4096, 60000, 50000.0
     sh = dataclasses.replace(wl.LLAMA3_8B, num_layers=L)
     block = duet.BlockShape(ffn, 0, duet.BLOCK_GQA_QKV | duet.BLOCK_FUSED_GATE_UP)
     ctx = duet.Context(0)
