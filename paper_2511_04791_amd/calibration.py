@@ -50,6 +50,7 @@ CAL_PREFILL = (8192, 8192)        # (q_len, cached_len) of the calibration chunk
 CAL_DECODE_SMALL = (48, (256, 2048))    # decodes, context range: the fixed-latency point
 CAL_DECODE_LARGE = (96, (1024, 8192))   # the throughput point
 LOOKAHEAD_K = (2, 10)             # decode steps of the two look-ahead calls a step time is taken from
+SHARED_K_CAP = 48                 # most look-ahead steps of a sharing measurement
 
 
 def calibration_batches(shape, seed: int = 4242, reserve_tokens: int = 0):
@@ -66,7 +67,8 @@ def calibration_batches(shape, seed: int = 4242, reserve_tokens: int = 0):
                           reserve_tokens=reserve_tokens)
     large = wl.make_batch(shape, large_rows, page_seed=seed + 2, name="calibration-decode-large",
                           reserve_tokens=reserve_tokens)
-    mixed = wl.make_batch(shape, pre_rows + large_rows, page_seed=seed + 3, name="calibration-mixed")
+    mixed = wl.make_batch(shape, pre_rows + large_rows, page_seed=seed + 3, name="calibration-mixed",
+                          reserve_tokens=max(reserve_tokens, SHARED_K_CAP))
     return pre, small, large, mixed
 
 
@@ -98,6 +100,33 @@ def _times(ctx, batch, layers, pt, split, reps, warmup=1):
             res.append({"prefill": kt["prefill_total_us"] / kt["layers"], "decode": kt["decode_total_us"] / kt["layers"]})
     ctx.set_profiling(0)
     return res
+
+
+def _shared_lookahead(ctx, batch, layers, pt, sp, k, reps):
+    """Per-layer prefill span and decode step (microseconds) of look-ahead calls of a mixed batch on
+    the split sp / (256 - sp) with k decode steps: the decode partition steps for the whole
+    prefill, as it does under Algorithm 1's own k.  Medians over `reps` calls."""
+    import torch
+    import paper_2511_04791_amd as duet
+    qs, kcs, vcs, la = layers
+    L = len(qs)
+    meta = batch.seq_meta
+    split = duet.CuSplit.split(sp, N.TOTAL_CUS - sp, k)
+    qa = [la[l][0][s_ - 1] for s_ in range(1, k) for l in range(L)]
+    ka = [la[l][1][s_ - 1] for s_ in range(1, k) for l in range(L)]
+    va = [la[l][2][s_ - 1] for s_ in range(1, k) for l in range(L)]
+    oa = [torch.empty_like(x) for x in qa]
+    ws = ctx.workspace(duet.lookahead_workspace_bytes(duet.shape_of(qs[0], kcs[0], L), meta, k))
+    ctx.set_profiling(2)
+    pre, dec = [], []
+    for i in range(reps + 1):
+        ctx.attn_lookahead(qs, qa, ka, va, kcs, vcs, pt, meta, split, workspace=ws, outs_ahead=oa)
+        if i:
+            kt = ctx.last_kernel_times()
+            pre.append(kt["prefill_total_us"] / L)
+            dec.append(kt["decode_step_us"] / L)
+    ctx.set_profiling(0)
+    return statistics.median(pre), statistics.median(dec)
 
 
 def _step_us(ctx, batch, layers, pt, share, reps):
@@ -181,26 +210,30 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, shared_l
     model.set_launch_tables([0.0] * len(TABLE_SHARES), fill_launch(t0_grid))
     model.set_efficiency(1.0, 1.0)
 
-    # 3. both halves at once, on every split of the grid
+    # 3. both halves at once, on every split of the grid, with the decode partition stepping for the
+    # whole prefill (k = the standalone prefill time over the standalone decode step)
     lay = [wl.make_tensors(mixed, seed=seed + 100 + l, device="cuda") for l in range(shared_layers)]
+    la = [wl.make_lookahead_tensors(mixed, SHARED_K_CAP, seed=seed + 120 + l, device="cuda") for l in range(shared_layers)]
     pt = torch.as_tensor(mixed.page_table, device="cuda")
+    parts = ([x[0] for x in lay], [x[1] for x in lay], [x[2] for x in lay], la)
     f_mix, _ = batch_work(mixed.seq_meta, sh, wl.KIND_PREFILL)
     _, b_mix = batch_work(mixed.seq_meta, sh, wl.KIND_DECODE)
     fl_sh, by_sh = dict(fl_grid), dict(by_grid)   # share 256 never runs split: keep standalone
-    t_pre_sh, t_dec_sh = {}, {}
+    t_pre_sh, t_dec_sh, k_sh = {}, {}, {}
     for sp in GRID_SHARES[:-1]:
         sd = N.TOTAL_CUS - sp
-        rows = _times(ctx, mixed, lay, pt, CuSplit.split(sp, sd), reps)
-        t_pre_sh[sp] = statistics.median(r["prefill"] for r in rows)
-        t_dec_sh[sd] = statistics.median(r["decode"] for r in rows)
+        t_p = t_pre[sp] * f_mix / f_pre  # the mixed batch's chunk, standalone, per layer (us)
+        k_sh[sp] = max(1, min(SHARED_K_CAP, int(t_p * 1e-6 / step["large"][sd])))
+        t_pre_sh[sp], t_dec_sh[sd] = _shared_lookahead(ctx, mixed, parts, pt, sp, k_sh[sp], reps)
         fl_sh[sp] = f_mix / (t_pre_sh[sp] * 1e-6)
         # the fixed term is priced separately; the shared rate covers the rest
         by_sh[sd] = b_mix / max(t_dec_sh[sd] * 1e-6 - t0_grid[sd], 0.5 * t_dec_sh[sd] * 1e-6)
-    del lay
+    del lay, la, parts
     model.set_sharing_tables(fill_table(fl_sh), fill_table(by_sh))
     return {"layers": layers, "shared_layers": shared_layers, "grid_shares": list(GRID_SHARES),
             "shared_prefill_us": [round(t_pre_sh.get(s_, 0.0), 1) for s_ in GRID_SHARES],
             "shared_decode_us": [round(t_dec_sh.get(s_, 0.0), 1) for s_ in GRID_SHARES],
+            "shared_k": [k_sh.get(s_, 0) for s_ in GRID_SHARES],
             "prefill_batch": f"1 prefill chunk: {CAL_PREFILL[0]} tokens after {CAL_PREFILL[1]}",
             "decode_batches": [f"{b.num_reqs} decodes, contexts {int(b.kv_lens.min())}..{int(b.kv_lens.max())}"
                                for b in (small, large)],
