@@ -841,6 +841,147 @@ def serve_main(args):
     ctx.close()
 
 
+def serve_attn_main(args):
+    """The serving loop on the attention share, with look-ahead (Section 4.3): the native engine
+    forms each iteration (continuous batching, chunked prefill under an 8192-token budget) from the
+    trace's request stream (Poisson 4 req/s, lognormal prompts mean 4096 and outputs mean 256) and
+    owns the KV pages; each iteration is the attention of 32 Llama-3-8B layers over the engine's
+    rows and pages.  Modes: aggregated; adaptive, Algorithm 1 at the 50 ms TBT bound with up to
+    --max-k decode steps per prefill step (a split iteration runs duet_attn_lookahead, and its
+    decode requests gain k tokens); adaptive with one decode step.  Closed loop: arrivals are
+    admitted on a clock advanced by each iteration's fork-to-join time.  A decode token exists at
+    the end of its decode step (fork to the step's end, from HIP events on the decode stream; the
+    whole iteration under aggregated execution); a request's times between tokens are the gaps
+    between its consecutive tokens."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from paper_2511_04791_amd.calibration import calibrate_model
+
+    L = args.layers if args.layers is not None else 32
+    kmax = max(1, args.max_k)
+    budget, max_pages, pool, tbt = 8192, 4096, 20000, 50000.0
+    sh = dataclasses.replace(wl.LLAMA3_8B, num_layers=L)
+    ctx = duet.Context(0)
+    if not args.no_calibrate:
+        calibrate_model(ctx)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1007)
+    rnd = lambda *shape_: (torch.randn(*shape_, generator=gen, device="cuda") * 0.1).to(torch.bfloat16)
+    kcs = [rnd(pool, 8, 16, 128) for _ in range(L)]
+    vcs = [rnd(pool, 8, 128, 16) for _ in range(L)]
+    qs = [rnd(budget, 32, 128) for _ in range(L)]
+    outs = [torch.empty_like(q) for q in qs]
+    max_dec = 256  # decodes per iteration the look-ahead inputs are allocated for (more: aggregated)
+    qa = [rnd(max_dec, 32, 128) for _ in range((kmax - 1) * L)]
+    ka = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
+    va = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
+    oa = [torch.empty_like(x) for x in qa]
+    arrivals, prompts, outputs = wl.trace_requests(1005)
+    modes = {"agg": 1, f"adaptive_50ms_k{kmax}": kmax, "adaptive_50ms_k1": 1}
+    res = {}
+    ctx.set_profiling(2)
+    for mode, kcap in modes.items():
+        eng = duet.Engine(budget, pool, max_pages, shuffle_seed=1006)
+        clock_us, nxt, it, recorded = 0.0, 0, 0, 0
+        last_tok, gaps, lat, split_used, ks = {}, [], [], [], []
+        out_len, made = {}, {}   # per request: output tokens, tokens produced so far
+        toks = 0
+        while recorded < args.trace_iters:
+            while nxt < len(arrivals) and arrivals[nxt] * 1e6 <= clock_us:
+                rid_ = eng.add_request(int(prompts[nxt]), int(outputs[nxt]))
+                out_len[rid_] = int(outputs[nxt])
+                nxt += 1
+            w_, r_, _ = eng.stats()
+            if w_ == 0 and r_ == 0:
+                clock_us = float(arrivals[nxt]) * 1e6
+                continue
+            meta, table, ids = eng.step(decode_steps=kcap)
+            n_dec = int((meta[:, 0] == 1).sum())
+            if it < 200 or not len(meta):  # engine-only warm-up on a 50 ms clock
+                for row in range(n_dec):
+                    made[int(ids[row])] = made.get(int(ids[row]), 0) + 1
+                eng.complete(decode_steps_run=1)
+                it += 1
+                clock_us += 50000.0
+                continue
+            rows3 = [(int(k_), int(q_), int(c_)) for k_, _, q_, c_ in meta]
+            if mode == "agg":
+                sp = duet.CuSplit.agg()
+            else:
+                sp = duet.choose_cu_split(rows3, tbt, sh, ctx.model, max_decode_steps=kcap)[0]
+            if n_dec > max_dec:
+                sp = duet.CuSplit.agg()
+            k = sp.k_decode_steps if sp.mode == duet.SPLIT and n_dec else 1
+            n_tok = int(meta[:, 2].sum())
+            pt = torch.as_tensor(table, device="cuda")
+            q_l, o_l = [q[:n_tok] for q in qs], [o[:n_tok] for o in outs]
+            if k > 1:
+                sl = lambda xs: [xs[(s_ - 1) * L + l][:n_dec] for s_ in range(1, k) for l in range(L)]
+                ctx.attn_lookahead(q_l, sl(qa), sl(ka), sl(va), kcs, vcs, pt, meta, sp, outs=o_l,
+                                   outs_ahead=sl(oa))
+            else:
+                ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
+            kt = ctx.last_kernel_times()
+            it_us = kt["iteration_us"]
+            if sp.mode != duet.SPLIT:
+                t_tok = [it_us]                      # the tokens exist when the iteration ends
+            elif k > 1:
+                first = kt["decode_start_us"] + kt["decode_first_step_us"]
+                t_tok = [first + s_ * (kt["decode_start_us"] + kt["decode_total_us"] - first) / (k - 1)
+                         for s_ in range(k)]         # step 0's end, then evenly to the decode half's end
+            else:
+                t_tok = [kt["decode_start_us"] + kt["decode_total_us"]]
+            n_new = 0
+            for row in range(n_dec):
+                rid = int(ids[row])
+                got = min(k, out_len[rid] - made.get(rid, 0))  # the engine credits the same
+                made[rid] = made.get(rid, 0) + got
+                n_new += got
+                for t in t_tok[:got]:
+                    if rid in last_tok:
+                        gaps.append(clock_us + t - last_tok[rid])
+                    last_tok[rid] = clock_us + t
+            eng.complete(decode_steps_run=k)
+            toks += n_tok - n_dec + n_new
+            lat.append(it_us)
+            split_used.append(sp.mode == duet.SPLIT)
+            ks.append(k)
+            clock_us += it_us
+            it += 1
+            recorded += 1
+            if recorded % 50 == 0:
+                print(f"serve-attn {mode}: {recorded}/{args.trace_iters} iterations", file=sys.stderr, flush=True)
+        eng.close()
+        g, a = np.array(gaps), np.array(lat)
+        res[mode] = {"tbt_p50_us": round(float(np.percentile(g, 50)), 1),
+                     "tbt_p99_us": round(float(np.percentile(g, 99)), 1),
+                     "tbt_max_us": round(float(g.max()), 1),
+                     "tbt_slo_attainment": round(float(np.mean(g <= tbt)), 4),
+                     "iteration_p50_us": round(float(np.percentile(a, 50)), 1),
+                     "iteration_p99_us": round(float(np.percentile(a, 99)), 1),
+                     "tokens_per_s": round(toks / (a.sum() * 1e-6), 1),
+                     "split_fraction": round(float(np.mean(split_used)), 3),
+                     "k_max_used": int(max(ks)), "decode_gaps": int(len(g))}
+    ctx.set_profiling(0)
+    k_mode = f"adaptive_50ms_k{kmax}"
+    line = {"metric": "serving-loop TBT p99, attention share, with look-ahead (us)",
+            "value": res[k_mode]["tbt_p99_us"], "unit": "us", "n_gpus": 1, "higher_is_better": False,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"serving loop: native engine, {args.trace_iters} iterations after 200 warm-up, "
+                                   "Poisson 4 req/s, prompts LogN(mean 4096, sigma 1.0) <= 32768, outputs LogN(mean 256, "
+                                   f"sigma 0.7), budget {budget}, {L} llama3-8b attention layers, KV pages persistent per "
+                                   f"request, TBT bound {tbt / 1000:.0f} ms, look-ahead up to {kmax} decode steps; closed "
+                                   "loop on each iteration's fork-to-join time"},
+            "modes": res,
+            "tbt_p99_vs_agg": round(res[k_mode]["tbt_p99_us"] / res["agg"]["tbt_p99_us"], 4),
+            "throughput_vs_agg": round(res[k_mode]["tokens_per_s"] / res["agg"]["tokens_per_s"], 4)}
+    print(json.dumps(line), flush=True)
+    ctx.close()
+
+
 def block_lookahead(args, L, ffn):
     """Look-ahead decode over whole blocks (Section 4.3): one call runs the 2048-token chunk once
     and --block-k decode steps of the 64 decodes (step s's residual rows are fresh synthetic rows).
@@ -1019,6 +1160,8 @@ def main():
     ap.add_argument("--serve", action="store_true",
                     help="run the serving loop: the native engine forms the trace's iterations over whole blocks, "
                          "aggregated vs adaptive vs static splits")
+    ap.add_argument("--attn-only", action="store_true",
+                    help="--serve: the attention share only, with look-ahead decode steps up to --max-k")
     ap.add_argument("--block-k", type=int, default=1,
                     help="with --block: decode steps per call (look-ahead), split 160/96 vs aggregated")
     ap.add_argument("--block", action="store_true",
@@ -1042,6 +1185,8 @@ def main():
         return trace_main(args)
     if args.lookahead:
         return lookahead_main(args)
+    if args.serve and args.attn_only:
+        return serve_attn_main(args)
     if args.serve:
         return serve_main(args)
     if args.block:

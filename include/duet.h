@@ -446,9 +446,19 @@ int duet_engine_add_request(duet_engine* engine, int32_t prompt_len, int32_t out
  * when max_reqs is too small or the previous step is not completed. */
 int duet_engine_step(duet_engine* engine, duet_seq_meta* meta, int32_t* page_table, int64_t* req_ids,
                      int32_t max_reqs, int32_t* num_reqs);
-/* Marks the last step done: chunks advance, each decode gains its token, finished requests release
- * their pages. */
+/* Section 4.3: the same step with decode_steps = k >= 1 look-ahead decode steps (for
+ * duet_attn_lookahead with k_decode_steps = k): each decode's page-table row covers
+ * cached_len + k tokens (the rows of meta are as for one step).  DUET_EINVAL also when a decode's
+ * k tokens would need more than max_pages_per_req pages. */
+int duet_engine_step_lookahead(duet_engine* engine, int32_t decode_steps, duet_seq_meta* meta, int32_t* page_table,
+                               int64_t* req_ids, int32_t max_reqs, int32_t* num_reqs);
+/* Marks the last step done: chunks advance, each decode gains its token (after a look-ahead step,
+ * min(k, its remaining output) tokens), finished requests release their pages. */
 int duet_engine_complete(duet_engine* engine);
+/* The same when only the first decode_steps_run (1 .. the step's k) look-ahead steps ran, e.g. a step
+ * formed with pages for the largest k allowed before Algorithm 1 chose a smaller one; the pages
+ * reserved for the other steps stay with their requests. */
+int duet_engine_complete_lookahead(duet_engine* engine, int32_t decode_steps_run);
 int duet_engine_stats(const duet_engine* engine, int64_t* waiting, int64_t* running, int64_t* free_pages);
 
 /* ---- look-ahead decode (Section 4.3, interruption-free dispatch) -------------------------------

@@ -290,20 +290,31 @@ class Engine:
                 "duet_engine_stats")
         return w.value, r.value, f.value
 
-    def step(self):
-        """The next step: (seq_meta int32 [R, 4], page_table int32 [R, max_pages], request ids int64 [R])."""
+    def step(self, decode_steps: int = 1):
+        """The next step: (seq_meta int32 [R, 4], page_table int32 [R, max_pages], request ids int64 [R]).
+        decode_steps > 1: a look-ahead step (duet_engine_step_lookahead)."""
         w, r, _ = self.stats()
         cap = int(w + r) + 1
         meta = np.zeros((cap, 4), dtype=np.int32)
         table = np.zeros((cap, self.max_pages), dtype=np.int32)
         ids = np.zeros(cap, dtype=np.int64)
         n = ctypes.c_int32()
-        N.check(N.lib().duet_engine_step(self.handle, meta.ctypes.data, table.ctypes.data, ids.ctypes.data, cap,
-                                         ctypes.byref(n)), "duet_engine_step")
+        if decode_steps == 1:
+            N.check(N.lib().duet_engine_step(self.handle, meta.ctypes.data, table.ctypes.data, ids.ctypes.data, cap,
+                                             ctypes.byref(n)), "duet_engine_step")
+        else:
+            N.check(N.lib().duet_engine_step_lookahead(self.handle, int(decode_steps), meta.ctypes.data,
+                                                       table.ctypes.data, ids.ctypes.data, cap, ctypes.byref(n)),
+                    "duet_engine_step_lookahead")
         return meta[:n.value].copy(), table[:n.value].copy(), ids[:n.value].copy()
 
-    def complete(self) -> None:
-        N.check(N.lib().duet_engine_complete(self.handle), "duet_engine_complete")
+    def complete(self, decode_steps_run: int | None = None) -> None:
+        """Completes the step; decode_steps_run: of a look-ahead step, the steps that ran."""
+        if decode_steps_run is None:
+            N.check(N.lib().duet_engine_complete(self.handle), "duet_engine_complete")
+        else:
+            N.check(N.lib().duet_engine_complete_lookahead(self.handle, int(decode_steps_run)),
+                    "duet_engine_complete_lookahead")
 
     def close(self) -> None:
         if self.handle:

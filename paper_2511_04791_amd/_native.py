@@ -85,7 +85,9 @@ _SIGS = {
     "duet_engine_destroy": (c_int32, [c_void_p]),
     "duet_engine_add_request": (c_int32, [c_void_p, c_int32, c_int32, P(c_int64)]),
     "duet_engine_step": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, P(c_int32)]),
+    "duet_engine_step_lookahead": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_int32, P(c_int32)]),
     "duet_engine_complete": (c_int32, [c_void_p]),
+    "duet_engine_complete_lookahead": (c_int32, [c_void_p, c_int32]),
     "duet_engine_stats": (c_int32, [c_void_p, P(c_int64), P(c_int64), P(c_int64)]),
     "duet_block_forward": (c_int32, [c_void_p, P(Shape), P(BlockShape), P(BlockWeights), ctypes.c_float, c_void_p,
                                      P(c_void_p), P(c_void_p), P(c_void_p), c_int64, c_void_p, c_int32, P(Batch), CuSplit,

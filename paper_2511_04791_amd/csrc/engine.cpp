@@ -10,7 +10,9 @@
 //   3. the cache pages the scheduled tokens need are reserved from a free list (all or nothing).
 // Completing the step advances the chunks, gives each decode its token, admits the requests
 // whose first chunk ran, and releases the pages of the requests that have produced all their
-// output tokens.  Host-only integer bookkeeping: the GPU work of a step is duet_block_forward
+// output tokens.  A look-ahead step (Section 4.3: k decode steps while one prefill step runs)
+// reserves pages for k tokens of every decode and credits each decode min(k, its remaining
+// output) tokens; the steps a finished request would not need are computed and dropped.  Host-only integer bookkeeping: the GPU work of a step is duet_block_forward
 // or duet_attn_iteration on the returned rows and page table.
 #include <algorithm>
 #include <cstdint>
@@ -40,6 +42,7 @@ struct duet_engine {
   std::vector<std::unique_ptr<Req>> running;
   // the step formed but not yet completed
   bool pending = false;
+  int step_k = 1;  // decode steps of the pending step
   std::vector<Req*> step_decodes;
   std::vector<std::pair<Req*, int>> step_chunks;
   int64_t next_id = 0;
@@ -106,11 +109,13 @@ int duet_engine_add_request(duet_engine* e, int32_t prompt_len, int32_t output_l
   return DUET_OK;
 }
 
-int duet_engine_step(duet_engine* e, duet_seq_meta* meta, int32_t* page_table, int64_t* req_ids, int32_t max_reqs,
-                     int32_t* num_reqs) {
+int duet_engine_step_lookahead(duet_engine* e, int32_t decode_steps, duet_seq_meta* meta, int32_t* page_table,
+                               int64_t* req_ids, int32_t max_reqs, int32_t* num_reqs) {
   duet::clear_error();
   if (!e || !meta || !page_table || !num_reqs) return fail(DUET_EINVAL, "NULL argument");
   if (e->pending) return fail(DUET_EINVAL, "the previous step is not completed");
+  if (decode_steps < 1) return fail(DUET_EINVAL, "decode_steps %d < 1", decode_steps);
+  const int k = decode_steps;
   std::vector<Req*> decodes;
   std::vector<std::pair<Req*, int>> chunks;
   int budget = e->budget;
@@ -130,10 +135,16 @@ int duet_engine_step(duet_engine* e, duet_seq_meta* meta, int32_t* page_table, i
   for (auto& r : e->waiting) take_chunk(r.get());
   const int n = (int)(decodes.size() + chunks.size());
   if (n > max_reqs) return fail(DUET_EINVAL, "the step holds %d requests, the arrays %d", n, max_reqs);
-  // Pages: a decode's token sits at position prompt + generated, a chunk's tokens at
-  // prefilled .. prefilled + take - 1.
+  // Pages: a decode's k tokens sit at positions prompt + generated .. + k - 1, a chunk's tokens
+  // at prefilled .. prefilled + take - 1.
   int64_t need = 0;
-  for (Req* r : decodes) need += std::max(0, pages_for((int64_t)r->prompt + r->generated + 1, e->page_size) - (int)r->pages.size());
+  for (Req* r : decodes) {
+    const int want = pages_for((int64_t)r->prompt + r->generated + k, e->page_size);
+    if (want > e->max_pages)
+      return fail(DUET_EINVAL, "request %lld: %d decode steps need %d pages, rows hold %d", (long long)r->id, k, want,
+                  e->max_pages);
+    need += std::max(0, want - (int)r->pages.size());
+  }
   for (auto& c : chunks)
     need += std::max(0, pages_for((int64_t)c.first->prefilled + c.second, e->page_size) - (int)c.first->pages.size());
   if (need > (int64_t)e->free_pages.size())
@@ -154,7 +165,7 @@ int duet_engine_step(duet_engine* e, duet_seq_meta* meta, int32_t* page_table, i
     ++row;
   };
   for (Req* r : decodes) {
-    reserve(r, (int64_t)r->prompt + r->generated + 1);
+    reserve(r, (int64_t)r->prompt + r->generated + k);
     emit(r, DUET_KIND_DECODE, 1, r->prompt + r->generated);
   }
   for (auto& c : chunks) {
@@ -164,14 +175,23 @@ int duet_engine_step(duet_engine* e, duet_seq_meta* meta, int32_t* page_table, i
   *num_reqs = n;
   e->step_decodes = std::move(decodes);
   e->step_chunks = std::move(chunks);
+  e->step_k = k;
   e->pending = true;
   return DUET_OK;
 }
 
-int duet_engine_complete(duet_engine* e) {
+int duet_engine_step(duet_engine* e, duet_seq_meta* meta, int32_t* page_table, int64_t* req_ids, int32_t max_reqs,
+                     int32_t* num_reqs) {
+  return duet_engine_step_lookahead(e, 1, meta, page_table, req_ids, max_reqs, num_reqs);
+}
+
+int duet_engine_complete_lookahead(duet_engine* e, int32_t decode_steps_run) {
   duet::clear_error();
   if (!e) return fail(DUET_EINVAL, "engine is NULL");
   if (!e->pending) return fail(DUET_EINVAL, "no step to complete");
+  if (decode_steps_run < 1 || decode_steps_run > e->step_k)
+    return fail(DUET_EINVAL, "decode_steps_run %d not in [1, %d]", decode_steps_run, e->step_k);
+  e->step_k = decode_steps_run;
   for (auto& c : e->step_chunks) {
     Req* r = c.first;
     auto it = std::find_if(e->waiting.begin(), e->waiting.end(), [&](const std::unique_ptr<Req>& w) { return w.get() == r; });
@@ -181,7 +201,7 @@ int duet_engine_complete(duet_engine* e) {
     }
     r->prefilled += c.second;
   }
-  for (Req* r : e->step_decodes) ++r->generated;
+  for (Req* r : e->step_decodes) r->generated = std::min(r->output, r->generated + e->step_k);
   std::vector<std::unique_ptr<Req>> keep;
   for (auto& r : e->running) {
     if (r->generated < r->output) {
@@ -195,6 +215,14 @@ int duet_engine_complete(duet_engine* e) {
   e->step_chunks.clear();
   e->pending = false;
   return DUET_OK;
+}
+
+int duet_engine_complete(duet_engine* e) {
+  if (!e) {
+    duet::clear_error();
+    return fail(DUET_EINVAL, "engine is NULL");
+  }
+  return duet_engine_complete_lookahead(e, e->step_k);
 }
 
 int duet_engine_stats(const duet_engine* e, int64_t* waiting, int64_t* running, int64_t* free_pages) {

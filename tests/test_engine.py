@@ -109,3 +109,60 @@ def test_engine_argument_checks():
         eng.complete()
     with pytest.raises(duet.DuetError):
         duet.Engine(0, 10, 4)
+
+
+def test_lookahead_step_reserves_and_credits_k_tokens():
+    """A look-ahead step (Section 4.3) reserves pages for k tokens of every decode and credits each
+    decode min(k, its remaining output) tokens; a request whose output ends inside the step is
+    released when the step completes."""
+    eng = duet.Engine(64, 100, 8)
+    a = eng.add_request(30, 10)        # decodes 10 tokens
+    b = eng.add_request(20, 2)         # decodes 2 tokens
+    meta, _, ids = eng.step()          # both prompts (50 tokens)
+    assert meta[:, 0].tolist() == [0, 0]
+    eng.complete()
+    meta, table, ids = eng.step(decode_steps=4)
+    assert meta.tolist() == [[1, 0, 1, 30], [1, 1, 1, 20]] and ids.tolist() == [a, b]
+    for row, c in enumerate((30, 20)):
+        n = -(-(c + 4) // PS)          # pages for the cached tokens and 4 new ones
+        assert (table[row, :n] >= 0).all() and (table[row, n:] == -1).all()
+    eng.complete()
+    w, r, _ = eng.stats()
+    assert (w, r) == (0, 1)            # b produced its 2 tokens and left
+    meta, _, ids = eng.step(decode_steps=3)
+    assert meta.tolist() == [[1, 0, 1, 34]] and ids.tolist() == [a]   # a gained 4 tokens
+    eng.complete()
+    meta, _, _ = eng.step(decode_steps=5)
+    assert meta.tolist() == [[1, 0, 1, 37]]
+    eng.complete()                     # 3 + 4 + 5 > 10: a is done
+    assert eng.stats() == (0, 0, 100)
+
+
+def test_lookahead_step_checks():
+    eng = duet.Engine(64, 100, 3)      # rows of 3 pages: 48 tokens
+    eng.add_request(40, 8)
+    eng.step()
+    eng.complete()
+    before = eng.stats()
+    with pytest.raises(duet.DuetError):
+        eng.step(decode_steps=9)       # 40 + 9 tokens need 4 pages
+    with pytest.raises(duet.DuetError):
+        eng.step(decode_steps=0)
+    assert eng.stats() == before
+    meta, _, _ = eng.step(decode_steps=8)
+    assert meta.tolist() == [[1, 0, 1, 40]]
+
+
+def test_lookahead_step_completed_with_fewer_steps():
+    eng = duet.Engine(64, 100, 8)
+    eng.add_request(30, 10)
+    eng.step()
+    eng.complete()
+    eng.step(decode_steps=6)           # pages for 6 tokens
+    with pytest.raises(duet.DuetError):
+        eng.complete(decode_steps_run=7)
+    eng.complete(decode_steps_run=2)   # only 2 ran
+    meta, table, _ = eng.step()
+    assert meta.tolist() == [[1, 0, 1, 32]]
+    assert (table[0, :3] >= 0).all()   # the page reserved for the 6 steps stays
+    eng.complete()
