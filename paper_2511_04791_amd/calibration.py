@@ -46,7 +46,8 @@ from . import _native as N
 TABLE_SHARES = tuple(range(N.CU_STEP, N.TOTAL_CUS + 1, N.CU_STEP))
 GRID_SHARES = tuple(range(N.SPLIT_STEP, N.TOTAL_CUS + 1, N.SPLIT_STEP))
 
-CAL_PREFILL = (8192, 8192)        # (q_len, cached_len) of the calibration chunk
+CAL_PREFILL = (8192, 8192)        # (q_len, cached_len) of the calibration chunk: the throughput point
+CAL_PREFILL_SHORT = (4, 1536, 0)  # (requests, q_len, cached_len) of short chunks: the fixed-latency point
 CAL_DECODE_SMALL = (48, (256, 2048))    # decodes, context range: the fixed-latency point
 CAL_DECODE_LARGE = (96, (1024, 8192))   # the throughput point
 LOOKAHEAD_K = (2, 10)             # decode steps of the two look-ahead calls a step time is taken from
@@ -54,7 +55,8 @@ SHARED_K_CAP = 48                 # most look-ahead steps of a sharing measureme
 
 
 def calibration_batches(shape, seed: int = 4242, reserve_tokens: int = 0):
-    """(prefill-only, small decode-only, large decode-only, mixed) calibration batches."""
+    """(prefill-only, small decode-only, large decode-only, mixed, short prefill-only) calibration
+    batches."""
     rng = np.random.Generator(np.random.PCG64(seed))
 
     def decodes(n, lo_hi):
@@ -69,7 +71,9 @@ def calibration_batches(shape, seed: int = 4242, reserve_tokens: int = 0):
                           reserve_tokens=reserve_tokens)
     mixed = wl.make_batch(shape, pre_rows + large_rows, page_seed=seed + 3, name="calibration-mixed",
                           reserve_tokens=max(reserve_tokens, SHARED_K_CAP))
-    return pre, small, large, mixed
+    n_s, q_s, c_s = CAL_PREFILL_SHORT
+    short = wl.make_batch(shape, [(wl.KIND_PREFILL, q_s, c_s)] * n_s, page_seed=seed + 4, name="calibration-prefill-short")
+    return pre, small, large, mixed, short
 
 
 def fill_table(grid_rates: dict) -> list:
@@ -173,17 +177,27 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, shared_l
     _, probe_fl, probe_by = model.tables()
     sh = wl.LLAMA3_8B if shape is None else shape
     kmax = max(LOOKAHEAD_K)
-    pre, small, large, mixed = calibration_batches(sh, seed, reserve_tokens=kmax)
+    pre, small, large, mixed, short = calibration_batches(sh, seed, reserve_tokens=kmax)
     f_pre, _ = batch_work(pre.seq_meta, sh, wl.KIND_PREFILL)
-    # prefill: Pi(S) = F / t on every grid share
-    t_pre, fl_grid = {}, {}
-    lay = [wl.make_tensors(pre, seed=seed + l, device="cuda") for l in range(layers)]
-    pt = torch.as_tensor(pre.page_table, device="cuda")
+    f_short, _ = batch_work(short.seq_meta, sh, wl.KIND_PREFILL)
+    # prefill: the long chunk and the short chunks on every grid share; the two points give Pi(S)
+    # (the slope) and the fixed per-layer latency t0(S) (the intercept)
+    t_pre, t_short = {}, {}
+    for b, t_out, sd in ((pre, t_pre, 0), (short, t_short, 50)):
+        lay = [wl.make_tensors(b, seed=seed + sd + l, device="cuda") for l in range(layers)]
+        pt = torch.as_tensor(b.page_table, device="cuda")
+        for s_ in GRID_SHARES:
+            split = CuSplit.agg() if s_ == N.TOTAL_CUS else CuSplit.split(s_, N.TOTAL_CUS - s_)
+            t_out[s_] = statistics.median(r["prefill"] for r in _times(ctx, b, lay, pt, split, reps))
+        del lay
+    fl_grid, t0_pre_grid = {}, {}
     for s_ in GRID_SHARES:
-        split = CuSplit.agg() if s_ == N.TOTAL_CUS else CuSplit.split(s_, N.TOTAL_CUS - s_)
-        t_pre[s_] = statistics.median(r["prefill"] for r in _times(ctx, pre, lay, pt, split, reps))
-        fl_grid[s_] = f_pre / (t_pre[s_] * 1e-6)
-    del lay
+        tl, ts = t_pre[s_] * 1e-6, t_short[s_] * 1e-6
+        fl = (f_pre - f_short) / (tl - ts) if tl > ts else 0.0
+        t0 = ts - f_short / fl if fl > 0 else -1.0
+        if fl <= 0 or t0 < 0:  # no usable intercept: the long chunk's rate and no fixed term
+            fl, t0 = f_pre / tl, 0.0
+        fl_grid[s_], t0_pre_grid[s_] = fl, t0
     # decode: a look-ahead step of the small and of the large batch on every grid share; the two
     # points give B(S) (the slope) and the fixed per-layer latency t0(S) (the intercept)
     step = {}
@@ -207,7 +221,7 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, shared_l
         by_grid[s_], t0_grid[s_] = bw, t0
     flops, bytes_ = fill_table(fl_grid), fill_table(by_grid)
     model.set_tables(flops, bytes_)
-    model.set_launch_tables([0.0] * len(TABLE_SHARES), fill_launch(t0_grid))
+    model.set_launch_tables(fill_launch(t0_pre_grid), fill_launch(t0_grid))
     model.set_efficiency(1.0, 1.0)
 
     # 3. both halves at once, on every split of the grid, with the decode partition stepping for the
@@ -225,7 +239,7 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, shared_l
         t_p = t_pre[sp] * f_mix / f_pre  # the mixed batch's chunk, standalone, per layer (us)
         k_sh[sp] = max(1, min(SHARED_K_CAP, int(t_p * 1e-6 / step["large"][sd])))
         t_pre_sh[sp], t_dec_sh[sd] = _shared_lookahead(ctx, mixed, parts, pt, sp, k_sh[sp], reps)
-        fl_sh[sp] = f_mix / (t_pre_sh[sp] * 1e-6)
+        fl_sh[sp] = f_mix / max(t_pre_sh[sp] * 1e-6 - t0_pre_grid[sp], 0.5 * t_pre_sh[sp] * 1e-6)
         # the fixed term is priced separately; the shared rate covers the rest
         by_sh[sd] = b_mix / max(t_dec_sh[sd] * 1e-6 - t0_grid[sd], 0.5 * t_dec_sh[sd] * 1e-6)
     del lay, la, parts
@@ -238,6 +252,10 @@ def calibrate_model(ctx, seed: int = 4242, reps: int = 5, scratch=None, shared_l
             "decode_batches": [f"{b.num_reqs} decodes, contexts {int(b.kv_lens.min())}..{int(b.kv_lens.max())}"
                                for b in (small, large)],
             "prefill_us": [round(t_pre[s_], 1) for s_ in GRID_SHARES],
+            "prefill_short_batch": f"{CAL_PREFILL_SHORT[0]} prefill chunks: {CAL_PREFILL_SHORT[1]} tokens after "
+                                   f"{CAL_PREFILL_SHORT[2]}",
+            "prefill_short_us": [round(t_short[s_], 1) for s_ in GRID_SHARES],
+            "prefill_t0_us": [round(t0_pre_grid[s_] * 1e6, 2) for s_ in GRID_SHARES],
             "decode_step_us_small": [round(step["small"][s_] * 1e6, 1) for s_ in GRID_SHARES],
             "decode_step_us_large": [round(step["large"][s_] * 1e6, 1) for s_ in GRID_SHARES],
             "pi_tflops": [round(fl_grid[s_] / 1e12, 1) for s_ in GRID_SHARES],
