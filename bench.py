@@ -742,15 +742,18 @@ def lookahead_main(args):
     ctx.close()
 
 def serve_main(args):
-    """The serving loop (Section 3 and Section 4 over whole blocks): the native engine forms each
-    iteration (continuous batching, chunked prefill under an 8192-token budget) from the trace's
-    request stream (Poisson 4 req/s, lognormal prompts mean 4096 and outputs mean 256, 50 ms per
-    iteration) and owns the KV pages, which persist per request; duet_block_forward runs the
-    iteration's 32 Llama-3-8B blocks and appends its tokens' keys and values to those pages.  Each
-    mode replays the same 200 iterations (after 200 engine-only warm-up iterations) on a fresh
-    engine: aggregated, adaptive (Algorithm 1 on the full-model estimate at a 50 ms TBT bound)
-    and static splits.  Decode-ready time: fork to the end of the decode partition (the whole
-    iteration under AGG)."""
+    """The serving loop (Sections 3 and 4): the native engine forms each iteration (continuous
+    batching, chunked prefill under an 8192-token budget) from the trace's request stream (Poisson
+    4 req/s, lognormal prompts mean 4096 and outputs mean 256) and owns the KV pages, which persist
+    per request.  Each iteration is 32 Llama-3-8B blocks (duet_block_forward, random-init weights),
+    or with --attn-only the attention of 32 layers, over the engine's rows and pages.  Modes:
+    aggregated; adaptive (Algorithm 1 at the 50 ms TBT bound, on the full-model estimate for
+    blocks) with one decode step, and with up to --max-k look-ahead decode steps (Section 4.3: a
+    split iteration's decode requests gain k tokens while its prefill runs once); static splits.
+    Closed loop: arrivals are admitted on a clock advanced by each iteration's fork-to-join time,
+    after 200 engine-only warm-up iterations on a 50 ms clock.  A decode token exists at the end of
+    its decode step (from HIP events; the whole iteration under aggregated execution), and a
+    request's times between tokens are the gaps between its consecutive tokens."""
     import dataclasses
     import numpy as np
     import torch
@@ -758,180 +761,42 @@ def serve_main(args):
     from paper_2511_04791_amd import workloads as wl
     from paper_2511_04791_amd.calibration import calibrate_model
 
+    full = not args.attn_only
     L = args.layers if args.layers is not None else 32
-    ffn, budget, max_pages, pool, tbt = 14336, 8192, 4096, 60000, 50000.0
+    kmax = max(1, args.max_k)
+    ffn, budget, max_pages, tbt = 14336, 8192, 4096, 50000.0
+    pool = 40000 if full else 20000
     sh = dataclasses.replace(wl.LLAMA3_8B, num_layers=L)
     block = duet.BlockShape(ffn, 0, duet.BLOCK_GQA_QKV | duet.BLOCK_FUSED_GATE_UP)
+    d_model = sh.num_q_heads * sh.head_dim
     ctx = duet.Context(0)
     if not args.no_calibrate:
         calibrate_model(ctx)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(1006)
-    kcs = [(torch.randn(pool, 8, 16, 128, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
-    vcs = [(torch.randn(pool, 8, 128, 16, generator=gen, device="cuda") * 0.1).to(torch.bfloat16) for _ in range(L)]
-    weights = wl.block_weights(sh, ffn, L, gen)
-    xbuf = torch.randn(budget, 32 * 128, generator=gen, device="cuda").to(torch.bfloat16)
-    arrivals, prompts, outputs = wl.trace_requests(1005)
-    modes = ["agg", "adaptive_50ms"] + [f"static_{p_}_{256 - p_}" for p_ in (64, 128, 192)]
-    res, tokens_total = {}, None
-    ctx.set_profiling(1)
-    for mode in modes:
-        eng = duet.Engine(budget, pool, max_pages, shuffle_seed=1006)
-        clock, nxt, it, recorded = 0.0, 0, 0, 0
-        lat, ready, split_used, toks, has_dec_it = [], [], [], 0, []
-        while recorded < args.trace_iters:
-            while nxt < len(arrivals) and arrivals[nxt] <= clock:
-                eng.add_request(int(prompts[nxt]), int(outputs[nxt]))
-                nxt += 1
-            w_, r_, _ = eng.stats()
-            if w_ == 0 and r_ == 0:
-                clock = float(arrivals[nxt])
-                continue
-            meta, table, _ = eng.step()
-            if it >= 200 and len(meta):
-                rows3 = [(int(k), int(q), int(c)) for k, _, q, c in meta]
-                if mode == "agg":
-                    sp = duet.CuSplit.agg()
-                elif mode == "adaptive_50ms":
-                    sp = duet.choose_cu_split_model(rows3, tbt, sh, block, ctx.model, max_decode_steps=1)[0]
-                else:
-                    s_p = int(mode.split("_")[1])
-                    sp = duet.CuSplit.split(s_p, 256 - s_p)
-                n_tok = int(meta[:, 2].sum())
-                pt = torch.as_tensor(table, device="cuda")
-                ctx.block_forward(xbuf[:n_tok], weights, kcs, vcs, pt, meta, ffn, sp)
-                kt = ctx.last_kernel_times()
-                lat.append(kt["iteration_us"])
-                ready.append(kt["decode_start_us"] + kt["decode_total_us"] if kt["decode_total_us"] > 0
-                             else kt["iteration_us"])
-                split_used.append(sp.mode == duet.SPLIT)
-                has_dec_it.append(bool((meta[:, 0] == 1).any()))
-                toks += n_tok
-                recorded += 1
-                if recorded % 50 == 0:
-                    print(f"serve {mode}: {recorded}/{args.trace_iters} iterations", file=sys.stderr, flush=True)
-            eng.complete()
-            it += 1
-            # the clock advances by the measured iteration (engine-only warm-up: 50 ms)
-            clock += lat[-1] * 1e-6 if it > 200 and lat else 0.05
-        eng.close()
-        a, r = np.array(lat), np.array(ready)
-        tb = np.array([x for x, d in zip(lat, has_dec_it) if d])
-        res[mode] = {"tbt_p50_us": round(float(np.percentile(tb, 50)), 1),
-                     "tbt_p99_us": round(float(np.percentile(tb, 99)), 1),
-                     "tbt_slo_attainment": round(float(np.mean(tb <= tbt)), 4),
-                     "decode_ready_p50_us": round(float(np.percentile(r, 50)), 1),
-                     "decode_ready_p99_us": round(float(np.percentile(r, 99)), 1),
-                     "decode_ready_max_us": round(float(r.max()), 1),
-                     "iteration_p50_us": round(float(np.percentile(a, 50)), 1),
-                     "iteration_p99_us": round(float(np.percentile(a, 99)), 1),
-                     "tokens_per_s": round(toks / (a.sum() * 1e-6), 1),
-                     "split_fraction": round(float(np.mean(split_used)), 3)}
-    ctx.set_profiling(0)
-    line = {"metric": "serving-loop TBT p99 (latency of the iterations that carry decodes), full model (us)",
-            "value": res["adaptive_50ms"]["tbt_p99_us"],
-            "unit": "us", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": f"serving loop: native engine, {args.trace_iters} iterations after 200 warm-up, Poisson "
-                                   "4 req/s, prompts LogN(mean 4096, sigma 1.0) <= 32768, outputs LogN(mean 256, sigma "
-                                   f"0.7), budget {budget}, {L} llama3-8b blocks (random-init weights, FFN {ffn}), "
-                                   f"KV pages persistent per request, TBT bound {tbt / 1000:.0f} ms; closed loop: arrivals are admitted "
-                                   "on a clock advanced by each measured iteration"},
-            "modes": res}
-    print(json.dumps(line), flush=True)
-    ctx.close()
-
-
-def accuracy_main(args):
-    """The latency model's accuracy per CU count (Appendix A): predicted against measured attention
-    latency of an 8 x 1024-token prefill batch and of a 16-request decode batch at context 1024
-    (Llama-3-8B shapes; 4 layers per call, each with its own KV pool; median of 5 calls) on every
-    share of the 32-CU grid, each batch alone on its share.  The model is calibrated on the generic
-    batches, none of these."""
-    import dataclasses
-    import statistics as st_
-    import torch
-    import paper_2511_04791_amd as duet
-    from paper_2511_04791_amd import workloads as wl
-    from paper_2511_04791_amd.calibration import GRID_SHARES, _times, calibrate_model
-
-    ctx = duet.Context(0)
-    calibrate_model(ctx)
-    L = 4
-    sh1 = dataclasses.replace(wl.LLAMA3_8B, num_layers=1)
-    batches = {"prefill 8 x 1024": (wl.make_batch(wl.LLAMA3_8B, [(0, 1024, 0)] * 8, page_seed=901), 0),
-               "decode 16 x 1024": (wl.make_batch(wl.LLAMA3_8B, [(1, 1, 1023)] * 16, page_seed=902), 1)}
-    out = {}
-    for name, (b, kind) in batches.items():
-        layers = [wl.make_tensors(b, seed=903 + l, device="cuda") for l in range(L)]
-        pt = torch.as_tensor(b.page_table, device="cuda")
-        rows3 = [(int(k_), int(q_), int(c_)) for k_, q_, c_ in zip(b.kinds, b.q_lens, b.cached_lens)]
-        rows = []
-        for cus in GRID_SHARES:
-            if cus == duet.TOTAL_CUS:
-                split = duet.CuSplit.agg()
-            else:
-                split = (duet.CuSplit.split(cus, duet.TOTAL_CUS - cus) if kind == 0 else
-                         duet.CuSplit.split(duet.TOTAL_CUS - cus, cus))
-            meas = st_.median(r["prefill" if kind == 0 else "decode"] for r in _times(ctx, b, layers, pt, split, 5))
-            pred = duet.predict_partition_latency(rows3, kind, cus, sh1, ctx.model, shared=False)
-            rows.append({"cus": cus, "measured_us": round(meas, 1), "predicted_us": round(pred, 1),
-                         "error": round((pred - meas) / meas, 4)})
-            print(f"[accuracy] {name} on {cus} CUs: measured {meas:.1f} us, predicted {pred:.1f} us", file=sys.stderr,
-                  flush=True)
-        errs = [r["error"] for r in rows]
-        out[name] = {"rows": rows, "mean_abs_error": round(st_.fmean(abs(e) for e in errs), 4),
-                     "min_error": min(errs), "max_error": max(errs)}
-        del layers
-    worst = max(v["mean_abs_error"] for v in out.values())
-    print(json.dumps({"metric": "latency model mean |prediction error| per CU share (Appendix A batches)",
-                      "value": worst, "unit": "fraction", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16",
-                      "data": "synthetic", "batches": out}), flush=True)
-    ctx.close()
-
-
-def serve_attn_main(args):
-    """The serving loop on the attention share, with look-ahead (Section 4.3): the native engine
-    forms each iteration (continuous batching, chunked prefill under an 8192-token budget) from the
-    trace's request stream (Poisson 4 req/s, lognormal prompts mean 4096 and outputs mean 256) and
-    owns the KV pages; each iteration is the attention of 32 Llama-3-8B layers over the engine's
-    rows and pages.  Modes: aggregated; adaptive, Algorithm 1 at the 50 ms TBT bound with up to
-    --max-k decode steps per prefill step (a split iteration runs duet_attn_lookahead, and its
-    decode requests gain k tokens); adaptive with one decode step.  Closed loop: arrivals are
-    admitted on a clock advanced by each iteration's fork-to-join time.  A decode token exists at
-    the end of its decode step (fork to the step's end, from HIP events on the decode stream; the
-    whole iteration under aggregated execution); a request's times between tokens are the gaps
-    between its consecutive tokens."""
-    import dataclasses
-    import numpy as np
-    import torch
-    import paper_2511_04791_amd as duet
-    from paper_2511_04791_amd import workloads as wl
-    from paper_2511_04791_amd.calibration import calibrate_model
-
-    L = args.layers if args.layers is not None else 32
-    kmax = max(1, args.max_k)
-    budget, max_pages, pool, tbt = 8192, 4096, 20000, 50000.0
-    sh = dataclasses.replace(wl.LLAMA3_8B, num_layers=L)
-    ctx = duet.Context(0)
-    if not args.no_calibrate:
-        calibrate_model(ctx)
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(1007)
     rnd = lambda *shape_: (torch.randn(*shape_, generator=gen, device="cuda") * 0.1).to(torch.bfloat16)
     kcs = [rnd(pool, 8, 16, 128) for _ in range(L)]
     vcs = [rnd(pool, 8, 128, 16) for _ in range(L)]
-    qs = [rnd(budget, 32, 128) for _ in range(L)]
-    outs = [torch.empty_like(q) for q in qs]
     max_dec = 256  # decodes per iteration the look-ahead inputs are allocated for (more: aggregated)
-    qa = [rnd(max_dec, 32, 128) for _ in range((kmax - 1) * L)]
-    ka = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
-    va = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
-    oa = [torch.empty_like(x) for x in qa]
+    if full:
+        weights = wl.block_weights(sh, ffn, L, gen)
+        xbuf = rnd(budget, d_model)
+        xa = [rnd(max_dec, d_model) for _ in range(kmax - 1)]
+    else:
+        qs = [rnd(budget, 32, 128) for _ in range(L)]
+        outs = [torch.empty_like(q) for q in qs]
+        qa = [rnd(max_dec, 32, 128) for _ in range((kmax - 1) * L)]
+        ka = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
+        va = [rnd(max_dec, 8, 128) for _ in range((kmax - 1) * L)]
+        oa = [torch.empty_like(x) for x in qa]
     arrivals, prompts, outputs = wl.trace_requests(1005)
-    modes = {"agg": 1, f"adaptive_50ms_k{kmax}": kmax, "adaptive_50ms_k1": 1}
+    modes = {"agg": ("agg", 1), "adaptive_50ms": ("adaptive", 1), f"adaptive_50ms_k{kmax}": ("adaptive", kmax)}
+    for p_ in (64, 128, 192):
+        modes[f"static_{p_}_{256 - p_}"] = ("static", p_)
     res = {}
-    ctx.set_profiling(2)
-    for mode, kcap in modes.items():
+    ctx.set_profiling(1 if full else 2)
+    for mode, (kind, arg) in modes.items():
+        kcap = arg if kind == "adaptive" else 1
         eng = duet.Engine(budget, pool, max_pages, shuffle_seed=1006)
         clock_us, nxt, it, recorded = 0.0, 0, 0, 0
         last_tok, gaps, lat, split_used, ks = {}, [], [], [], []
@@ -956,32 +821,42 @@ def serve_attn_main(args):
                 clock_us += 50000.0
                 continue
             rows3 = [(int(k_), int(q_), int(c_)) for k_, _, q_, c_ in meta]
-            if mode == "agg":
+            if kind == "agg":
                 sp = duet.CuSplit.agg()
+            elif kind == "static":
+                sp = duet.CuSplit.split(arg, duet.TOTAL_CUS - arg)
+            elif full:
+                sp = duet.choose_cu_split_model(rows3, tbt, sh, block, ctx.model, max_decode_steps=kcap)[0]
             else:
                 sp = duet.choose_cu_split(rows3, tbt, sh, ctx.model, max_decode_steps=kcap)[0]
             if n_dec > max_dec:
                 sp = duet.CuSplit.agg()
             k = sp.k_decode_steps if sp.mode == duet.SPLIT and n_dec else 1
+            if sp.mode == duet.SPLIT and k != sp.k_decode_steps:
+                sp = duet.CuSplit.split(sp.cus_prefill, sp.cus_decode)
             n_tok = int(meta[:, 2].sum())
             pt = torch.as_tensor(table, device="cuda")
-            q_l, o_l = [q[:n_tok] for q in qs], [o[:n_tok] for o in outs]
-            if k > 1:
-                sl = lambda xs: [xs[(s_ - 1) * L + l][:n_dec] for s_ in range(1, k) for l in range(L)]
-                ctx.attn_lookahead(q_l, sl(qa), sl(ka), sl(va), kcs, vcs, pt, meta, sp, outs=o_l,
-                                   outs_ahead=sl(oa))
+            if full:
+                ctx.block_forward(xbuf[:n_tok], weights, kcs, vcs, pt, meta, ffn, sp,
+                                  x_ahead=[x[:n_dec] for x in xa[:k - 1]] if k > 1 else None)
             else:
-                ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
+                q_l, o_l = [q[:n_tok] for q in qs], [o[:n_tok] for o in outs]
+                if k > 1:
+                    sl = lambda xs: [xs[(s_ - 1) * L + l][:n_dec] for s_ in range(1, k) for l in range(L)]
+                    ctx.attn_lookahead(q_l, sl(qa), sl(ka), sl(va), kcs, vcs, pt, meta, sp, outs=o_l,
+                                       outs_ahead=sl(oa))
+                else:
+                    ctx.attn_iteration(q_l, kcs, vcs, pt, meta, sp, outs=o_l)
             kt = ctx.last_kernel_times()
             it_us = kt["iteration_us"]
-            if sp.mode != duet.SPLIT:
+            dec_end = kt["decode_start_us"] + kt["decode_total_us"]
+            if sp.mode != duet.SPLIT or n_dec == 0:
                 t_tok = [it_us]                      # the tokens exist when the iteration ends
             elif k > 1:
                 first = kt["decode_start_us"] + kt["decode_first_step_us"]
-                t_tok = [first + s_ * (kt["decode_start_us"] + kt["decode_total_us"] - first) / (k - 1)
-                         for s_ in range(k)]         # step 0's end, then evenly to the decode half's end
+                t_tok = [first + s_ * (dec_end - first) / (k - 1) for s_ in range(k)]
             else:
-                t_tok = [kt["decode_start_us"] + kt["decode_total_us"]]
+                t_tok = [dec_end]
             n_new = 0
             for row in range(n_dec):
                 rid = int(ids[row])
@@ -1001,7 +876,7 @@ def serve_attn_main(args):
             it += 1
             recorded += 1
             if recorded % 50 == 0:
-                print(f"serve-attn {mode}: {recorded}/{args.trace_iters} iterations", file=sys.stderr, flush=True)
+                print(f"serve {mode}: {recorded}/{args.trace_iters} iterations", file=sys.stderr, flush=True)
         eng.close()
         g, a = np.array(gaps), np.array(lat)
         res[mode] = {"tbt_p50_us": round(float(np.percentile(g, 50)), 1),
@@ -1015,14 +890,15 @@ def serve_attn_main(args):
                      "k_max_used": int(max(ks)), "decode_gaps": int(len(g))}
     ctx.set_profiling(0)
     k_mode = f"adaptive_50ms_k{kmax}"
-    line = {"metric": "serving-loop TBT p99, attention share, with look-ahead (us)",
+    what = f"{L} llama3-8b blocks (random-init weights, FFN {ffn})" if full else f"{L} llama3-8b attention layers"
+    line = {"metric": f"serving-loop TBT p99, {'full model' if full else 'attention share'}, adaptive with look-ahead (us)",
             "value": res[k_mode]["tbt_p99_us"], "unit": "us", "n_gpus": 1, "higher_is_better": False,
             "dtype": "bf16", "data": "synthetic",
             "config": {"workload": f"serving loop: native engine, {args.trace_iters} iterations after 200 warm-up, "
                                    "Poisson 4 req/s, prompts LogN(mean 4096, sigma 1.0) <= 32768, outputs LogN(mean 256, "
-                                   f"sigma 0.7), budget {budget}, {L} llama3-8b attention layers, KV pages persistent per "
-                                   f"request, TBT bound {tbt / 1000:.0f} ms, look-ahead up to {kmax} decode steps; closed "
-                                   "loop on each iteration's fork-to-join time"},
+                                   f"sigma 0.7), budget {budget}, {what}, KV pages persistent per request, TBT bound "
+                                   f"{tbt / 1000:.0f} ms, look-ahead up to {kmax} decode steps; closed loop on each "
+                                   "iteration's fork-to-join time"},
             "modes": res,
             "tbt_p99_vs_agg": round(res[k_mode]["tbt_p99_us"] / res["agg"]["tbt_p99_us"], 4),
             "throughput_vs_agg": round(res[k_mode]["tokens_per_s"] / res["agg"]["tokens_per_s"], 4)}
@@ -1204,14 +1080,14 @@ def main():
     ap.add_argument("--lookahead", action="store_true",
                     help="run look-ahead decode (k decode steps per prefill step) on the prefill-heavy Llama-3-70B "
                          "batch instead")
-    ap.add_argument("--max-k", type=int, default=64, help="cap on Algorithm 1's k for --lookahead")
+    ap.add_argument("--max-k", type=int, default=64, help="cap on Algorithm 1's k for --lookahead and --serve")
     ap.add_argument("--serve", action="store_true",
                     help="run the serving loop: the native engine forms the trace's iterations over whole blocks, "
                          "aggregated vs adaptive vs static splits")
     ap.add_argument("--accuracy", action="store_true",
                     help="the latency model's predicted vs measured latency per CU share (Appendix A batches)")
     ap.add_argument("--attn-only", action="store_true",
-                    help="--serve: the attention share only, with look-ahead decode steps up to --max-k")
+                    help="--serve: the attention share only (default: whole blocks)")
     ap.add_argument("--block-k", type=int, default=1,
                     help="with --block: decode steps per call (look-ahead), split 160/96 vs aggregated")
     ap.add_argument("--block", action="store_true",
@@ -1237,8 +1113,6 @@ def main():
         return lookahead_main(args)
     if args.accuracy:
         return accuracy_main(args)
-    if args.serve and args.attn_only:
-        return serve_attn_main(args)
     if args.serve:
         return serve_main(args)
     if args.block:
