@@ -223,3 +223,76 @@ def test_lookahead_profiling_reports_steps(ctx):
         assert (t["prefill_us"] > 0) == (level == 2)
         for x, y in zip(dev.outs + dev.outs_a + dev.kcs + dev.vcs, ref.outs + ref.outs_a + ref.kcs + ref.vcs):
             assert _same_bits(x, y)
+
+
+def test_engine_driven_lookahead_iterations_carry_the_cache(ctx):
+    """Iterations formed by the serving engine with look-ahead steps (duet_engine_step_lookahead:
+    pages for k tokens of every decode), run as duet_attn_lookahead calls: each scheduled token's
+    key and value are written into the paged caches (the QKV split's job, done here identically on
+    the GPU and in the oracle's fp64 copy), the look-ahead steps write theirs, and the next
+    iteration's decodes attend over all of them.  Every step's outputs against the oracle, and the
+    caches bit for bit after every iteration."""
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from oracle import attention as oa
+    sh = wl.AttnShape(4, 2, 128, "bf16")
+    pool, max_pages, k = 64, 16, 3
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(4201)
+    bf = lambda *s_: (torch.randn(*s_, generator=gen) * 0.1).to(torch.bfloat16)
+    kc, vc = bf(pool, 2, 16, 128), bf(pool, 2, 128, 16)
+    kcg, vcg = kc.cuda(), vc.cuda()
+    k64, v64 = to64(kc), to64(vc)
+    eng = duet.Engine(48, pool, max_pages, shuffle_seed=5)
+    eng.add_request(70, 14)
+    eng.add_request(20, 11)
+    n_la = n_split = 0
+    for it in range(16):
+        if it == 2:
+            eng.add_request(30, 7)
+        if it == 4:
+            eng.add_request(120, 3)  # three chunked-prefill steps beside running decodes
+        meta, table, ids = eng.step(decode_steps=k)
+        if not len(meta):
+            break
+        n_dec = int((meta[:, 0] == 1).sum())
+        n_tok = int(meta[:, 2].sum())
+        # the scheduled tokens' keys and values, into both caches
+        kn, vn = bf(n_tok, 2, 128), bf(n_tok, 2, 128)
+        for r in range(len(meta)):
+            for t in range(int(meta[r, 2])):
+                pos, row = int(meta[r, 3]) + t, int(meta[r, 1]) + t
+                oa.append_token(k64, v64, table[r], pos, to64(kn[row]), to64(vn[row]), 16)
+                page, slot = int(table[r][pos // 16]), pos % 16
+                kcg[page, :, slot, :] = kn[row].cuda()
+                vcg[page, :, :, slot] = vn[row].cuda()
+        q = bf(n_tok, 4, 128)
+        kk = k if n_dec else 1
+        both = (meta[:, 0] == 0).any() and n_dec
+        sp = duet.CuSplit.split(128, 128, kk) if both else duet.CuSplit.agg(kk)
+        n_split += bool(both)
+        pt = torch.as_tensor(table, device="cuda")
+        qa, ka, va = ([bf(n_dec, h, 128) for _ in range(kk - 1)] for h in (4, 2, 2))
+        if kk > 1:
+            outs, outs_a = ctx.attn_lookahead([q.cuda()], [x.cuda() for x in qa], [x.cuda() for x in ka],
+                                              [x.cuda() for x in va], [kcg], [vcg], pt, meta, sp, check_errors=True)
+            n_la += 1
+        else:
+            outs, outs_a = ctx.attn_iteration([q.cuda()], [kcg], [vcg], pt, meta, sp, check_errors=True), []
+        torch.cuda.synchronize()
+        want0 = oa.mixed_batch(to64(q), k64, v64, table, meta, 16)
+        got = [(to64(outs[0]), want0)]
+        if kk > 1:
+            wa, k64, v64 = oa.lookahead_decode([to64(x) for x in qa], [to64(x) for x in ka], [to64(x) for x in va],
+                                               k64, v64, table, meta, kk)
+            got += [(to64(o), w) for o, w in zip(outs_a, wa)]
+        for s, (g, w) in enumerate(got):
+            e = np.abs(g - w)
+            print(f"[engine look-ahead] iteration {it} step {s}: rows={len(meta)} decodes={n_dec} {sp} "
+                  f"max_abs={e.max():.3e}", flush=True)
+            assert e.max() <= BF16_MAX_ABS and e.mean() <= BF16_MEAN_ABS
+        assert np.array_equal(to64(kcg), k64) and np.array_equal(to64(vcg), v64), f"caches after iteration {it}"
+        eng.complete(decode_steps_run=kk)
+    assert eng.stats() == (0, 0, pool)
+    eng.close()
+    assert n_la >= 5 and n_split >= 3
