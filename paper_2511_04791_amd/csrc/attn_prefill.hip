@@ -58,6 +58,20 @@ __device__ __forceinline__ void load_lds16(const char* src, __bf16* lds_block) {
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 __device__ __forceinline__ bool page_ok(int id, long long num_phys) { return id >= 0 && (long long)id < num_phys; }
 
+// Max and sum of a value over lanes l and l ^ 32, by the half-wave swap permute (a vector-ALU op;
+// an LDS permute would wait behind the fragment reads in flight).  The swap returns the lane's own
+// value and its partner's, in an order that depends on the half; both combinations are symmetric.
+__device__ __forceinline__ float pair_max(float x) {
+  const unsigned u = __float_as_uint(x);
+  auto s = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const unsigned u = __float_as_uint(x);
+  auto s = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
 // A-operand row rho of a 32-row MFMA tile carries key swap_bits23(rho): within each group of 16,
 // bits 2 and 3 are exchanged, so output register v of lane l holds key 16 (v / 8) + 8 (l / 32) + v % 8.
 __device__ __forceinline__ int swap_bits23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
@@ -146,7 +160,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
   int* ids = reinterpret_cast<int*>(reinterpret_cast<char*>(lds) + PrefillSmem<D>::kTileBytes);
   const int id0 = (BN / 16) * kt0;
   const int n_used_pages = min(n_pages, (kt1 * BN + 15) >> 4) - id0;
-  for (int i = tid; i < n_used_pages; i += kThreads) ids[i] = prow[id0 + i];
+  // Ids are checked here, once: a missing page is recorded and replaced by page 0 (its keys lie
+  // past the end, or the request is flagged).
+  for (int i = tid; i < n_used_pages; i += kThreads) {
+    const int id = prow[id0 + i];
+    const bool ok = page_ok(id, a.num_phys_pages);
+    bad |= !ok;
+    ids[i] = ok ? id : 0;
+  }
   __syncthreads();
 
   // Tiles arrive by direct global-to-LDS loads (16 bytes per lane; lane i of a wave writes bytes
@@ -170,26 +191,31 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     v_pi[i] = vc >> 1;
     v_off[i] = vrow * 32 + (vc & 1) * 16;
   }
+  // Per-lane parts of the tile addresses.  A K block lies inside one page (uniform over the wave),
+  // so its address is a scalar page base plus the lane's 32-bit offset; a V^T block spans the
+  // tile's pages, so each lane adds its page's slab to a 64-bit base.  Pages past the request's
+  // end (only in its last tile) re-read its last page: their keys are masked and their values
+  // zeroed before use.
+  const size_t page_stride = (size_t)a.h_kv * kSlab;
+  const char* kbase_j = kbase + (size_t)j * kSlab;
+  const char* vlane[BPW];
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) vlane[i] = vbase + (size_t)j * kSlab + v_off[i];
+  const int last_page = n_pages - 1 - id0;
   auto issue_tile = [&](int kt) {
     __bf16* kdst = lds + (kt % kStages) * PrefillSmem<D>::kStageElems;
     __bf16* vdst = kdst + BN * D;
+    int kid[BPW], vid[BPW];  // all ids first: one LDS wait for the tile
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      kid[i] = ids[min(4 * kt + k_pi[i] - id0, last_page)];
+      vid[i] = ids[min(4 * kt + v_pi[i] - id0, last_page)];
+    }
 #pragma unroll
     for (int i = 0; i < BPW; ++i) {
       const int blk = wave + kWaves * i;
-      int lp = 4 * kt + k_pi[i];
-      bool in_range = lp < n_pages;
-      int id = in_range ? ids[min(lp, n_pages - 1) - id0] : 0;  // the LDS read stays inside the table
-      bool ok = in_range && page_ok(id, a.num_phys_pages);
-      bad |= in_range & !ok;
-      // A missing page reads page 0: its keys lie past the end (masked) or the request is
-      // already flagged; values past the end are zeroed once the last tile has landed.
-      load_lds16(kbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + k_off[i], kdst + blk * 512);
-      lp = 4 * kt + v_pi[i];
-      in_range = lp < n_pages;
-      id = in_range ? ids[min(lp, n_pages - 1) - id0] : 0;
-      ok = in_range && page_ok(id, a.num_phys_pages);
-      bad |= in_range & !ok;
-      load_lds16(vbase + ((size_t)(ok ? id : 0) * a.h_kv + j) * kSlab + v_off[i], vdst + blk * 512);
+      load_lds16(kbase_j + (size_t)uniform(kid[i]) * page_stride + k_off[i], kdst + blk * 512);
+      load_lds16(vlane[i] + (size_t)(unsigned)vid[i] * page_stride, vdst + blk * 512);
     }
   };
   // Waits until this wave's loads of all but the `later` most recent tiles have landed
@@ -318,7 +344,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[nb][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32)) * a.scale_log2;
+      mx = pair_max(mx) * a.scale_log2;
       // Move the reference max only when some score exceeds it by more than the slack.
       if (__any(mx > m_ref + kRescaleSlack)) {
         const float m_new = fmaxf(m_ref, mx);
@@ -437,7 +463,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
       }
     }
   }
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = pair_sum(l_run);
   if (row_ok) {
     const float inv = 1.0f / l_tot;
     __bf16* op = reinterpret_cast<__bf16*>(a.out) + ((size_t)(q_start + qi) * a.h_q + h) * D + 4 * hh;
