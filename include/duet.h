@@ -491,8 +491,9 @@ int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* ba
  * Steps run in order, so step s reads the tokens steps 1 .. s - 1 wrote.  Every decode request's
  * page_table row must hold pages for cached_len + k tokens; the slots written must not be read
  * by any other request of the batch (the prefill half runs at the same time).
- * SPLIT / CONCURRENT: every decode step is enqueued (decode first) on the decode stream, then the
- * prefill layers on the prefill stream; one fork and one join on `stream`.  AGG: decode step 0,
+ * SPLIT / CONCURRENT: the first prefill layer is enqueued on the prefill stream, then every decode
+ * step on the decode stream, then the other prefill layers; one fork and one join on `stream`.
+ * AGG: decode step 0,
  * then the prefill layers, then decode steps 1 .. k - 1, on `stream`.
  * Decode steps run from graphs by default: the kernels of the steps that run back to back (all k
  * steps with SPLIT / CONCURRENT; step 0, then steps 1 .. k - 1, with AGG; one step per graph

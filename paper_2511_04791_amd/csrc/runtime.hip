@@ -793,9 +793,9 @@ int run_decode_step(duet_ctx* ctx, const std::vector<DecodeLaunch>& launches, hi
 
 // Look-ahead decode (Section 4.3): the prefill half once over all layers and the decode half for
 // k = split.k_decode_steps steps, step s >= 1 writing its token before attending.  SPLIT and
-// CONCURRENT enqueue every decode step first (one graph per step) on the decode stream, then the
-// prefill kernels one by one on the prefill stream; AGG runs decode step 0, the prefill layers
-// and decode steps 1 .. k - 1 in that order on the caller's stream.
+// CONCURRENT enqueue the first prefill layer, every decode step (one graph) on the decode stream,
+// then the other prefill layers; AGG runs decode step 0, the prefill layers and decode steps
+// 1 .. k - 1 in that order on the caller's stream.
 int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_l, const void* const* q_ahead,
                    const void* const* k_ahead, const void* const* v_ahead, void* const* kc_l, void* const* vc_l,
                    int64_t num_phys_pages, const int32_t* page_table, int32_t max_pages_per_req,
@@ -921,8 +921,8 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
     }
     return DUET_OK;
   };
-  auto prefill_layers = [&]() -> int {
-    for (int l = 0; l < layers; ++l) {
+  auto prefill_layers = [&](int l0, int l1) -> int {
+    for (int l = l0; l < l1; ++l) {
       AttnArgs al = a;
       al.q = q_l[l];
       al.k_cache = kc_l[l];
@@ -936,12 +936,16 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
   };
   if (has_decode && prof_iter) HIP_TRY(hipEventRecord(ctx->ev_step[0], forked ? sd : order));
   if (forked) {
-    // decode first: all k steps are enqueued before any prefill kernel
+    // The first prefill layer is enqueued, then every decode step, then the other prefill layers:
+    // the prefill stream starts at once (enqueueing the k steps first would hold it back by their
+    // host-side launch time, up to a millisecond with one graph per step), and the decode
+    // partition waits for one kernel launch only.
+    if (has_prefill && (rc = prefill_layers(0, 1))) return rc;
     if (has_decode && (rc = decode_steps(0, k))) return rc;
-    if (has_prefill && (rc = prefill_layers())) return rc;
+    if (has_prefill && (rc = prefill_layers(1, layers))) return rc;
   } else {
     if (has_decode && (rc = decode_steps(0, 1))) return rc;
-    if (has_prefill && (rc = prefill_layers())) return rc;
+    if (has_prefill && (rc = prefill_layers(0, layers))) return rc;
     if (has_decode && k > 1 && (rc = decode_steps(1, k))) return rc;
   }
   if (forked) {

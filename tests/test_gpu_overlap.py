@@ -30,14 +30,19 @@ def _times(ctx, split, layers=8):
     pt = torch.as_tensor(b.page_table, device="cuda")
     outs = [torch.empty_like(q) for _ in range(layers)]
     ctx.set_profiling(2)
+    best = None
     try:
-        for _ in range(3):
+        # The fastest of several calls: a rare stall of the whole call before its first kernel
+        # (seen once, 3.5 ms, at the upload) says nothing about whether the halves overlap.
+        for _ in range(5):
             ctx.attn_iteration([q] * layers, [kc] * layers, [vc] * layers, pt, b.seq_meta, split, outs=outs)
-        t = ctx.last_kernel_times()
+            t = ctx.last_kernel_times()
+            if best is None or t["iteration_us"] < best["iteration_us"]:
+                best = t
     finally:
         ctx.set_profiling(0)
     torch.cuda.synchronize()
-    return t
+    return best
 
 
 def test_split_halves_overlap_in_time(ctx):
