@@ -1,6 +1,7 @@
 """Turn rocprofv3 CSV output into the short summaries kept with the sources.
 
-    python -m paper_2511_04791_amd.profsum stats  <run_kernel_stats.csv>  --command "..."  > summary.md
+    python -m paper_2511_04791_amd.profsum stats  <run_kernel_stats.csv>  --command "..." \
+        [--trace <run_kernel_trace.csv>]  > summary.md
     python -m paper_2511_04791_amd.profsum traffic --fetch <counter_collection.csv> \
         --write <counter_collection.csv> --command "..." --tag WORKLOAD --out-dir profiles
     python -m paper_2511_04791_amd.profsum counters <counter_collection.csv> [...] \
@@ -44,7 +45,21 @@ def source_hash(name: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def stats_markdown(path: str, command: str, top: int = 12) -> str:
+def warm_durations(trace_path: str, skip: int = 2) -> dict:
+    """kernel (as named in the summaries) -> durations in us of its dispatches in start order,
+    from a kernel trace, without the first `skip` (cold: first use of the code, caches, clocks)."""
+    with open(trace_path, newline="") as f:
+        rows = list(csv.DictReader(f))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    out = {}
+    for r in rows:
+        for kernel, (needle, _) in KERNELS.items():
+            if needle in r["Kernel_Name"]:
+                out.setdefault(kernel, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    return {k: v[skip:] for k, v in out.items() if len(v) > skip}
+
+
+def stats_markdown(path: str, command: str, top: int = 12, trace: str | None = None, skip: int = 2) -> str:
     with open(path, newline="") as f:
         rows = list(csv.DictReader(f))
     rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
@@ -57,6 +72,12 @@ def stats_markdown(path: str, command: str, top: int = 12) -> str:
         out.append(f"| `{name}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                    f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    if trace:
+        warm = warm_durations(trace, skip)
+        out += ["", f"Attention kernels without the first {skip} (cold) dispatches of each, from the same run's "
+                "kernel trace:", "", "| kernel | dispatches | avg us | median us | min us |", "|---|---:|---:|---:|---:|"]
+        for k, v in warm.items():
+            out.append(f"| `{k}` | {len(v)} | {statistics.fmean(v):.2f} | {statistics.median(v):.2f} | {min(v):.2f} |")
     return "\n".join(out) + "\n"
 
 
@@ -180,6 +201,7 @@ def main(argv=None) -> None:
     s = sub.add_parser("stats")
     s.add_argument("csv")
     s.add_argument("--command", required=True)
+    s.add_argument("--trace", default=None, help="the run's kernel trace: adds warm per-kernel averages")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -192,7 +214,7 @@ def main(argv=None) -> None:
     c.add_argument("--title", default="rocprofv3 counters per attention kernel")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
-        sys.stdout.write(stats_markdown(a.csv, a.command))
+        sys.stdout.write(stats_markdown(a.csv, a.command, trace=a.trace))
     elif a.cmd == "traffic":
         traffic(a.fetch, a.write, a.command, a.out_dir, a.tag)
     else:
