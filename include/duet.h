@@ -496,8 +496,8 @@ int duet_lookahead_workspace_bytes(const duet_shape* shape, const duet_batch* ba
  * AGG: decode step 0,
  * then the prefill layers, then decode steps 1 .. k - 1, on `stream`.
  * Decode steps run from graphs by default: the kernels of the steps that run back to back (all k
- * steps with SPLIT / CONCURRENT; step 0, then steps 1 .. k - 1, with AGG; one step per graph
- * while profiling is on, so events can mark each step's end) are captured on first use, and the
+ * steps with SPLIT / CONCURRENT; step 0, then steps 1 .. k - 1, with AGG and while profiling is
+ * on, so that an event can mark when step 0's tokens are ready) are captured on first use, and the
  * graph is replayed on later calls whose launch arguments (pointers, work-list sizes, CU share)
  * are the same; at most 128 graphs are kept per context (least recently used evicted, after a
  * device synchronisation).  Outputs and cache writes are bit-identical with graphs on or off,

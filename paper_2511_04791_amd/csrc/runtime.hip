@@ -905,13 +905,14 @@ int attn_lookahead(duet_ctx* ctx, const duet_shape* shape, const void* const* q_
       launches.push_back(dl);
     }
   };
-  // Enqueues decode steps first .. last - 1 on the decode stream.  Unprofiled, they form one
-  // graph (one launch for the whole run of steps); profiled, each step is its own graph, so an
-  // event can mark its end.
+  // Enqueues decode steps first .. last - 1 on the decode stream as one graph (one launch for the
+  // whole run of steps).  Profiled, step 0 is a graph of its own, so that an event marks when its
+  // tokens are ready; the other steps still run as one graph, as they do unprofiled (one graph per
+  // step would add the launch gaps between graphs to every step it measures).
   auto decode_steps = [&](int first, int last) -> int {
     hipStream_t ds = forked ? sd : order;
     for (int st = first; st < last;) {
-      const int end = prof_iter ? st + 1 : last;
+      const int end = prof_iter && st == 0 ? 1 : last;
       launches.clear();
       for (int x = st; x < end; ++x) add_step(x);
       int r2 = run_decode_step(ctx, launches, ds);
@@ -1602,7 +1603,7 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out) {
   out->layers = L;
   int rc;
   if (ctx->prof_steps > 0) {
-    // look-ahead call: decode steps are graphs, timed step by step on the decode stream
+    // look-ahead call: the decode partition's start, the end of step 0 and the end of its last step
     const int k = ctx->prof_steps;
     out->decode_steps = k;
     if (ctx->prof_decode) {
