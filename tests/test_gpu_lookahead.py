@@ -205,7 +205,8 @@ def test_lookahead_bad_slot_page_is_reported_not_written(ctx):
 
 
 def test_lookahead_profiling_reports_steps(ctx):
-    """Profiled calls run one graph per step (events between steps) and compute the same bits."""
+    """Profiled calls (step 0 and steps 1 .. k - 1 as two graphs, events around them) compute the
+    same bits and report the partitions' spans."""
     import paper_2511_04791_amd as duet
     k = 4
     b, layers = _bf16_case(k, L=2)
@@ -224,6 +225,26 @@ def test_lookahead_profiling_reports_steps(ctx):
         for x, y in zip(dev.outs + dev.outs_a + dev.kcs + dev.vcs, ref.outs + ref.outs_a + ref.kcs + ref.vcs):
             assert _same_bits(x, y)
 
+
+
+def test_lookahead_prefill_starts_with_the_fork(ctx):
+    """Under a split the prefill partition starts right after the fork: its first layer is enqueued
+    before the decode steps, whose host-side launches would otherwise hold it back."""
+    import paper_2511_04791_amd as duet
+    k = 16
+    b, layers = _bf16_case(k, L=4)
+    dev = _Dev(b, layers, k)
+    _call(ctx, b, dev, duet.CuSplit.split(128, 128, k))
+    ctx.set_profiling(2)  # level 2: per-kernel events on the prefill stream as well
+    starts = []
+    for _ in range(3):
+        _call(ctx, b, dev, duet.CuSplit.split(128, 128, k))
+        t = ctx.last_kernel_times()
+        starts.append((t["prefill_start_us"], t["decode_start_us"], t["decode_total_us"]))
+    ctx.set_profiling(0)
+    print(f"[look-ahead] (prefill start, decode start, decode span) us: {starts}", flush=True)
+    p0, d0, _ = min(starts)
+    assert p0 <= d0 + 100.0  # the prefill does not wait for the decode steps' launches
 
 def test_engine_driven_lookahead_iterations_carry_the_cache(ctx):
     """Iterations formed by the serving engine with look-ahead steps (duet_engine_step_lookahead:
