@@ -224,12 +224,13 @@ __global__ __launch_bounds__(256, 1) void decode_partial_bf16(AttnArgs a, WorkAr
     n_staged = 0;
   };
 
-  // Wave v of the grid starts with items v and n_waves + v; the items past those are dealt
-  // round-robin to n_queues counters (one atomic per item on a single counter would saturate it),
-  // and wave v takes them from counter v % n_queues: ticket t is item 2 n_waves + t n_queues + c.
-  // Every queue has a wave (n_waves >= n_queues), and a wave's tickets rise, as do their items,
-  // all of them above the static ones: when a wave stops at an item past the end, every ticket it
-  // still holds is past the end too.
+  // Wave v of the grid starts with item v; every item past the first n_waves is dealt round-robin
+  // to n_queues counters (one atomic per item on a single counter would saturate it), and wave v
+  // takes them from counter v % n_queues: ticket t is item n_waves + t n_queues + c.  Only one
+  // item per wave is static, so from its second item on a wave that streams more slowly takes
+  // fewer.  Every queue has a wave (n_waves >= n_queues), and a wave's tickets rise, as do their
+  // items, all of them above the static ones: when a wave stops at an item past the end, every
+  // ticket it still holds is past the end too.
   const int n_waves = gridDim.x * (blockDim.x >> 6);
   const int n_queues = n_waves >= kDecodeQueues ? kDecodeQueues : 1;
   const int first = blockIdx.x * (blockDim.x >> 6) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -307,7 +308,12 @@ __global__ __launch_bounds__(256, 1) void decode_partial_bf16(AttnArgs a, WorkAr
     return;
   }
   DItem cur = unpack_item(sload4(w.ditems + first), true);
-  DItem nxt = unpack_item(sload4(w.ditems + min(first + n_waves, n_items - 1)), first + n_waves < n_items);
+  // The second item's ticket: its atomic returns while the first item's data loads.
+  DItem nxt;
+  {
+    const int idx = n_waves + __builtin_amdgcn_readfirstlane(grab()) * n_queues + queue;
+    nxt = desc_item(load_desc(idx), idx);
+  }
   int cur_ids;
   bf16x8 qf[D / 32];
   fetch_lane_data(cur, cur_ids, qf);
@@ -402,7 +408,7 @@ __global__ __launch_bounds__(256, 1) void decode_partial_bf16(AttnArgs a, WorkAr
         }
         if constexpr (kLast) {
           if (u == 0) {
-            nn_idx = 2 * n_waves + __builtin_amdgcn_readfirstlane(ticket) * n_queues + queue;
+            nn_idx = n_waves + __builtin_amdgcn_readfirstlane(ticket) * n_queues + queue;
             nn_words = load_desc(nn_idx);
           }
         }
