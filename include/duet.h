@@ -545,7 +545,9 @@ int duet_last_kernel_times(duet_ctx* ctx, duet_kernel_times* out);
  * (256 = the unrestricted stream); repeated `iters` times.  Returns achieved bytes/s. */
 int duet_probe_read_bw(duet_ctx* ctx, int32_t cus, const void* buf, size_t bytes, int32_t iters,
                        double* bytes_per_s);
-/* Register-resident bf16 MFMA loop on `cus` CUs.  Returns achieved FLOP/s. */
+/* Register-resident bf16 MFMA loop (16x16x32, four independent chains, two waves per SIMD) on
+ * `cus` CUs; `iters` trips of 32 MFMAs per wave (8192 keeps a full-chip launch long enough that
+ * dispatch and ramp stay out of the figure).  Returns achieved FLOP/s. */
 int duet_probe_mfma(duet_ctx* ctx, int32_t cus, int32_t iters, double* flops_per_s);
 /* Record the hardware placement of `blocks` workgroups launched on the stream restricted to
  * `cus` CUs taken from the low end (high_end == 0, the decode side) or the high end (1, the

@@ -661,7 +661,7 @@ class Context:
                                            ctypes.byref(v)), "duet_probe_read_bw")
         return v.value
 
-    def probe_mfma(self, cus: int, iters: int = 2048) -> float:
+    def probe_mfma(self, cus: int, iters: int = 8192) -> float:
         v = ctypes.c_double()
         N.check(N.lib().duet_probe_mfma(self.handle, cus, iters, ctypes.byref(v)), "duet_probe_mfma")
         return v.value

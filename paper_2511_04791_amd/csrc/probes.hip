@@ -8,7 +8,9 @@
 // and compute throughput are profiled once per partition size):
 //   read probe  -- every thread streams 16-byte loads over a buffer larger than the last-level
 //                  cache and folds them into a checksum;
-//   MFMA probe  -- independent chains of 32x32x16 bf16 MFMAs on register operands;
+//   MFMA probe  -- independent chains of 16x16x32 bf16 MFMAs on register operands, two waves per
+//                  SIMD (on this part that instruction reaches about 98% of the nominal rate,
+//                  the 32x32x16 one about 80%, so this is the share's ceiling);
 //   placement   -- each workgroup records the XCC_ID and HW_ID hardware registers, which tell
 //                  on which XCD / shader engine / CU it ran, to check a stream's CU mask.
 #include <hip/hip_runtime.h>
@@ -19,7 +21,7 @@ namespace duet {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <typename T>
 __global__ __launch_bounds__(256) void gather_kernel(const T* cache, int which, int h_kv, int d,
@@ -58,7 +60,9 @@ __global__ __launch_bounds__(256) void read_probe_kernel(const uint4* buf, size_
   if (acc == 0x9e3779b9u) sink[0] = acc;  // keeps the loads alive; practically never stores
 }
 
-__global__ __launch_bounds__(256) void mfma_probe_kernel(int iters, float* sink) {
+// One workgroup of 8 waves per CU (two per SIMD); each loop trip issues 32 MFMAs over the four
+// chains, so loop overhead stays out of the measurement.
+__global__ __launch_bounds__(512, 1) void mfma_probe_kernel(int iters, float* sink) {
   const int lane = threadIdx.x & 63;
   bf16x8 a, b;
 #pragma unroll
@@ -66,16 +70,19 @@ __global__ __launch_bounds__(256) void mfma_probe_kernel(int iters, float* sink)
     a[e] = static_cast<__bf16>(0.001f * (lane + e));
     b[e] = static_cast<__bf16>(0.002f * (lane - e));
   }
-  f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  f32x4 c0 = {}, c1 = {}, c2 = {}, c3 = {};
   for (int i = 0; i < iters; ++i) {
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c1, 0, 0, 0);
+      c2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c2, 0, 0, 0);
+      c3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c3, 0, 0, 0);
+    }
   }
   float s = 0.f;
 #pragma unroll
-  for (int v = 0; v < 16; ++v) s += c0[v] + c1[v] + c2[v] + c3[v];
+  for (int v = 0; v < 4; ++v) s += c0[v] + c1[v] + c2[v] + c3[v];
   if (s == 1234.5f) sink[0] = s;  // keeps the chains alive
 }
 
@@ -125,7 +132,7 @@ hipError_t launch_read_probe(const void* buf, size_t bytes, int blocks, unsigned
 }
 
 hipError_t launch_mfma_probe(int blocks, int iters, float* sink, hipStream_t s) {
-  hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(256), 0, s, iters, sink);
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(512), 0, s, iters, sink);
   return hipGetLastError();
 }
 

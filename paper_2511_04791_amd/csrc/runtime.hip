@@ -1693,16 +1693,17 @@ int duet_probe_mfma(duet_ctx* ctx, int32_t cus, int32_t iters, double* flops_per
   hipStream_t st;
   int rc = get_stream(ctx, cus, 0, &st);
   if (rc) return rc;
-  const int blocks = cus * 2;  // 8 waves per CU, two per SIMD
+  const int blocks = cus;  // one 8-wave workgroup per CU, two waves per SIMD
   float* sink = reinterpret_cast<float*>(ctx->dev_sink);
-  // Clocks settle under sustained matrix load: warm up with four launches, then keep the best of
-  // three timed launches.
+  // Clocks settle under sustained matrix load and drop in idle gaps: warm up with four launches,
+  // then time three back-to-back launches per sample (no host wait between them) and keep the
+  // best of three samples.
   for (int i = 0; i < 4; ++i) HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
   double best = 0.0;
-  const double flops = (double)blocks * 4 /*waves*/ * iters * 4 /*chains*/ * (32.0 * 32 * 16 * 2);
+  const double flops = 3.0 * blocks * 8 /*waves*/ * iters * 32 /*MFMAs per trip*/ * (16.0 * 16 * 32 * 2);
   for (int rep = 0; rep < 3; ++rep) {
     HIP_TRY(hipEventRecord(ctx->prof[kEvA], st));
-    HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
+    for (int l = 0; l < 3; ++l) HIP_TRY(launch_mfma_probe(blocks, iters, sink, st));
     HIP_TRY(hipEventRecord(ctx->prof[kEvB], st));
     HIP_TRY(hipEventSynchronize(ctx->prof[kEvB]));
     float ms = 0.f;

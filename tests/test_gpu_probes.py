@@ -53,3 +53,6 @@ def test_read_and_mfma_probes_are_sane(ctx):
           f"mfma {fl_full/1e12:.0f} TF (256) {fl_64/1e12:.0f} TF (64)", flush=True)
     assert 1e12 < bw_full < 8.5e12 and bw_64 <= bw_full * 1.05
     assert 2e14 < fl_full < 2.7e15 and fl_64 < fl_full
+    # The MFMA probe is a ceiling, not a kernel figure: it reaches 96-98% of the nominal 2.5 PFLOP/s
+    # (pro rata per CU) on this part; the bounds leave room for box-to-box clock differences.
+    assert fl_full > 0.85 * 2.5e15 and fl_64 > 0.88 * 2.5e15 * 64 / 256
