@@ -102,9 +102,16 @@ int prefill_rows_per_unit(int group, int dtype);
 // on the batch only, never on the CU split, so results are the same for every split.  Each piece
 // writes its partial state to a slot; the piece that finishes last (an arrival counter per unit)
 // merges the slots in piece order and writes the output.  Split units number at most
-// T / P <= kPrefillPieceFill and their slots at most 2 T / P.
+// T / P <= kPrefillPieceFill and their slots at most 2 T / P, plus the tail split's below
+// (kPrefillPieceFill units, kPrefillTailPieces slots each).
 constexpr int kPrefillPieceMinTiles = 8;
 constexpr int kPrefillPieceFill = 256;
+// Tail split (batch-only as well): when the whole units number at least 2 kPrefillPieceFill, the
+// kPrefillPieceFill shortest of them (dispatched last) run as kPrefillTailPieces pieces, each of
+// at least kPrefillTailMinTiles tiles, so the last round of workgroups is fine-grained on any share
+// (one workgroup per CU leaves up to one unit's length idle at the end otherwise).
+constexpr int kPrefillTailPieces = 4;
+constexpr int kPrefillTailMinTiles = 16;
 constexpr int kPrefillPieceBits = 12;  // piece index field of an item's w (pieces <= 4095)
 int prefill_piece_tiles_for(long long total_tiles);
 size_t prefill_slot_bytes(int head_dim);  // one piece's partial state

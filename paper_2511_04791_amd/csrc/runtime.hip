@@ -186,6 +186,41 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
   }
   const int P = bf16 && total_tiles > 0 ? prefill_piece_tiles_for(total_tiles) : 0;
   p->prefill_piece_tiles = P;
+  // Units longer than 1.5 P: n pieces of equal length (the last may be shorter), none empty.
+  auto pieces_of = [&](int nt) { return P > 0 && 2 * nt > 3 * P ? (nt + P - 1) / P : 1; };
+  // Tail split: when the whole units (those the rule above leaves in one piece) number more than
+  // two rounds of one workgroup per CU of the whole chip, the shortest round of them -- the last
+  // dispatched -- runs as kPrefillTailPieces pieces each (of at least kPrefillTailMinTiles
+  // tiles), so the final round is fine-grained on any CU share.  It depends on the batch only.
+  std::vector<std::pair<int, int>> tail_blocks;  // (request, row block), sorted
+  if (bf16 && P > 0) {
+    struct Whole {
+      int nt, r, t;
+    };
+    std::vector<Whole> whole;
+    int64_t n_whole_units = 0;
+    for (int r = 0; r < b->num_reqs; ++r) {
+      const duet_seq_meta& q = b->reqs[r];
+      if (q.kind != DUET_KIND_PREFILL) continue;
+      for (int t = 0; t * rows < q.q_len; ++t) {
+        const int nt = block_tiles(q, t);
+        if (pieces_of(nt) == 1) {
+          whole.push_back({nt, r, t});
+          n_whole_units += units;
+        }
+      }
+    }
+    if (n_whole_units >= 2 * kPrefillPieceFill) {
+      std::stable_sort(whole.begin(), whole.end(), [](const Whole& x, const Whole& y) { return x.nt < y.nt; });
+      int64_t taken = 0;
+      for (const Whole& w : whole) {
+        if (taken >= kPrefillPieceFill) break;
+        if (w.nt >= kPrefillTailPieces * kPrefillTailMinTiles) tail_blocks.emplace_back(w.r, w.t);
+        taken += units;
+      }
+      std::sort(tail_blocks.begin(), tail_blocks.end());
+    }
+  }
   int64_t n_pitems = 0;
   int n_su = 0, n_slots = 0;
   struct Tile {
@@ -201,8 +236,9 @@ void plan_batch(const duet_shape* s, const duet_batch* b, int layers, int steps,
     p->prefill_id_cap = std::max(p->prefill_id_cap, (int)((L + 15) / 16));
     for (int t = 0; t * rows < q.q_len; ++t) {
       const int nt = block_tiles(q, t);
-      // Units longer than 1.5 P: n pieces of equal length (the last may be shorter), none empty
-      int pieces = P > 0 && 2 * nt > 3 * P ? (nt + P - 1) / P : 1;
+      int pieces = pieces_of(nt);
+      if (pieces == 1 && std::binary_search(tail_blocks.begin(), tail_blocks.end(), std::make_pair(r, t)))
+        pieces = kPrefillTailPieces;
       const int len = (nt + pieces - 1) / pieces;
       pieces = (nt + len - 1) / len;
       n_pitems += (int64_t)pieces * units;
