@@ -297,8 +297,9 @@ duet_model* duet_ctx_model(duet_ctx* ctx);
  * and batch: an error word, the decode work-queue counters, metadata, work lists, two buffers
  * of decode split-K partials (consecutive layers alternate between them) and the partial states
  * of prefill pieces (bf16: a prefill unit whose causal key range is long against the batch's
- * total runs as several pieces over runs of its keys, merged by the last one to finish; at most
- * 512 pieces write a partial, 128 KiB each at head_dim 128).  The layers of a call share all of
+ * total runs as several pieces over runs of its keys, merged by the last one to finish, and when
+ * a batch has at least 512 whole units its 256 shortest run as 4 pieces each; at most 512 + 1024
+ * pieces write a partial, 128 KiB each at head_dim 128).  The layers of a call share all of
  * it, so the size does not depend on shape->num_layers.  Host only. */
 int duet_workspace_bytes(const duet_shape* shape, const duet_batch* batch, size_t* bytes);
 
