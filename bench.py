@@ -741,6 +741,54 @@ def lookahead_main(args):
     print(json.dumps(line), flush=True)
     ctx.close()
 
+def accuracy_main(args):
+    """The latency model's accuracy per CU count (Appendix A): predicted against measured attention
+    latency of an 8 x 1024-token prefill batch and of a 16-request decode batch at context 1024
+    (Llama-3-8B shapes; 4 layers per call, each with its own KV pool; median of 5 calls) on every
+    share of the 32-CU grid, each batch alone on its share.  The model is calibrated on the generic
+    batches, none of these."""
+    import dataclasses
+    import statistics as st_
+    import torch
+    import paper_2511_04791_amd as duet
+    from paper_2511_04791_amd import workloads as wl
+    from paper_2511_04791_amd.calibration import GRID_SHARES, _times, calibrate_model
+
+    ctx = duet.Context(0)
+    calibrate_model(ctx)
+    L = 4
+    sh1 = dataclasses.replace(wl.LLAMA3_8B, num_layers=1)
+    batches = {"prefill 8 x 1024": (wl.make_batch(wl.LLAMA3_8B, [(0, 1024, 0)] * 8, page_seed=901), 0),
+               "decode 16 x 1024": (wl.make_batch(wl.LLAMA3_8B, [(1, 1, 1023)] * 16, page_seed=902), 1)}
+    out = {}
+    for name, (b, kind) in batches.items():
+        layers = [wl.make_tensors(b, seed=903 + l, device="cuda") for l in range(L)]
+        pt = torch.as_tensor(b.page_table, device="cuda")
+        rows3 = [(int(k_), int(q_), int(c_)) for k_, q_, c_ in zip(b.kinds, b.q_lens, b.cached_lens)]
+        rows = []
+        for cus in GRID_SHARES:
+            if cus == duet.TOTAL_CUS:
+                split = duet.CuSplit.agg()
+            else:
+                split = (duet.CuSplit.split(cus, duet.TOTAL_CUS - cus) if kind == 0 else
+                         duet.CuSplit.split(duet.TOTAL_CUS - cus, cus))
+            meas = st_.median(r["prefill" if kind == 0 else "decode"] for r in _times(ctx, b, layers, pt, split, 5))
+            pred = duet.predict_partition_latency(rows3, kind, cus, sh1, ctx.model, shared=False)
+            rows.append({"cus": cus, "measured_us": round(meas, 1), "predicted_us": round(pred, 1),
+                         "error": round((pred - meas) / meas, 4)})
+            print(f"[accuracy] {name} on {cus} CUs: measured {meas:.1f} us, predicted {pred:.1f} us", file=sys.stderr,
+                  flush=True)
+        errs = [r["error"] for r in rows]
+        out[name] = {"rows": rows, "mean_abs_error": round(st_.fmean(abs(e) for e in errs), 4),
+                     "min_error": min(errs), "max_error": max(errs)}
+        del layers
+    worst = max(v["mean_abs_error"] for v in out.values())
+    print(json.dumps({"metric": "latency model mean |prediction error| per CU share (Appendix A batches)",
+                      "value": worst, "unit": "fraction", "n_gpus": 1, "higher_is_better": False, "dtype": "bf16",
+                      "data": "synthetic", "batches": out}), flush=True)
+    ctx.close()
+
+
 def serve_main(args):
     """The serving loop (Sections 3 and 4): the native engine forms each iteration (continuous
     batching, chunked prefill under an 8192-token budget) from the trace's request stream (Poisson
