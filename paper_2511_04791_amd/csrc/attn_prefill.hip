@@ -300,16 +300,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[nb][v] = 0.f;
-    // The score MFMAs issue at a raised wave priority: a wave that reaches them first keeps the
-    // matrix core while its SIMD partner is still in its softmax, so the two waves of a SIMD drift
-    // out of phase (measured 1-2% faster on long chunks; priority around the PV products was slower).
+    // The score MFMAs and the V fragment reads after them issue at a raised wave priority: a wave
+    // that reaches them first keeps the matrix core while its SIMD partner is still in its
+    // softmax, so the two waves of a SIMD drift out of phase (measured 1-3% faster; priority
+    // around the PV products was slower).
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk)
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
         sacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[nb][kk], qf[kk], sacc[nb], 0, 0, 0);
-    __builtin_amdgcn_s_setprio(0);
   };
 
   for (int kt = kt0; kt < kt1; ++kt) {
@@ -332,6 +332,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_bf16(AttnArgs a, WorkArgs
           vf[n][k2] = *reinterpret_cast<const bf16x8*>(vs + vrow * BN + ch * 8);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       // Only tiles that cross this wave's diagonal need the causal mask.
       if (BN * kt + BN - 1 > w_first_pos) {
 #pragma unroll
