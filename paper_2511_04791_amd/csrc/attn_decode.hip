@@ -130,13 +130,33 @@ __device__ __forceinline__ void merge_pair(const AttnArgs& a, const WorkArgs& w,
   const int i = pair / a.h_q;
   const int h = pair - i * a.h_q;
   const int4 dr = w.dreq[i];
-  const int4 m = w.meta[dr.x];
   const int g = a.group;
   const int j = h / g, col = h - j * g;
   const size_t base = (size_t)(dr.y + j * dr.z) * g + col;  // partial row of split 0
   const int n = dr.z;
-  float M = -INFINITY;
-  for (int s = lane; s < n; s += 64) M = fmaxf(M, pml[(base + (size_t)s * g) * 2]);
+  // Eight partial rows (splits s0 + t0 .. + 7 of the cnt from s0) are loaded before any is used,
+  // so their loads overlap.
+  float part[8][E];
+  auto load_rows = [&](int s0, int t0, int cnt) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = min(t0 + u, cnt - 1);
+      const float* pa = pacc + (base + (size_t)(s0 + t) * g) * D + lane;
+#pragma unroll
+      for (int e = 0; e < E; ++e) part[u][e] = pa[64 * e];
+    }
+  };
+  auto load_ml = [&](int s) {
+    return s < n ? *reinterpret_cast<const float2*>(pml + (base + (size_t)s * g) * 2) : make_float2(-INFINITY, 0.f);
+  };
+  // The first 64 splits' (max, denominator) pairs, the first eight partial rows and the output
+  // row's request metadata are all in flight together: a request of up to eight splits costs one
+  // memory round trip before its arithmetic.
+  float2 ml = load_ml(lane);
+  if (n > 0) load_rows(0, 0, min(64, n));  // every decode request has at least one split
+  const int4 m = w.meta[dr.x];
+  float M = ml.x;
+  for (int s = lane + 64; s < n; s += 64) M = fmaxf(M, pml[(base + (size_t)s * g) * 2]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
   float den = 0.f, num[E];
@@ -144,20 +164,12 @@ __device__ __forceinline__ void merge_pair(const AttnArgs& a, const WorkArgs& w,
   for (int e = 0; e < E; ++e) num[e] = 0.f;
   for (int s0 = 0; s0 < n; s0 += 64) {
     const int s = s0 + lane;
-    const size_t row = base + (size_t)s * g;
-    const float wgt = s < n ? fast_exp2(pml[row * 2] - M) : 0.f;
-    den += s < n ? wgt * pml[row * 2 + 1] : 0.f;
+    if (s0 > 0) ml = load_ml(s);
+    const float wgt = s < n ? fast_exp2(ml.x - M) : 0.f;
+    den += s < n ? wgt * ml.y : 0.f;
     const int cnt = min(64, n - s0);
-    // Eight partial rows are loaded before any is accumulated, so their loads overlap.
     for (int t0 = 0; t0 < cnt; t0 += 8) {
-      float part[8][E];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int t = min(t0 + u, cnt - 1);
-        const float* pa = pacc + (base + (size_t)(s0 + t) * g) * D + lane;
-#pragma unroll
-        for (int e = 0; e < E; ++e) part[u][e] = pa[64 * e];
-      }
+      if (s0 > 0 || t0 > 0) load_rows(s0, t0, cnt);
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const float wt = t0 + u < cnt ? __shfl(wgt, t0 + u) : 0.f;
