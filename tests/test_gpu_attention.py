@@ -118,6 +118,10 @@ RAGGED = [
     ((16, 2, 64, "bf16"), [(1, 1, 5), (0, 300, 0), (1, 1, 1000), (0, 17, 1)]),
     ((4, 4, 128, "bf16"), [(0, 64, 64), (1, 1, 63), (1, 1, 64), (1, 1, 65)]),
     ((8, 2, 128, "f32"), [(0, 37, 11), (1, 1, 0), (1, 1, 47)]),
+    # long decodes: 81, 65 and 9 bf16 splits of 32 pages (the merge's second block of 64 splits, a
+    # lone split past 64, a second group of eight partial rows); over a thousand fp32 splits
+    ((8, 2, 128, "bf16"), [(1, 1, 40999), (0, 20, 5), (1, 1, 33000), (1, 1, 4100)]),
+    ((8, 2, 128, "f32"), [(1, 1, 40999), (1, 1, 4100)]),
 ]
 
 
